@@ -1,0 +1,170 @@
+/*
+ * ls_ffn.h - C ABI of the MI355X (gfx950) sparse-FFN decode library.
+ *
+ * One decode step of the activation-sparse gated FFN of LeanStream's
+ * speculate-and-refine decode (arxiv 2609.03079): a low-rank predictor scores
+ * neuron blocks, the blocks are selected in descending predicted priority,
+ * and only the selected blocks' gate/up/down weights are read and computed.
+ *
+ * Conventions (every entry point):
+ *  - Every call returns ls_status; nothing aborts, throws or exits.
+ *  - Pointers marked "dev" are device pointers (HBM) owned by the caller;
+ *    pointers marked "host" are host pointers.  Weight storage is owned by the
+ *    context.
+ *  - Activations (x, h, scores, y) are fp32; weights are in the context dtype;
+ *    accumulation is fp32.  Row-major ("C") layouts throughout.
+ *  - Compute calls enqueue on the context's stream and return; argument
+ *    validation is synchronous.  A HIP failure makes the context sticky in
+ *    LS_E_DEVICE until ls_ffn_destroy.
+ *  - One host thread per context.  ls_last_error() describes the last failure.
+ *  - Every call that the library accepts for a given context, shape and
+ *    selection computes the same bits on every run (fixed reduction orders,
+ *    no floating-point atomics).
+ */
+#ifndef LS_FFN_H
+#define LS_FFN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ls_ffn ls_ffn; /* opaque context; owns all weight storage */
+
+typedef enum {
+    LS_OK = 0,
+    LS_E_INVAL = 1,       /* bad argument (null pointer, shape, range, cap too small) */
+    LS_E_NOMEM = 2,       /* host or device allocation failed */
+    LS_E_DEVICE = 3,      /* a HIP call failed; sticky until ls_ffn_destroy */
+    LS_E_STATE = 4,       /* call not valid in the context's state (e.g. layer not set) */
+    LS_E_UNSUPPORTED = 5, /* valid request this build does not implement */
+    LS_E_CAPACITY = 6     /* request larger than the HBM block cache */
+} ls_status;
+
+typedef enum { LS_F32 = 0, LS_F16 = 1, LS_BF16 = 2 } ls_dtype;
+
+/* Gating of the gate branch (Eq. 1, Sec. 2.1):
+ *  REGLU:          a_j = max(g_j, 0) * u_j
+ *  SWIGLU_THRESH:  s_j = g_j / (1 + exp(-g_j));  a_j = s_j * u_j if |s_j| > t_l else 0 */
+typedef enum { LS_ACT_REGLU = 0, LS_ACT_SWIGLU_THRESH = 1 } ls_act;
+
+/* Where the FFN blocks live: resident in HBM, or in pinned host memory with a
+ * bounded HBM block cache filled by ls_stream_weights. */
+typedef enum { LS_WEIGHTS_HBM = 0, LS_WEIGHTS_HOST = 1 } ls_residency;
+
+/* Block selection: top-k by score, or every score strictly above tau. */
+typedef enum { LS_SEL_TOPK = 0, LS_SEL_THRESHOLD = 1 } ls_sel_mode;
+
+typedef struct {
+    int32_t n_layers;
+    int32_t d_model;      /* d; multiple of 64 */
+    int32_t d_ff;         /* F; multiple of block */
+    int32_t block;        /* neurons per block; multiple of 8 */
+    int32_t rank;         /* predictor rank r; multiple of 64 */
+    int32_t max_batch;    /* 1..8 tokens per call */
+    ls_dtype dtype;       /* weight storage type */
+    ls_act act;
+    ls_residency residency;
+    int32_t prenorm_rms;  /* 0: h = x;  1: h = x / sqrt(mean(x^2) + 1e-6) */
+    uint64_t hbm_cache_bytes; /* LS_WEIGHTS_HOST only: HBM block-cache budget */
+    void* stream;         /* hipStream_t borrowed for all compute (NULL: the null stream);
+                             must outlive the context */
+    uint32_t debug_flags; /* reserved, 0 */
+} ls_ffn_desc;
+
+/* One layer's weights, host pointers in the context dtype, nn.Linear layouts.
+ * Copied by ls_ffn_set_layer; the caller may free them afterwards. */
+typedef struct {
+    const void* w_gate; /* [F, d] */
+    const void* w_up;   /* [F, d] */
+    const void* w_down; /* [d, F] (nn.Linear down_proj.weight) */
+    const void* b_gate; /* [F] or NULL (gate-branch bias) */
+    const void* p1;     /* [r, d]      predictor input projection (Sec. 3.3.3) */
+    const void* p2;     /* [n_blk, r]  predictor head scoring neuron blocks */
+    float threshold;    /* t_l of LS_ACT_SWIGLU_THRESH; ignored for ReGLU */
+} ls_layer_weights;
+
+typedef struct {
+    int64_t hits;       /* requested blocks already in the HBM cache */
+    int64_t misses;     /* requested blocks copied host -> HBM */
+    int64_t bytes;      /* bytes copied host -> HBM by this call */
+    int64_t evictions;  /* cache slots reassigned by this call */
+} ls_stream_stats;
+
+/* Create a context on the current HIP device.  Allocates the weight arena
+ * (HBM, or pinned host + HBM cache) and the workspaces.
+ * LS_E_INVAL on a bad descriptor; LS_E_NOMEM if an allocation fails. */
+ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out);
+
+/* Copy one layer's weights (host, nn.Linear layouts) into the context's own
+ * layout: per block of `block` neurons one contiguous chunk
+ * [gate rows | up rows | down columns], which serves coalesced 128-bit loads
+ * and one copy per block (Sec. 3.2.2: blocks appended in arrival order form a
+ * contiguous buffer).  Synchronous.  LS_E_INVAL on null pointers or layer out
+ * of range. */
+ls_status ls_ffn_set_layer(ls_ffn* ctx, int32_t layer, const ls_layer_weights* w);
+
+/* Release everything the context owns.  Synchronises the stream. */
+ls_status ls_ffn_destroy(ls_ffn* ctx);
+
+/* Predictor (Sec. 3.3.3): h = prenorm(x); z = P1 h; scores = P2 z.
+ * x: dev fp32 [B, d]; scores: dev fp32 [B, n_blk].  1 <= B <= max_batch. */
+ls_status ls_predict(ls_ffn* ctx, int32_t layer, const float* x, int32_t B, float* scores);
+
+/* Block selection over dev fp32 scores [B, n_blk] (priority list, Sec. 2.1).
+ * Total order: a before b iff key(a) > key(b), or keys equal and a < b, where
+ * key puts NaN below every number, treats -0 == +0, and is IEEE order
+ * otherwise.  TOPK: the first k entries.  THRESHOLD: every non-NaN score > tau,
+ * in the same order.  union_batch != 0 and B > 1: the union of the tokens'
+ * selections, ordered by the largest key over all B tokens, then by index.
+ * Output, dev int32: per token idx [B, cap], count [B]; union idx [cap], count [1].
+ * cap must be >= k (TOPK), >= min(n_blk, B*k) (TOPK union) or >= n_blk
+ * (THRESHOLD); 1 <= k <= n_blk for TOPK.  LS_E_INVAL otherwise. */
+ls_status ls_select_blocks(ls_ffn* ctx, const float* scores, int32_t B, ls_sel_mode mode,
+                           int32_t k, float tau, int32_t union_batch, int32_t cap, int32_t* idx,
+                           int32_t* count);
+
+/* Sparse FFN over entries [begin, min(end, *count)) of the priority list idx
+ * (dev int32, one list shared by all B tokens) for layer `layer`:
+ *   h = prenorm(x_in);  for every neuron j of those blocks:
+ *   g_j = Wg[j,:] h + b_j, u_j = Wu[j,:] h, a_j = gate(g_j, u_j)   (Eq. 1)
+ *   y = sum_j a_j Wd[:, j]                                          (Sec. 3.2.2)
+ *   begin == 0: x_acc = x_in + y;   begin > 0: x_acc += y            (Eq. 2)
+ * so after the stages [0,e1), [e1,e2), ... x_acc holds the refined feature
+ * x_tilde of Eq. 2.  x_in, x_acc: dev fp32 [B, d], must not alias.
+ * count: dev int32 [1].  0 <= begin <= end.  Every idx entry in range must be a
+ * valid block id (not checked on the device). */
+ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int32_t B,
+                             const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
+                             float* x_acc);
+
+/* LS_WEIGHTS_HOST: make blocks idx_host[0..n) of `layer` resident in the HBM
+ * cache, copying misses from pinned host memory in priority order on a copy
+ * stream, in n_stages equal contiguous stages; the following
+ * ls_sparse_ffn_step calls of this layer wait for the stages they read.  No
+ * block of this request is evicted to make room for another of it.
+ * LS_WEIGHTS_HBM: no copy, all hits.  LS_E_CAPACITY if n exceeds the cache
+ * slots.  stats may be NULL. */
+ls_status ls_stream_weights(ls_ffn* ctx, int32_t layer, const int32_t* idx_host, int32_t n,
+                            int32_t n_stages, ls_stream_stats* stats);
+
+/* One decode step over every layer: for l in 0..L-1:
+ *   scores = predict(l, x); idx = topk(scores, k) (union over the B tokens if B > 1);
+ *   x = x + sparse_ffn(l, x, idx[0..count)).
+ * x: dev fp32 [B, d], updated in place.  Equal to composing the calls above. */
+ls_status ls_decode_step(ls_ffn* ctx, float* x, int32_t B, int32_t k);
+
+/* Debug: copy the activations a [B, n_sel * block] (fp32, priority-list order)
+ * of the most recent ls_sparse_ffn_step into dst (dev).  LS_E_INVAL if cap is
+ * smaller than what the last step produced; *n_out receives n_sel * block. */
+ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_t* n_out);
+
+/* Text of the last failure on ctx (or of the last failed ls_ffn_create when
+ * ctx is NULL); valid until the next call on ctx. */
+const char* ls_last_error(const ls_ffn* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LS_FFN_H */

@@ -1,0 +1,173 @@
+"""Python binding of the gfx950 sparse-FFN decode library (``liblsffn.so``).
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels behind the C ABI of ``include/ls_ffn.h``.  Function names mirror the C
+entry points.  PyTorch supplies device memory and the stream.
+
+The library is loaded from this package directory.  There is no fallback: if
+it has not been built, every call raises ``RuntimeError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblsffn.so")
+
+LS_OK, LS_E_INVAL, LS_E_NOMEM, LS_E_DEVICE, LS_E_STATE, LS_E_UNSUPPORTED, LS_E_CAPACITY = range(7)
+STATUS_NAMES = {0: "LS_OK", 1: "LS_E_INVAL", 2: "LS_E_NOMEM", 3: "LS_E_DEVICE", 4: "LS_E_STATE",
+                5: "LS_E_UNSUPPORTED", 6: "LS_E_CAPACITY"}
+LS_F32, LS_F16, LS_BF16 = 0, 1, 2
+LS_ACT_REGLU, LS_ACT_SWIGLU_THRESH = 0, 1
+LS_WEIGHTS_HBM, LS_WEIGHTS_HOST = 0, 1
+LS_SEL_TOPK, LS_SEL_THRESHOLD = 0, 1
+
+EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", "ls_select_blocks",
+           "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step",
+           "ls_debug_last_activations", "ls_last_error")
+
+
+class LsFfnDesc(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("d_ff", ctypes.c_int32), ("block", ctypes.c_int32), ("rank", ctypes.c_int32),
+                ("max_batch", ctypes.c_int32), ("dtype", ctypes.c_int), ("act", ctypes.c_int),
+                ("residency", ctypes.c_int), ("prenorm_rms", ctypes.c_int32),
+                ("hbm_cache_bytes", ctypes.c_uint64), ("stream", ctypes.c_void_p),
+                ("debug_flags", ctypes.c_uint32)]
+
+
+class LsLayerWeights(ctypes.Structure):
+    _fields_ = [("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p),
+                ("w_down", ctypes.c_void_p), ("b_gate", ctypes.c_void_p),
+                ("p1", ctypes.c_void_p), ("p2", ctypes.c_void_p), ("threshold", ctypes.c_float)]
+
+
+class LsStreamStats(ctypes.Structure):
+    _fields_ = [("hits", ctypes.c_int64), ("misses", ctypes.c_int64), ("bytes", ctypes.c_int64),
+                ("evictions", ctypes.c_int64)]
+
+
+class LsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load():
+    """Load ``liblsffn.so`` (no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library not built: {LIB_PATH} is missing (run __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.ls_ffn_create.argtypes = [ctypes.POINTER(LsFfnDesc), ctypes.POINTER(ctypes.c_void_p)]
+    lib.ls_ffn_set_layer.argtypes = [P, I32, ctypes.POINTER(LsLayerWeights)]
+    lib.ls_ffn_destroy.argtypes = [P]
+    lib.ls_predict.argtypes = [P, I32, P, I32, P]
+    lib.ls_select_blocks.argtypes = [P, P, I32, ctypes.c_int, I32, ctypes.c_float, I32, I32, P, P]
+    lib.ls_sparse_ffn_step.argtypes = [P, I32, P, I32, P, P, I32, I32, P]
+    lib.ls_stream_weights.argtypes = [P, I32, P, I32, I32, ctypes.POINTER(LsStreamStats)]
+    lib.ls_decode_step.argtypes = [P, P, I32, I32]
+    lib.ls_debug_last_activations.argtypes = [P, P, I64, ctypes.POINTER(I64)]
+    lib.ls_last_error.argtypes = [P]
+    lib.ls_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS[:-1]:
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(lib, ctx, status: int):
+    if status != LS_OK:
+        msg = lib.ls_last_error(ctx)
+        raise LsError(status, msg.decode() if msg else "")
+
+
+def _ptr(t) -> int | None:
+    """Device pointer of a torch tensor (or None)."""
+    return None if t is None else t.data_ptr()
+
+
+def _host_ptr(a):
+    return None if a is None else np.ascontiguousarray(a).ctypes.data
+
+
+class Ffn:
+    """One library context.  Methods mirror the C entry points one to one."""
+
+    def __init__(self, *, n_layers, d_model, d_ff, block, rank, max_batch=1, dtype=LS_F16,
+                 act=LS_ACT_REGLU, residency=LS_WEIGHTS_HBM, prenorm_rms=1, hbm_cache_bytes=0,
+                 stream=None):
+        self.lib = load()
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.torch_stream = stream
+        desc = LsFfnDesc(n_layers, d_model, d_ff, block, rank, max_batch, dtype, act, residency,
+                         prenorm_rms, hbm_cache_bytes, ctypes.c_void_p(stream.cuda_stream), 0)
+        h = ctypes.c_void_p()
+        st = self.lib.ls_ffn_create(ctypes.byref(desc), ctypes.byref(h))
+        _check(self.lib, None, st)
+        self.ctx = h
+        self.n_layers, self.d_model, self.d_ff, self.block, self.rank = (n_layers, d_model, d_ff,
+                                                                          block, rank)
+        self.n_blk = d_ff // block
+        self.max_batch = max_batch
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.lib.ls_ffn_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def ls_ffn_set_layer(self, layer: int, w) -> None:
+        """w: object with gate, up, down, bias, p1, p2 (host arrays in storage type), threshold."""
+        arrs = [np.ascontiguousarray(a) if a is not None else None
+                for a in (w.gate, w.up, w.down, w.bias, w.p1, w.p2)]
+        lw = LsLayerWeights(*[_host_ptr(a) for a in arrs], float(getattr(w, "threshold", 0.0)))
+        _check(self.lib, self.ctx, self.lib.ls_ffn_set_layer(self.ctx, layer, ctypes.byref(lw)))
+
+    def ls_predict(self, layer: int, x, B: int, scores) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_predict(self.ctx, layer, _ptr(x), B, _ptr(scores)))
+
+    def ls_select_blocks(self, scores, B: int, mode: int, k: int, tau: float, union_batch: int,
+                         cap: int, idx, count) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_select_blocks(self.ctx, _ptr(scores), B, mode, k, tau,
+                                                             union_batch, cap, _ptr(idx),
+                                                             _ptr(count)))
+
+    def ls_sparse_ffn_step(self, layer: int, x_in, B: int, idx, count, begin: int, end: int,
+                           x_acc) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_sparse_ffn_step(self.ctx, layer, _ptr(x_in), B,
+                                                               _ptr(idx), _ptr(count), begin, end,
+                                                               _ptr(x_acc)))
+
+    def ls_stream_weights(self, layer: int, idx_host, n_stages: int = 1) -> LsStreamStats:
+        a = np.ascontiguousarray(idx_host, dtype=np.int32)
+        stats = LsStreamStats()
+        _check(self.lib, self.ctx, self.lib.ls_stream_weights(self.ctx, layer, a.ctypes.data,
+                                                              int(a.size), n_stages,
+                                                              ctypes.byref(stats)))
+        return stats
+
+    def ls_decode_step(self, x, B: int, k: int) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_decode_step(self.ctx, _ptr(x), B, k))
+
+    def ls_debug_last_activations(self, dst) -> int:
+        n = ctypes.c_int64()
+        _check(self.lib, self.ctx, self.lib.ls_debug_last_activations(self.ctx, _ptr(dst),
+                                                                      dst.numel(), ctypes.byref(n)))
+        return n.value

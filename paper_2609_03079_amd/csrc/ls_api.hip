@@ -1,0 +1,535 @@
+// ls_api.hip - host engine behind the C ABI of include/ls_ffn.h.
+//
+// Owns the per-layer weight arenas in the library's block layout, the
+// workspaces of the decode step and the stream bookkeeping; validates every
+// argument before anything is enqueued.
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <thread>
+
+#include "block_cache.h"
+#include "ls_internal.h"
+
+using ls::Shape;
+
+struct ls_ffn {
+    ls_ffn_desc desc{};
+    Shape shape{};
+    int device = 0;
+    hipStream_t stream = nullptr;
+    hipStream_t copy_stream = nullptr;
+    size_t block_bytes = 0;
+    size_t layer_bytes = 0;  // blocks + bias + p1 + p2 (resident arena of one layer)
+
+    // per layer
+    std::vector<uint8_t*> arena;  // device: [blocks][bias][p1][p2]  (resident mode)
+    std::vector<ls::LayerDev> dev;
+    std::vector<uint8_t> is_set;
+
+    // workspaces (device)
+    float* h = nullptr;       // [maxB, d]
+    float* z = nullptr;       // [maxB, r]
+    float* scores = nullptr;  // [maxB, n_blk]
+    int32_t* idx = nullptr;   // [maxB, n_blk]
+    int32_t* count = nullptr; // [maxB]
+    float* a = nullptr;       // [maxB, F]
+    float* xbuf = nullptr;    // [maxB, d]  ping-pong partner of the decode step
+    int64_t last_act_n = 0;
+    int32_t last_act_B = 0;
+
+    // staging for set_layer (pinned host)
+    uint8_t* staging = nullptr;
+    size_t staging_bytes = 0;
+
+    // host-resident weights (LS_WEIGHTS_HOST)
+    uint8_t* host_blocks = nullptr;  // pinned, [L][n_blk][block_bytes]
+    uint8_t* cache = nullptr;        // device, [slots][block_bytes]
+    int32_t* slot_tables = nullptr;  // device, [L][n_blk]
+    int32_t* slot_tables_host = nullptr;  // pinned mirror
+    ls::BlockCache* bcache = nullptr;
+    std::vector<hipEvent_t> stage_events;
+    std::vector<std::pair<int, int>> stage_ranges;  // [begin,end) of each pending stage
+    int pending_layer = -1;
+    hipEvent_t compute_done = nullptr;
+
+    std::vector<hipEvent_t> table_uploaded;  // per layer: last slot-table upload
+
+    ls_status sticky = LS_OK;
+    std::string err;
+};
+
+namespace {
+
+std::string g_create_error;
+
+ls_status fail(ls_ffn* c, ls_status st, const std::string& msg) {
+    if (c) {
+        c->err = msg;
+        if (st == LS_E_DEVICE) c->sticky = LS_E_DEVICE;
+    } else {
+        g_create_error = msg;
+    }
+    return st;
+}
+
+ls_status hip_fail(ls_ffn* c, hipError_t e, const char* what) {
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    if (c) return fail(c, LS_E_DEVICE, m);
+    g_create_error = m;
+    return LS_E_DEVICE;
+}
+
+#define LS_HIP(ctx, call)                                   \
+    do {                                                    \
+        hipError_t e_ = (call);                             \
+        if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
+    } while (0)
+
+ls_status check_ctx(ls_ffn* c) {
+    if (!c) return LS_E_INVAL;
+    if (c->sticky != LS_OK) {
+        c->err = "context is in a failed state after an earlier device error";
+        return c->sticky;
+    }
+    return LS_OK;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Offsets inside one layer arena.
+struct LayerLayout {
+    size_t blocks, bias, p1, p2, total;
+};
+
+LayerLayout layout_of(const Shape& s, size_t block_bytes) {
+    const size_t es = ls::elem_size(s.dtype);
+    LayerLayout L{};
+    L.blocks = 0;
+    L.bias = align_up((size_t)s.n_blk * block_bytes, 256);
+    L.p1 = align_up(L.bias + (size_t)s.F * es, 256);
+    L.p2 = align_up(L.p1 + (size_t)s.r * s.d * es, 256);
+    L.total = align_up(L.p2 + (size_t)s.n_blk * s.r * es, 256);
+    return L;
+}
+
+// Convert one layer's FFN weights from nn.Linear layouts into the block layout:
+// block b = [gate rows b*blk.. (blk x d) | up rows (blk x d) | down piece], where the
+// down piece is [d/16][blk/V][16][V]: element (neuron q, column m) of the block sits at
+// ((m/16) * (blk/V) + q/V) * 16*V + (m%16) * V + q%V.
+void convert_blocks(const Shape& s, const uint8_t* gate, const uint8_t* up, const uint8_t* down,
+                    uint8_t* dst, size_t block_bytes) {
+    const size_t es = ls::elem_size(s.dtype);
+    const int V = ls::vec_elems(s.dtype);
+    const size_t rows_bytes = (size_t)s.blk * s.d * es;
+    unsigned nth = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+    auto work = [&](unsigned t) {
+        for (int b = (int)t; b < s.n_blk; b += (int)nth) {
+            uint8_t* blk = dst + (size_t)b * block_bytes;
+            std::memcpy(blk, gate + (size_t)b * rows_bytes, rows_bytes);
+            std::memcpy(blk + rows_bytes, up + (size_t)b * rows_bytes, rows_bytes);
+            uint8_t* dn = blk + 2 * rows_bytes;
+            for (int m = 0; m < s.d; ++m) {
+                const uint8_t* src_row = down + ((size_t)m * s.F + (size_t)b * s.blk) * es;
+                const size_t tile_base = (size_t)(m / ls::kColTile) * (s.blk / V);
+                const size_t col = m % ls::kColTile;
+                for (int q = 0; q < s.blk; ++q) {
+                    const size_t pos = ((tile_base + q / V) * ls::kColTile + col) * V + q % V;
+                    std::memcpy(dn + pos * es, src_row + (size_t)q * es, es);
+                }
+            }
+        }
+    };
+    std::vector<std::thread> th;
+    for (unsigned t = 1; t < nth; ++t) th.emplace_back(work, t);
+    work(0);
+    for (auto& x : th) x.join();
+}
+
+ls_status validate_desc(const ls_ffn_desc* d) {
+    if (!d) return fail(nullptr, LS_E_INVAL, "desc is NULL");
+    if (d->n_layers < 1) return fail(nullptr, LS_E_INVAL, "n_layers must be >= 1");
+    if (d->d_model < 64 || d->d_model % 64) return fail(nullptr, LS_E_INVAL, "d_model must be a positive multiple of 64");
+    if (d->block < 8 || d->block % 8) return fail(nullptr, LS_E_INVAL, "block must be a positive multiple of 8");
+    if (d->d_ff < d->block || d->d_ff % d->block) return fail(nullptr, LS_E_INVAL, "d_ff must be a positive multiple of block");
+    if (d->d_ff / d->block > ls::kMaxBlocks) return fail(nullptr, LS_E_INVAL, "d_ff / block exceeds 2048 blocks");
+    if (d->rank < 64 || d->rank % 64) return fail(nullptr, LS_E_INVAL, "rank must be a positive multiple of 64");
+    if (d->max_batch < 1 || d->max_batch > ls::kMaxBatch) return fail(nullptr, LS_E_INVAL, "max_batch must be in 1..8");
+    if (d->dtype != LS_F32 && d->dtype != LS_F16 && d->dtype != LS_BF16) return fail(nullptr, LS_E_INVAL, "bad dtype");
+    if (d->act != LS_ACT_REGLU && d->act != LS_ACT_SWIGLU_THRESH) return fail(nullptr, LS_E_INVAL, "bad act");
+    if (d->residency != LS_WEIGHTS_HBM && d->residency != LS_WEIGHTS_HOST) return fail(nullptr, LS_E_INVAL, "bad residency");
+    if (d->prenorm_rms != 0 && d->prenorm_rms != 1) return fail(nullptr, LS_E_INVAL, "prenorm_rms must be 0 or 1");
+    if (d->debug_flags != 0) return fail(nullptr, LS_E_INVAL, "debug_flags must be 0");
+    return LS_OK;
+}
+
+void free_all(ls_ffn* c) {
+    for (auto p : c->arena) if (p) (void)hipFree(p);
+    c->arena.clear();
+    for (void* p : {(void*)c->h, (void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
+                    (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables})
+        if (p) (void)hipFree(p);
+    if (c->staging) (void)hipHostFree(c->staging);
+    if (c->host_blocks) (void)hipHostFree(c->host_blocks);
+    if (c->slot_tables_host) (void)hipHostFree(c->slot_tables_host);
+    for (auto e : c->stage_events) (void)hipEventDestroy(e);
+    if (c->compute_done) (void)hipEventDestroy(c->compute_done);
+    if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
+    for (auto e : c->table_uploaded) if (e) (void)hipEventDestroy(e);
+    delete c->bcache;
+}
+
+template <typename T>
+hipError_t dmalloc(T** p, size_t n) {
+    return hipMalloc(reinterpret_cast<void**>(p), std::max<size_t>(n, 1) * sizeof(T));
+}
+
+}  // namespace
+
+extern "C" {
+
+ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
+    if (!out) return fail(nullptr, LS_E_INVAL, "out is NULL");
+    *out = nullptr;
+    ls_status st = validate_desc(desc);
+    if (st != LS_OK) return st;
+    ls_ffn* c = new (std::nothrow) ls_ffn();
+    if (!c) return fail(nullptr, LS_E_NOMEM, "host allocation failed");
+    c->desc = *desc;
+    Shape& s = c->shape;
+    s.d = desc->d_model;
+    s.F = desc->d_ff;
+    s.blk = desc->block;
+    s.r = desc->rank;
+    s.n_blk = desc->d_ff / desc->block;
+    s.dtype = desc->dtype;
+    s.act = desc->act;
+    s.prenorm = desc->prenorm_rms;
+    s.block_elems = (size_t)3 * s.blk * s.d;
+    c->block_bytes = s.block_elems * ls::elem_size(s.dtype);
+    c->stream = static_cast<hipStream_t>(desc->stream);
+    const int L = desc->n_layers, B = desc->max_batch;
+    auto bail = [&](ls_status code, const std::string& m) {
+        free_all(c);
+        delete c;
+        return fail(nullptr, code, m);
+    };
+    if (hipGetDevice(&c->device) != hipSuccess) return bail(LS_E_DEVICE, "no HIP device");
+    const LayerLayout lay = layout_of(s, c->block_bytes);
+    c->dev.resize(L);
+    c->is_set.assign(L, 0);
+    c->arena.assign(L, nullptr);
+    if (desc->residency == LS_WEIGHTS_HBM) {
+        c->layer_bytes = lay.total;
+        for (int l = 0; l < L; ++l) {
+            if (hipMalloc(reinterpret_cast<void**>(&c->arena[l]), lay.total) != hipSuccess) {
+                (void)hipGetLastError();
+                return bail(LS_E_NOMEM, "device allocation of the weight arena failed");
+            }
+            c->dev[l].blocks = c->arena[l] + lay.blocks;
+            c->dev[l].bias = c->arena[l] + lay.bias;
+            c->dev[l].p1 = c->arena[l] + lay.p1;
+            c->dev[l].p2 = c->arena[l] + lay.p2;
+        }
+    } else {
+        // predictors and bias stay resident in HBM; the blocks live in pinned host memory and
+        // are streamed into a bounded HBM cache.
+        const size_t small = lay.total - lay.bias;
+        c->layer_bytes = small;
+        const int64_t slots = (int64_t)(desc->hbm_cache_bytes / c->block_bytes);
+        if (slots < 1) return bail(LS_E_INVAL, "hbm_cache_bytes holds no block");
+        for (int l = 0; l < L; ++l) {
+            if (hipMalloc(reinterpret_cast<void**>(&c->arena[l]), small) != hipSuccess) {
+                (void)hipGetLastError();
+                return bail(LS_E_NOMEM, "device allocation of the predictor arena failed");
+            }
+            c->dev[l].bias = c->arena[l];
+            c->dev[l].p1 = c->arena[l] + (lay.p1 - lay.bias);
+            c->dev[l].p2 = c->arena[l] + (lay.p2 - lay.bias);
+        }
+        const size_t host_bytes = (size_t)L * s.n_blk * c->block_bytes;
+        if (hipHostMalloc(reinterpret_cast<void**>(&c->host_blocks), host_bytes, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(LS_E_NOMEM, "pinned host allocation of the weight arena failed");
+        }
+        if (hipMalloc(reinterpret_cast<void**>(&c->cache), (size_t)slots * c->block_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(LS_E_NOMEM, "device allocation of the block cache failed");
+        }
+        if (dmalloc(&c->slot_tables, (size_t)L * s.n_blk) != hipSuccess ||
+            hipHostMalloc(reinterpret_cast<void**>(&c->slot_tables_host), (size_t)L * s.n_blk * sizeof(int32_t),
+                          hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(LS_E_NOMEM, "slot table allocation failed");
+        }
+        for (size_t i = 0; i < (size_t)L * s.n_blk; ++i) c->slot_tables_host[i] = -1;
+        if (hipMemcpy(c->slot_tables, c->slot_tables_host, (size_t)L * s.n_blk * sizeof(int32_t),
+                      hipMemcpyHostToDevice) != hipSuccess)
+            return bail(LS_E_DEVICE, "slot table upload failed");
+        c->bcache = new (std::nothrow) ls::BlockCache(slots, L, s.n_blk);
+        if (!c->bcache) return bail(LS_E_NOMEM, "host allocation failed");
+        if (hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&c->compute_done, hipEventDisableTiming) != hipSuccess)
+            return bail(LS_E_DEVICE, "stream/event creation failed");
+        c->table_uploaded.assign(L, nullptr);
+        for (int l = 0; l < L; ++l)
+            if (hipEventCreateWithFlags(&c->table_uploaded[l], hipEventDisableTiming) != hipSuccess)
+                return bail(LS_E_DEVICE, "event creation failed");
+    }
+    if (dmalloc(&c->h, (size_t)B * s.d) != hipSuccess || dmalloc(&c->z, (size_t)B * s.r) != hipSuccess ||
+        dmalloc(&c->scores, (size_t)B * s.n_blk) != hipSuccess ||
+        dmalloc(&c->idx, (size_t)B * s.n_blk) != hipSuccess || dmalloc(&c->count, (size_t)B) != hipSuccess ||
+        dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess) {
+        (void)hipGetLastError();
+        return bail(LS_E_NOMEM, "workspace allocation failed");
+    }
+    *out = c;
+    return LS_OK;
+}
+
+ls_status ls_ffn_destroy(ls_ffn* c) {
+    if (!c) return LS_E_INVAL;
+    (void)hipStreamSynchronize(c->stream);
+    if (c->copy_stream) (void)hipStreamSynchronize(c->copy_stream);
+    free_all(c);
+    delete c;
+    return LS_OK;
+}
+
+const char* ls_last_error(const ls_ffn* c) { return c ? c->err.c_str() : g_create_error.c_str(); }
+
+ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!w || !w->w_gate || !w->w_up || !w->w_down || !w->p1 || !w->p2)
+        return fail(c, LS_E_INVAL, "null weight pointer");
+    const size_t es = ls::elem_size(s.dtype);
+    const LayerLayout lay = layout_of(s, c->block_bytes);
+    const size_t need = c->desc.residency == LS_WEIGHTS_HBM ? lay.total : lay.total - lay.bias;
+    if (!c->staging || c->staging_bytes < need) {
+        if (c->staging) (void)hipHostFree(c->staging);
+        c->staging = nullptr;
+        if (hipHostMalloc(reinterpret_cast<void**>(&c->staging), need, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            c->staging_bytes = 0;
+            return fail(c, LS_E_NOMEM, "pinned staging allocation failed");
+        }
+        c->staging_bytes = need;
+    }
+    LS_HIP(c, hipStreamSynchronize(c->stream));  // staging may still feed an earlier copy
+    uint8_t* blocks_dst;
+    size_t off_small;
+    if (c->desc.residency == LS_WEIGHTS_HBM) {
+        blocks_dst = c->staging;
+        off_small = lay.bias;
+    } else {
+        blocks_dst = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+        off_small = 0;
+    }
+    convert_blocks(s, static_cast<const uint8_t*>(w->w_gate), static_cast<const uint8_t*>(w->w_up),
+                   static_cast<const uint8_t*>(w->w_down), blocks_dst, c->block_bytes);
+    uint8_t* sm = c->staging + off_small;
+    std::memset(sm, 0, lay.p1 - lay.bias);
+    if (w->b_gate) std::memcpy(sm, w->b_gate, (size_t)s.F * es);
+    std::memcpy(sm + (lay.p1 - lay.bias), w->p1, (size_t)s.r * s.d * es);
+    std::memcpy(sm + (lay.p2 - lay.bias), w->p2, (size_t)s.n_blk * s.r * es);
+    LS_HIP(c, hipMemcpyAsync(c->arena[layer], c->staging, need, hipMemcpyHostToDevice, c->stream));
+    LS_HIP(c, hipStreamSynchronize(c->stream));
+    c->dev[layer].bias =
+        w->b_gate ? c->arena[layer] + (c->desc.residency == LS_WEIGHTS_HBM ? lay.bias : 0) : nullptr;
+    c->dev[layer].threshold = w->threshold;
+    if (c->desc.residency == LS_WEIGHTS_HOST) c->bcache->invalidate_layer(layer);
+    c->is_set[layer] = 1;
+    return LS_OK;
+}
+
+ls_status ls_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, float* scores) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!x || !scores) return fail(c, LS_E_INVAL, "null pointer");
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
+    const Shape& s = c->shape;
+    LS_HIP(c, ls::launch_prenorm(s, x, B, c->h, c->stream));
+    LS_HIP(c, ls::launch_gemv_rows(s.dtype, c->dev[layer].p1, s.r, s.d, c->h, B, c->z, c->stream));
+    LS_HIP(c, ls::launch_gemv_rows(s.dtype, c->dev[layer].p2, s.n_blk, s.r, c->z, B, scores, c->stream));
+    return LS_OK;
+}
+
+ls_status ls_select_blocks(ls_ffn* c, const float* scores, int32_t B, ls_sel_mode mode, int32_t k,
+                           float tau, int32_t union_batch, int32_t cap, int32_t* idx, int32_t* count) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const int n = c->shape.n_blk;
+    if (!scores || !idx || !count) return fail(c, LS_E_INVAL, "null pointer");
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    if (mode != LS_SEL_TOPK && mode != LS_SEL_THRESHOLD) return fail(c, LS_E_INVAL, "bad selection mode");
+    const bool uni = union_batch && B > 1;
+    if (mode == LS_SEL_TOPK) {
+        if (k < 1 || k > n) return fail(c, LS_E_INVAL, "k must be in 1..n_blk");
+        const int need = uni ? std::min(n, B * k) : k;
+        if (cap < need) return fail(c, LS_E_INVAL, "cap too small for the selection");
+    } else if (cap < n) {
+        return fail(c, LS_E_INVAL, "threshold selection needs cap >= n_blk");
+    }
+    LS_HIP(c, ls::launch_select(scores, B, n, (int)mode, k, tau, union_batch ? 1 : 0, cap, idx, count,
+                                c->stream));
+    return LS_OK;
+}
+
+// Waits of the compute stream for the copy stages of a streamed layer that overlap [begin,end).
+static ls_status wait_stages(ls_ffn* c, int32_t layer, int32_t begin, int32_t end) {
+    if (c->desc.residency != LS_WEIGHTS_HOST || c->pending_layer != layer) return LS_OK;
+    for (size_t s = 0; s < c->stage_ranges.size(); ++s) {
+        const auto r = c->stage_ranges[s];
+        if (r.first < end && begin < r.second)
+            LS_HIP(c, hipStreamWaitEvent(c->stream, c->stage_events[s], 0));
+    }
+    return LS_OK;
+}
+
+ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_t B,
+                             const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
+                             float* x_acc) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!x_in || !idx || !count || !x_acc) return fail(c, LS_E_INVAL, "null pointer");
+    if (x_in == x_acc) return fail(c, LS_E_INVAL, "x_in and x_acc must not alias");
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    if (begin < 0 || end < begin) return fail(c, LS_E_INVAL, "need 0 <= begin <= end");
+    if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
+    end = std::min(end, s.n_blk);
+    begin = std::min(begin, end);
+    ls::LayerDev L = c->dev[layer];
+    const int32_t* slot_table = nullptr;
+    if (c->desc.residency == LS_WEIGHTS_HOST) {
+        if (c->pending_layer != layer)
+            return fail(c, LS_E_STATE, "blocks of this layer were not streamed (ls_stream_weights)");
+        L.blocks = c->cache;
+        slot_table = c->slot_tables + (size_t)layer * s.n_blk;
+        st = wait_stages(c, layer, begin, end);
+        if (st != LS_OK) return st;
+    }
+    LS_HIP(c, ls::launch_prenorm(s, x_in, B, c->h, c->stream));
+    LS_HIP(c, ls::launch_gateup(s, L, slot_table, c->h, B, idx, count, begin, end, c->a, c->stream));
+    LS_HIP(c, ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream));
+    if (c->desc.residency == LS_WEIGHTS_HOST) LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
+    c->last_act_n = (int64_t)end * s.blk;
+    c->last_act_B = B;
+    return LS_OK;
+}
+
+ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t* n_out) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (!dst || !n_out) return fail(c, LS_E_INVAL, "null pointer");
+    const int64_t n = c->last_act_n;
+    *n_out = n;
+    if (cap < (int64_t)c->last_act_B * n) return fail(c, LS_E_INVAL, "cap too small");
+    for (int b = 0; b < c->last_act_B; ++b)
+        LS_HIP(c, hipMemcpyAsync(dst + (size_t)b * n, c->a + (size_t)b * c->shape.F, (size_t)n * sizeof(float),
+                                 hipMemcpyDeviceToDevice, c->stream));
+    return LS_OK;
+}
+
+ls_status ls_stream_weights(ls_ffn* c, int32_t layer, const int32_t* idx_host, int32_t n,
+                            int32_t n_stages, ls_stream_stats* stats) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (n < 0 || (n > 0 && !idx_host)) return fail(c, LS_E_INVAL, "bad idx_host / n");
+    if (n_stages < 1) return fail(c, LS_E_INVAL, "n_stages must be >= 1");
+    for (int i = 0; i < n; ++i)
+        if (idx_host[i] < 0 || idx_host[i] >= s.n_blk) return fail(c, LS_E_INVAL, "block id out of range");
+    if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
+    ls_stream_stats local{};
+    if (c->desc.residency == LS_WEIGHTS_HBM) {
+        local.hits = n;
+        if (stats) *stats = local;
+        return LS_OK;
+    }
+    if (n > c->bcache->slots()) return fail(c, LS_E_CAPACITY, "request exceeds the HBM cache slots");
+    // Slots reassigned by this call may still be read by compute enqueued earlier: the copy
+    // stream first waits for all compute enqueued so far.
+    LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
+    LS_HIP(c, hipStreamWaitEvent(c->copy_stream, c->compute_done, 0));
+    std::vector<ls::BlockCache::Fill> fills;
+    ls::BlockCache::Result res = c->bcache->request(layer, idx_host, n, &fills);
+    if (!res.ok) return fail(c, LS_E_CAPACITY, "cache could not place the request");
+    int32_t* tab = c->slot_tables_host + (size_t)layer * s.n_blk;
+    // the pinned table of this layer may still feed its previous upload
+    LS_HIP(c, hipEventSynchronize(c->table_uploaded[layer]));
+    c->bcache->slot_table(layer, tab);
+    // table upload first: it only changes entries of blocks filled below, which no earlier
+    // compute of this layer reads any more (the copy stream waited for it).
+    LS_HIP(c, hipMemcpyAsync(c->slot_tables + (size_t)layer * s.n_blk, tab, (size_t)s.n_blk * sizeof(int32_t),
+                             hipMemcpyHostToDevice, c->copy_stream));
+    LS_HIP(c, hipEventRecord(c->table_uploaded[layer], c->copy_stream));
+    while ((int)c->stage_events.size() < n_stages) {
+        hipEvent_t e;
+        LS_HIP(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        c->stage_events.push_back(e);
+    }
+    c->stage_ranges.clear();
+    size_t fi = 0;
+    const uint8_t* layer_host = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+    for (int sidx = 0; sidx < n_stages; ++sidx) {
+        const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);
+        for (; fi < fills.size() && fills[fi].pos < hi; ++fi) {
+            const auto& f = fills[fi];
+            LS_HIP(c, hipMemcpyAsync(c->cache + (size_t)f.slot * c->block_bytes,
+                                     layer_host + (size_t)f.block * c->block_bytes, c->block_bytes,
+                                     hipMemcpyHostToDevice, c->copy_stream));
+        }
+        LS_HIP(c, hipEventRecord(c->stage_events[sidx], c->copy_stream));
+        c->stage_ranges.emplace_back(lo, hi);
+    }
+    c->pending_layer = layer;
+    local.hits = res.hits;
+    local.misses = res.misses;
+    local.bytes = (int64_t)res.misses * (int64_t)c->block_bytes;
+    local.evictions = res.evictions;
+    if (stats) *stats = local;
+    return LS_OK;
+}
+
+ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (!x) return fail(c, LS_E_INVAL, "null pointer");
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    if (k < 1 || k > s.n_blk) return fail(c, LS_E_INVAL, "k must be in 1..n_blk");
+    for (int l = 0; l < c->desc.n_layers; ++l)
+        if (!c->is_set[l]) return fail(c, LS_E_STATE, "layer weights not set");
+    if (c->desc.residency != LS_WEIGHTS_HBM)
+        return fail(c, LS_E_UNSUPPORTED, "ls_decode_step needs HBM-resident weights; use the per-layer calls");
+    const int cap = B > 1 ? std::min(s.n_blk, B * k) : k;
+    float* cur = x;
+    float* nxt = c->xbuf;
+    for (int l = 0; l < c->desc.n_layers; ++l) {
+        const ls::LayerDev& L = c->dev[l];
+        LS_HIP(c, ls::launch_prenorm(s, cur, B, c->h, c->stream));
+        LS_HIP(c, ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, c->h, B, c->z, c->stream));
+        LS_HIP(c, ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, c->z, B, c->scores, c->stream));
+        LS_HIP(c, ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count,
+                                    c->stream));
+        LS_HIP(c, ls::launch_gateup(s, L, nullptr, c->h, B, c->idx, c->count, 0, cap, c->a, c->stream));
+        LS_HIP(c, ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->stream));
+        std::swap(cur, nxt);
+    }
+    if (cur != x)
+        LS_HIP(c, hipMemcpyAsync(x, cur, (size_t)B * s.d * sizeof(float), hipMemcpyDeviceToDevice, c->stream));
+    c->last_act_n = (int64_t)cap * s.blk;
+    c->last_act_B = B;
+    return LS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,58 @@
+// ls_internal.h - shared declarations of the gfx950 sparse-FFN library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/ls_ffn.h"
+
+namespace ls {
+
+// Down-projection column tile: a block's down weights are stored as
+// [d/kColTile][block/V][kColTile][V] with V = 16 bytes / element size, so one
+// 16-byte lane load holds V neurons of one output column and a wave's load
+// instruction covers a contiguous kilobyte.
+constexpr int kColTile = 16;
+constexpr int kMaxBatch = 8;
+constexpr int kMaxBlocks = 2048;  // n_blk limit of the selection kernel
+
+inline int elem_size(ls_dtype t) { return t == LS_F32 ? 4 : 2; }
+inline int vec_elems(ls_dtype t) { return 16 / elem_size(t); }
+
+// Device views of one layer.
+struct LayerDev {
+    const uint8_t* blocks = nullptr;  // n_blk blocks of block_bytes (resident mode)
+    const void* bias = nullptr;       // [F] or null
+    const void* p1 = nullptr;         // [r, d]
+    const void* p2 = nullptr;         // [n_blk, r]
+    float threshold = 0.f;
+};
+
+struct Shape {
+    int d, F, blk, r, n_blk;
+    ls_dtype dtype;
+    ls_act act;
+    int prenorm;
+    size_t block_elems;  // 3 * blk * d
+};
+
+// ---- kernel launchers (ls_kernels.hip) -------------------------------------------------
+hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st);
+hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, const float* v, int B,
+                            float* out, hipStream_t st);
+hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
+                         int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st);
+// slot_table: null in resident mode (block b lives at blocks + b*block_bytes); else
+// device int32 [n_blk] giving the cache slot of block b, relative to `blocks`.
+hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                         const float* h, int B, const int32_t* idx, const int32_t* count,
+                         int begin, int end, float* a_buf, hipStream_t st);
+hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                       const float* a_buf, int B, const int32_t* idx, const int32_t* count,
+                       int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
+
+}  // namespace ls

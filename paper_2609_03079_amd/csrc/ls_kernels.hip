@@ -1,0 +1,538 @@
+// ls_kernels.hip - gfx950 kernels of one sparse-FFN decode step.
+//
+//  gemv_rows  predictor projections (Sec. 3.3.3): z = P1 h and scores = P2 z.
+//             One wave per output row; 16-byte nontemporal loads of the row,
+//             the fp32 input vector read through the L1, butterfly row sum.
+//  select     priority list (Sec. 2.1): deterministic top-k / threshold /
+//             batch union over fp32 scores, one workgroup, rank by counting.
+//  gateup     gate/up row gather for the selected blocks plus the gating of
+//             Eq. 1, one wave per neuron; writes a in priority-list order.
+//  down       down projection as the sum over hidden neurons (Sec. 3.2.2) plus
+//             the residual of Eq. 2, one workgroup per 16-column tile over all
+//             selected blocks, so no partial sums leave the workgroup.
+//
+// Every reduction has a fixed order: results are bitwise reproducible.
+#include "ls_internal.h"
+
+namespace ls {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---- weight storage types: V elements per 16-byte vector, widened to fp32 -------------
+template <ls_dtype T>
+struct Wt;
+
+template <>
+struct Wt<LS_F32> {
+    static constexpr int V = 4;
+    static constexpr int kBytes = 4;
+    __device__ static inline void widen(const u32x4& r, float* o) {
+        o[0] = __uint_as_float(r.x);
+        o[1] = __uint_as_float(r.y);
+        o[2] = __uint_as_float(r.z);
+        o[3] = __uint_as_float(r.w);
+    }
+    __device__ static inline float scalar(const void* p, size_t i) {
+        return static_cast<const float*>(p)[i];
+    }
+};
+
+__device__ inline float half_bits_to_float(unsigned int bits16) {
+    unsigned short s = static_cast<unsigned short>(bits16);
+    return static_cast<float>(__builtin_bit_cast(_Float16, s));
+}
+
+template <>
+struct Wt<LS_F16> {
+    static constexpr int V = 8;
+    static constexpr int kBytes = 2;
+    __device__ static inline void widen(const u32x4& r, float* o) {
+        o[0] = half_bits_to_float(r.x & 0xffffu);
+        o[1] = half_bits_to_float(r.x >> 16);
+        o[2] = half_bits_to_float(r.y & 0xffffu);
+        o[3] = half_bits_to_float(r.y >> 16);
+        o[4] = half_bits_to_float(r.z & 0xffffu);
+        o[5] = half_bits_to_float(r.z >> 16);
+        o[6] = half_bits_to_float(r.w & 0xffffu);
+        o[7] = half_bits_to_float(r.w >> 16);
+    }
+    __device__ static inline float scalar(const void* p, size_t i) {
+        return half_bits_to_float(static_cast<const unsigned short*>(p)[i]);
+    }
+};
+
+template <>
+struct Wt<LS_BF16> {
+    static constexpr int V = 8;
+    static constexpr int kBytes = 2;
+    // bfloat16 is the upper half of a binary32: widening is a shift.
+    __device__ static inline void widen(const u32x4& r, float* o) {
+        o[0] = __uint_as_float(r.x << 16);
+        o[1] = __uint_as_float(r.x & 0xffff0000u);
+        o[2] = __uint_as_float(r.y << 16);
+        o[3] = __uint_as_float(r.y & 0xffff0000u);
+        o[4] = __uint_as_float(r.z << 16);
+        o[5] = __uint_as_float(r.z & 0xffff0000u);
+        o[6] = __uint_as_float(r.w << 16);
+        o[7] = __uint_as_float(r.w & 0xffff0000u);
+    }
+    __device__ static inline float scalar(const void* p, size_t i) {
+        return __uint_as_float(static_cast<unsigned int>(static_cast<const unsigned short*>(p)[i]) << 16);
+    }
+};
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ inline u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
+
+// ---- MLP input --------------------------------------------------------------------------
+// h = x (no prenorm) or h = x / sqrt(mean(x^2) + 1e-6).  One workgroup per token; the sum of
+// squares is reduced in a fixed order (per-thread strided sums, wave butterfly, then waves
+// in index order).
+__global__ __launch_bounds__(256) void prenorm_kernel(const float* __restrict__ x, int d, int rms,
+                                                      float* __restrict__ h) {
+    const int b = blockIdx.x;
+    const float* xb = x + (size_t)b * d;
+    float* hb = h + (size_t)b * d;
+    float scale = 1.f;
+    if (rms) {
+        __shared__ float part[4];
+        float ss = 0.f;
+        for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xb[i], xb[i], ss);
+        ss = wave_sum(ss);
+        if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+        __syncthreads();
+        float tot = ((part[0] + part[1]) + part[2]) + part[3];
+        scale = 1.f / sqrtf(tot / (float)d + 1e-6f);
+    }
+    for (int i = threadIdx.x; i < d; i += 256) hb[i] = xb[i] * scale;
+}
+
+// ---- GEMV over rows: out[b, row] = sum_c W[row, c] * v[b, c] ------------------------------
+template <ls_dtype T, int B>
+__global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
+                                                        int cols, const float* __restrict__ v,
+                                                        float* __restrict__ out) {
+    constexpr int V = Wt<T>::V;
+    constexpr int U = 8;  // 16-byte loads in flight per lane
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int nchunk = cols / V;
+    const u32x4* wr = reinterpret_cast<const u32x4*>(W + (size_t)row * cols * Wt<T>::kBytes);
+    float acc[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) acc[b] = 0.f;
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+        u32x4 raw[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            raw[u] = c < nchunk ? ld_stream(wr + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            if (c < nchunk) {
+                float w[V];
+                Wt<T>::widen(raw[u], w);
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    const f32x4* vp = reinterpret_cast<const f32x4*>(v + (size_t)b * cols + (size_t)c * V);
+#pragma unroll
+                    for (int q = 0; q < V / 4; ++q) {
+                        const f32x4 x4 = vp[q];
+                        acc[b] = fmaf(w[4 * q + 0], x4.x, acc[b]);
+                        acc[b] = fmaf(w[4 * q + 1], x4.y, acc[b]);
+                        acc[b] = fmaf(w[4 * q + 2], x4.z, acc[b]);
+                        acc[b] = fmaf(w[4 * q + 3], x4.w, acc[b]);
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const float s = wave_sum(acc[b]);
+        if (lane == 0) out[(size_t)b * rows + row] = s;
+    }
+}
+
+// ---- block selection --------------------------------------------------------------------
+// Order-preserving map of a binary32 score to uint32: NaN -> 0 (below every number),
+// -0 -> +0, otherwise a monotone bit transform.  Ties are broken by the smaller index.
+__device__ inline uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ scores, int B,
+                                                      int n, int mode, int k, float tau,
+                                                      int union_batch, int cap,
+                                                      int32_t* __restrict__ idx,
+                                                      int32_t* __restrict__ count) {
+    __shared__ uint32_t key[kMaxBlocks];
+    __shared__ uint32_t ukey[kMaxBlocks];
+    __shared__ uint8_t member[kMaxBlocks];
+    __shared__ int cnt[kMaxBatch + 1];
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const bool do_union = union_batch && B > 1;
+    for (int i = tid; i < n; i += nt) {
+        member[i] = 0;
+        ukey[i] = 0u;
+    }
+    if (tid <= kMaxBatch) cnt[tid] = 0;
+    for (int b = 0; b < B; ++b) {
+        __syncthreads();
+        for (int i = tid; i < n; i += nt) key[i] = order_key(scores[(size_t)b * n + i]);
+        __syncthreads();
+        for (int i = tid; i < n; i += nt) {
+            const uint32_t ki = key[i];
+            int rank = 0;
+            for (int j = 0; j < n; ++j) {
+                const uint32_t kj = key[j];
+                rank += (kj > ki) | ((kj == ki) & (j < i));
+            }
+            const float si = scores[(size_t)b * n + i];
+            const bool sel = (mode == LS_SEL_TOPK) ? (rank < k) : (!isnan(si) && si > tau);
+            if (sel) {
+                member[i] = 1;
+                if (!do_union) idx[(size_t)b * cap + rank] = i;
+                atomicAdd(&cnt[b], 1);
+            }
+            ukey[i] = ki > ukey[i] ? ki : ukey[i];
+        }
+    }
+    __syncthreads();
+    if (!do_union) {
+        if (tid < B) count[tid] = cnt[tid];
+        return;
+    }
+    for (int i = tid; i < n; i += nt) {
+        if (!member[i]) continue;
+        const uint32_t ki = ukey[i];
+        int rank = 0;
+        for (int j = 0; j < n; ++j) {
+            const uint32_t kj = ukey[j];
+            rank += member[j] & ((kj > ki) | ((kj == ki) & (j < i)));
+        }
+        idx[rank] = i;
+        atomicAdd(&cnt[kMaxBatch], 1);
+    }
+    __syncthreads();
+    if (tid == 0) count[0] = cnt[kMaxBatch];
+}
+
+// ---- gate/up gather + gating --------------------------------------------------------------
+__device__ inline int list_end(const int32_t* count, int end, int n_blk) {
+    int c = *count;
+    c = c < 0 ? 0 : (c > n_blk ? n_blk : c);
+    return end < c ? end : c;
+}
+
+template <ls_dtype T, ls_act A, int B>
+__global__ __launch_bounds__(256) void gateup_kernel(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
+    int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
+    int end, float* __restrict__ a_buf) {
+    constexpr int V = Wt<T>::V;
+    constexpr int U = 4;
+    const int lane = threadIdx.x & 63;
+    const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int e = begin + (int)(t / blk);
+    const int q = (int)(t % blk);
+    if (e >= list_end(count, end, n_blk)) return;
+    const int b = idx[e];
+    const size_t apos = (size_t)e * blk + q;
+    if (b < 0 || b >= n_blk) {  // invalid id: the entry contributes nothing
+        if (lane < B) a_buf[(size_t)lane * F + apos] = 0.f;
+        return;
+    }
+    const int slot = slot_table ? slot_table[b] : b;
+    if (slot < 0) {  // block not in the cache: contributes nothing
+        if (lane < B) a_buf[(size_t)lane * F + apos] = 0.f;
+        return;
+    }
+    const uint8_t* base = blocks + (size_t)slot * block_bytes;
+    const size_t row_bytes = (size_t)d * Wt<T>::kBytes;
+    const u32x4* grow = reinterpret_cast<const u32x4*>(base + (size_t)q * row_bytes);
+    const u32x4* urow = reinterpret_cast<const u32x4*>(base + (size_t)(blk + q) * row_bytes);
+    const int nchunk = d / V;
+    float ag[B], au[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) ag[i] = au[i] = 0.f;
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+        u32x4 rg[U], ru[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            const bool ok = c < nchunk;
+            rg[u] = ok ? ld_stream(grow + c) : u32x4{0u, 0u, 0u, 0u};
+            ru[u] = ok ? ld_stream(urow + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            if (c < nchunk) {
+                float wg[V], wu[V];
+                Wt<T>::widen(rg[u], wg);
+                Wt<T>::widen(ru[u], wu);
+#pragma unroll
+                for (int i = 0; i < B; ++i) {
+                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
+#pragma unroll
+                    for (int qq = 0; qq < V / 4; ++qq) {
+                        const f32x4 x4 = hp[qq];
+                        ag[i] = fmaf(wg[4 * qq + 0], x4.x, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 1], x4.y, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 2], x4.z, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 3], x4.w, ag[i]);
+                        au[i] = fmaf(wu[4 * qq + 0], x4.x, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 1], x4.y, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 2], x4.z, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 3], x4.w, au[i]);
+                    }
+                }
+            }
+        }
+    }
+    const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+        const float g = wave_sum(ag[i]) + bj;
+        const float u = wave_sum(au[i]);
+        float a;
+        if (A == LS_ACT_REGLU) {
+            a = fmaxf(g, 0.f) * u;  // exactly zero for g <= 0
+        } else {
+            const float sg = g / (1.f + expf(-g));
+            a = fabsf(sg) > thresh ? sg * u : 0.f;
+        }
+        if (lane == 0) a_buf[(size_t)i * F + apos] = a;
+    }
+}
+
+// ---- down projection + residual -----------------------------------------------------------
+template <ls_dtype T, int B>
+__global__ __launch_bounds__(256) void down_kernel(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
+    const float* __restrict__ x_in, float* __restrict__ x_acc) {
+    constexpr int V = Wt<T>::V;
+    constexpr int EU = 4;  // list entries in flight per wave
+    const int tile = blockIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n_end = list_end(count, end, n_blk);
+    const int nchunk = blk * Wt<T>::kBytes;  // 16-byte chunks of one (block, tile) piece
+    const int per_lane = (nchunk + 63) / 64;
+    const size_t down_off = (size_t)2 * blk * d * Wt<T>::kBytes +
+                            (size_t)tile * blk * kColTile * Wt<T>::kBytes;
+    float acc[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) acc[i] = 0.f;
+    for (int e0 = begin + wave; e0 < n_end; e0 += 4 * EU) {
+        const u32x4* src[EU];
+        int ent[EU];
+#pragma unroll
+        for (int u = 0; u < EU; ++u) {
+            const int e = e0 + 4 * u;
+            int b = e < n_end ? idx[e] : -1;
+            if (b >= n_blk) b = -1;
+            int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
+            ent[u] = slot < 0 ? -1 : e;
+            src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
+                                                    down_off);
+        }
+        for (int i0 = 0; i0 < per_lane; i0 += 2) {
+            u32x4 raw[EU][2];
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    raw[u][r] = (ent[u] >= 0 && c < nchunk) ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    if (ent[u] >= 0 && c < nchunk) {
+                        float w[V];
+                        Wt<T>::widen(raw[u][r], w);
+                        const int grp = c / kColTile;  // this lane's V neurons
+                        const float* ap = a_buf + (size_t)ent[u] * blk + (size_t)grp * V;
+#pragma unroll
+                        for (int i = 0; i < B; ++i) {
+                            const f32x4* a4 = reinterpret_cast<const f32x4*>(ap + (size_t)i * F);
+#pragma unroll
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = a4[qq];
+                                acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
+                                acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
+                                acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
+                                acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
+                            }
+                        }
+                    }
+                }
+        }
+    }
+    // lanes l, l+16, l+32, l+48 hold the same column
+    __shared__ float part[4][kMaxBatch][kColTile];
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+        float v = acc[i];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        if (lane < kColTile) part[wave][i][lane] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < B * kColTile) {
+        const int i = threadIdx.x / kColTile, col = threadIdx.x % kColTile;
+        const float y = ((part[0][i][col] + part[1][i][col]) + part[2][i][col]) + part[3][i][col];
+        const size_t m = (size_t)i * d + (size_t)tile * kColTile + col;
+        x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
+    }
+}
+
+// ---- dispatch helpers -----------------------------------------------------------------------
+template <template <ls_dtype, int> class K, ls_dtype T>
+struct ByBatch;
+
+}  // namespace
+
+hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st) {
+    hipLaunchKernelGGL(prenorm_kernel, dim3(B), dim3(256), 0, st, x, s.d, s.prenorm, h);
+    return hipGetLastError();
+}
+
+template <ls_dtype T>
+static hipError_t gemv_t(const void* W, int rows, int cols, const float* v, int B, float* out,
+                         hipStream_t st) {
+    const dim3 grid((rows + 3) / 4), blk(256);
+    const uint8_t* w = static_cast<const uint8_t*>(W);
+    switch (B) {
+        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, const float* v, int B,
+                            float* out, hipStream_t st) {
+    switch (t) {
+        case LS_F32: return gemv_t<LS_F32>(W, rows, cols, v, B, out, st);
+        case LS_F16: return gemv_t<LS_F16>(W, rows, cols, v, B, out, st);
+        case LS_BF16: return gemv_t<LS_BF16>(W, rows, cols, v, B, out, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
+                         int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st) {
+    int threads = ((n_blk + 63) / 64) * 64;
+    threads = threads < 64 ? 64 : (threads > 1024 ? 1024 : threads);
+    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
+                       union_batch, cap, idx, count);
+    return hipGetLastError();
+}
+
+template <ls_dtype T, ls_act A>
+static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                           const float* h, int B, const int32_t* idx, const int32_t* count,
+                           int begin, int end, float* a_buf, hipStream_t st) {
+    const long tasks = (long)(end - begin) * s.blk;
+    if (tasks <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((tasks + 3) / 4)), blk(256);
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+#define LS_GU(NB)                                                                                 \
+    hipLaunchKernelGGL((gateup_kernel<T, A, NB>), grid, blk, 0, st, L.blocks, bb, slot_table,     \
+                       L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, \
+                       a_buf)
+    switch (B) {
+        case 1: LS_GU(1); break;
+        case 2: LS_GU(2); break;
+        case 3: LS_GU(3); break;
+        case 4: LS_GU(4); break;
+        case 5: LS_GU(5); break;
+        case 6: LS_GU(6); break;
+        case 7: LS_GU(7); break;
+        case 8: LS_GU(8); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef LS_GU
+    return hipGetLastError();
+}
+
+hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                         const float* h, int B, const int32_t* idx, const int32_t* count,
+                         int begin, int end, float* a_buf, hipStream_t st) {
+    const bool relu = s.act == LS_ACT_REGLU;
+    switch (s.dtype) {
+        case LS_F32:
+            return relu ? gateup_t<LS_F32, LS_ACT_REGLU>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st)
+                        : gateup_t<LS_F32, LS_ACT_SWIGLU_THRESH>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st);
+        case LS_F16:
+            return relu ? gateup_t<LS_F16, LS_ACT_REGLU>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st)
+                        : gateup_t<LS_F16, LS_ACT_SWIGLU_THRESH>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st);
+        case LS_BF16:
+            return relu ? gateup_t<LS_BF16, LS_ACT_REGLU>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st)
+                        : gateup_t<LS_BF16, LS_ACT_SWIGLU_THRESH>(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <ls_dtype T>
+static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                         const float* a_buf, int B, const int32_t* idx, const int32_t* count,
+                         int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+    const dim3 grid(s.d / kColTile), blk(256);
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+#define LS_DN(NB)                                                                             \
+    hipLaunchKernelGGL((down_kernel<T, NB>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
+                       s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc)
+    switch (B) {
+        case 1: LS_DN(1); break;
+        case 2: LS_DN(2); break;
+        case 3: LS_DN(3); break;
+        case 4: LS_DN(4); break;
+        case 5: LS_DN(5); break;
+        case 6: LS_DN(6); break;
+        case 7: LS_DN(7); break;
+        case 8: LS_DN(8); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef LS_DN
+    return hipGetLastError();
+}
+
+hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                       const float* a_buf, int B, const int32_t* idx, const int32_t* count,
+                       int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+    switch (s.dtype) {
+        case LS_F32: return down_t<LS_F32>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
+        case LS_F16: return down_t<LS_F16>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
+        case LS_BF16: return down_t<LS_BF16>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace ls

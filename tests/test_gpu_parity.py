@@ -1,0 +1,331 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Per step: scores (rel-L2 <= 1e-5), block ids (bit-exact on identical fp32
+scores), FFN output y = x_out - x_in teacher-forced with the GPU's input and
+block list (rel-L2 <= 1e-5 fp32, <= 2e-3 fp16/bf16).
+"""
+import numpy as np
+import pytest
+
+import lsgen
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_03079_amd as lsffn  # noqa: E402
+from gpu_util import (SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn,  # noqa: E402
+                      rel_l2)
+
+C = lsgen.CONFIGS
+
+# Shapes spanning several tiles with ragged tails, small enough for the oracle.
+SMALL = {
+    "c1": C["c1_reglu_512"],
+    "f16_ragged": C["llama2_7b_ffn"].with_(n_layers=2, d_model=576, d_ff=1200, block=24, rank=192,
+                                           keep_pct=30),
+    "bf16_swiglu": C["mistral_7b_ffn"].with_(n_layers=2, d_model=512, d_ff=2048, block=128,
+                                             rank=128, keep_pct=50),
+    "f32_stack": C["c1_reglu_512"].with_(n_layers=3, prenorm=True, d_model=320, d_ff=960,
+                                         block=40, rank=64),
+}
+
+
+GUARD = 1e-4  # |SiLU(g)| this close to the threshold may be decided either way
+
+
+def _oracle_y(w, cfg, x, blocks):
+    h = oracle.mlp_input(x, cfg.prenorm)
+    return oracle.sparse_ffn(w, h, blocks, cfg.block, cfg.act, w.threshold)
+
+
+def _check_y(f, ws_l, cfg, xin, yg, blocks, tol, tag):
+    """y of every token against the oracle.  SwiGLU-threshold: the GPU's keep/drop decisions
+    (from its activation dump) must equal the oracle's outside a guard band around the
+    threshold; the oracle then recomputes y with the GPU's decisions."""
+    B = xin.shape[0]
+    neurons = oracle.neurons_of_blocks(blocks, cfg.block)
+    a_gpu = None
+    if cfg.act == lsgen.ACT_SWIGLU_THRESH:
+        buf = empty_f32(B * max(1, cfg.d_ff))
+        n = f.ls_debug_last_activations(buf)
+        a_gpu = host(buf)[:B * n].reshape(B, n)[:, :len(neurons)]
+    for b in range(B):
+        if a_gpu is None:
+            y_ref = _oracle_y(ws_l, cfg, xin[b], blocks)
+        else:
+            h = oracle.mlp_input(xin[b], cfg.prenorm)
+            g, _, a_t = oracle.activations(ws_l, h, neurons, cfg.act, ws_l.threshold)
+            _, _, a_all = oracle.activations(ws_l, h, neurons, cfg.act, -1.0)
+            sig = np.abs(g / (1.0 + np.exp(-g)))
+            keep_gpu = a_gpu[b] != 0
+            keep_ref = a_t != 0
+            flips = keep_gpu != keep_ref
+            assert np.all(np.abs(sig[flips] - ws_l.threshold) <= GUARD), (tag, b, int(flips.sum()))
+            y_ref = oracle.down(ws_l, neurons, np.where(keep_gpu, a_all, 0.0))
+        assert rel_l2(yg[b], y_ref) <= tol, (tag, b, rel_l2(yg[b], y_ref))
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_predict_parity(name):
+    cfg = SMALL[name]
+    f, ws = make_ffn(cfg, max_batch=4)
+    xs = lsgen.tokens(cfg, 0, 1, 4)[0]
+    scores = empty_f32(4, cfg.n_blk)
+    for l in range(cfg.n_layers):
+        f.ls_predict(l, dev_f32(xs), 4, scores)
+        got = host(scores)
+        for b in range(4):
+            ref = oracle.predict(ws[l].p1, ws[l].p2, oracle.mlp_input(xs[b], cfg.prenorm))
+            assert rel_l2(got[b], ref) <= SCORE_TOL, (name, l, b)
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 8])
+@pytest.mark.parametrize("kind", ["normal", "ties", "zeros", "special"])
+@pytest.mark.parametrize("n_blk", [1, 48, 172, 224, 2048])
+def test_select_bit_exact(B, kind, n_blk):
+    cfg = C["c1_reglu_512"].with_(d_ff=8 * n_blk, block=8, d_model=64, rank=64)
+    f, _ = make_ffn(cfg, max_batch=8)
+    rng = np.random.default_rng(1000 * B + n_blk)
+    S = lsgen.adversarial_scores(rng, B, n_blk, kind)
+    s_dev = dev_f32(S)
+    for k in sorted({1, max(1, n_blk // 7), n_blk}):
+        for uni in ([0, 1] if B > 1 else [0]):
+            cap = min(n_blk, B * k) if uni else k
+            idx = empty_i32(cap if uni else B * cap)
+            cnt = empty_i32(1 if uni else B)
+            f.ls_select_blocks(s_dev, B, lsffn.LS_SEL_TOPK, k, 0.0, uni, cap, idx, cnt)
+            ref_idx, ref_cnt = oracle.select(S, k=k, union_batch=bool(uni), cap=cap)
+            gi, gc = host(idx), host(cnt)
+            assert np.array_equal(gc, ref_cnt)
+            if uni:
+                assert np.array_equal(gi[:gc[0]], ref_idx[:ref_cnt[0]])
+            else:
+                gi = gi.reshape(B, cap)
+                for b in range(B):
+                    assert np.array_equal(gi[b, :gc[b]], ref_idx[b, :ref_cnt[b]])
+    for tau in (0.0, -0.5, 1.0):
+        for uni in ([0, 1] if B > 1 else [0]):
+            idx = empty_i32(n_blk if uni else B * n_blk)
+            cnt = empty_i32(1 if uni else B)
+            f.ls_select_blocks(s_dev, B, lsffn.LS_SEL_THRESHOLD, 1, tau, uni, n_blk, idx, cnt)
+            ref_idx, ref_cnt = oracle.select(S, mode=oracle.SEL_THRESHOLD, tau=tau,
+                                             union_batch=bool(uni), cap=n_blk)
+            gi, gc = host(idx), host(cnt)
+            assert np.array_equal(gc, ref_cnt)
+            if uni:
+                assert np.array_equal(gi[:gc[0]], ref_idx[:ref_cnt[0]])
+            else:
+                gi = gi.reshape(B, n_blk)
+                for b in range(B):
+                    assert np.array_equal(gi[b, :gc[b]], ref_idx[b, :ref_cnt[b]])
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("B", [1, 3])
+def test_sparse_step_teacher_forced(name, B):
+    cfg = SMALL[name]
+    f, ws = make_ffn(cfg, max_batch=B)
+    tol = Y_TOL[cfg.dtype]
+    xs = lsgen.tokens(cfg, 5, 1, B)[0]
+    x_in = dev_f32(xs)
+    scores = empty_f32(B, cfg.n_blk)
+    cap = min(cfg.n_blk, B * cfg.k)
+    idx, cnt = empty_i32(cap), empty_i32(1)
+    x_out = empty_f32(B, cfg.d_model)
+    for l in range(cfg.n_layers):
+        f.ls_predict(l, x_in, B, scores)
+        f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+        f.ls_sparse_ffn_step(l, x_in, B, idx, cnt, 0, cap, x_out)
+        gi, gc = host(idx), host(cnt)
+        blocks = gi[:gc[0]]
+        # the GPU's block list is the oracle's selection on the GPU's scores
+        ref_idx, ref_cnt = oracle.select(host(scores), k=cfg.k, union_batch=True, cap=cap)
+        assert np.array_equal(blocks, (ref_idx if B > 1 else ref_idx[0])[:gc[0]])
+        xin_h, xout_h = host(x_in), host(x_out)
+        yg = xout_h.astype(np.float64) - xin_h.astype(np.float64)
+        _check_y(f, ws[l], cfg, xin_h, yg, blocks, tol, (name, l))
+        x_in, x_out = x_out, x_in
+
+
+@pytest.mark.parametrize("name", ["c1", "f16_ragged", "f32_stack"])
+def test_stages_eq1_eq2(name):
+    """Stages over the priority list: x_acc after the last stage equals the single-shot output
+    (Eq. 1-2); each intermediate x_acc matches the oracle's refined feature x_tilde^(j)."""
+    cfg = SMALL[name]
+    f, ws = make_ffn(cfg, n_layers=1)
+    tol = Y_TOL[cfg.dtype]
+    x = lsgen.tokens(cfg, 7, 1, 1)[0]
+    x_in = dev_f32(x)
+    scores = empty_f32(1, cfg.n_blk)
+    k = max(cfg.k, 5)
+    idx, cnt = empty_i32(k), empty_i32(1)
+    f.ls_predict(0, x_in, 1, scores)
+    f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, k, 0.0, 0, k, idx, cnt)
+    blocks = host(idx)[:k]
+    single = empty_f32(1, cfg.d_model)
+    f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, 0, k, single)
+    for K in (2, 3, k):
+        acc = empty_f32(1, cfg.d_model)
+        h = oracle.mlp_input(x[0], cfg.prenorm)
+        _, xt = oracle.staged_ffn(ws[0], x[0], h, blocks, cfg.block, K, cfg.act, ws[0].threshold)
+        for j, (lo, hi) in enumerate(oracle.stage_bounds(k, K)):
+            f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, lo, hi, acc)
+            got = host(acc)[0].astype(np.float64)
+            assert rel_l2(got - x[0], xt[j] - x[0]) <= tol, (K, j)
+        assert rel_l2(host(acc)[0] - x[0], host(single)[0] - x[0]) <= tol
+
+
+@pytest.mark.parametrize("name", ["c1", "f16_ragged"])
+def test_permutation_invariance(name):
+    cfg = SMALL[name]
+    f, ws = make_ffn(cfg, n_layers=1)
+    tol = Y_TOL[cfg.dtype]
+    x = lsgen.tokens(cfg, 9, 1, 1)[0]
+    x_in = dev_f32(x)
+    rng = np.random.default_rng(2)
+    blocks = rng.choice(cfg.n_blk, size=min(cfg.n_blk, 11), replace=False).astype(np.int32)
+    outs = []
+    for perm in range(3):
+        order = blocks if perm == 0 else rng.permutation(blocks)
+        out = empty_f32(1, cfg.d_model)
+        f.ls_sparse_ffn_step(0, x_in, 1, dev_f32(order).int(), dev_f32([len(order)]).int(), 0,
+                             len(order), out)
+        outs.append(host(out)[0].astype(np.float64) - x[0])
+    y_ref = _oracle_y(ws[0], cfg, x[0], blocks)
+    for y in outs:
+        assert rel_l2(y, y_ref) <= tol
+        assert rel_l2(y, outs[0]) <= tol
+
+
+def test_relu_dead_blocks_exact_zero():
+    cfg = SMALL["f16_ragged"].with_(n_layers=1)
+    w = lsgen.layer_weights(cfg, 0)
+    dead = [2, 5, 11]
+    b = w.bias.copy()
+    for blk in dead:
+        b[blk * cfg.block:(blk + 1) * cfg.block] = np.float16(-1e4)
+    w.bias = b
+    f, _ = make_ffn(cfg, n_layers=1, weights=[w])
+    x = lsgen.tokens(cfg, 3, 1, 1)[0]
+    x_in = dev_f32(x)
+    live = [0, 3, 7]
+    order = np.array([0, 2, 3, 5, 7, 11], np.int32)
+    out = empty_f32(1, cfg.d_model)
+    f.ls_sparse_ffn_step(0, x_in, 1, dev_f32(order).int(), dev_f32([6]).int(), 0, 6, out)
+    a = empty_f32(6 * cfg.block)
+    n = f.ls_debug_last_activations(a)
+    assert n == 6 * cfg.block
+    a = host(a).reshape(6, cfg.block)
+    for pos, blk in enumerate(order):
+        if blk in dead:
+            assert np.all(a[pos] == 0.0)
+    y = host(out)[0].astype(np.float64) - x[0]
+    y_ref = _oracle_y(w, cfg, x[0], live)
+    assert rel_l2(y, y_ref) <= Y_TOL[cfg.dtype]
+
+
+def test_empty_and_clamped_ranges():
+    cfg = SMALL["c1"]
+    f, ws = make_ffn(cfg)
+    x = lsgen.tokens(cfg, 1, 1, 1)[0]
+    x_in = dev_f32(x)
+    idx = dev_f32([3, 1, 4, 1, 5]).int()
+    cnt = dev_f32([3]).int()
+    out = empty_f32(1, cfg.d_model)
+    f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, 0, 0, out)   # empty: x_acc = x_in
+    assert np.array_equal(host(out)[0], x[0])
+    f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, 0, 5, out)   # clamped to count = 3
+    y = host(out)[0].astype(np.float64) - x[0]
+    assert rel_l2(y, _oracle_y(ws[0], cfg, x[0], [3, 1, 4])) <= Y_TOL[cfg.dtype]
+    zero = dev_f32([0]).int()
+    f.ls_sparse_ffn_step(0, x_in, 1, idx, zero, 0, 5, out)  # count 0
+    assert np.array_equal(host(out)[0], x[0])
+
+
+def test_decode_step_equals_composition_and_is_deterministic():
+    cfg = SMALL["f16_ragged"].with_(n_layers=3)
+    for B in (1, 4):
+        f, ws = make_ffn(cfg, max_batch=B)
+        x0 = lsgen.tokens(cfg, 11, 1, B)[0]
+        xd = dev_f32(x0)
+        f.ls_decode_step(xd, B, cfg.k)
+        got = host(xd)
+        xd2 = dev_f32(x0)
+        f.ls_decode_step(xd2, B, cfg.k)
+        assert np.array_equal(host(xd2), got)
+        # composition of the per-layer calls, teacher-forced oracle check at every layer
+        cap = min(cfg.n_blk, B * cfg.k)
+        x_in = dev_f32(x0)
+        x_out = empty_f32(B, cfg.d_model)
+        scores = empty_f32(B, cfg.n_blk)
+        idx, cnt = empty_i32(cap), empty_i32(1)
+        for l in range(cfg.n_layers):
+            f.ls_predict(l, x_in, B, scores)
+            f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+            f.ls_sparse_ffn_step(l, x_in, B, idx, cnt, 0, cap, x_out)
+            blocks = host(idx)[:host(cnt)[0]]
+            xi, xo = host(x_in), host(x_out)
+            _check_y(f, ws[l], cfg, xi, xo.astype(np.float64) - xi, blocks, Y_TOL[cfg.dtype], l)
+            x_in, x_out = x_out, x_in
+        assert rel_l2(host(x_in) - x0, got - x0) <= Y_TOL[cfg.dtype]
+
+
+def test_invalid_arguments_return_codes():
+    cfg = SMALL["c1"]
+    f, _ = make_ffn(cfg, max_batch=2)
+    x = empty_f32(2, cfg.d_model)
+    s = empty_f32(2, cfg.n_blk)
+    idx, cnt = empty_i32(cfg.n_blk), empty_i32(2)
+    bad = [
+        lambda: f.ls_predict(1, x, 1, s),                      # layer out of range
+        lambda: f.ls_predict(0, x, 3, s),                      # B > max_batch
+        lambda: f.ls_predict(0, None, 1, s),                   # null
+        lambda: f.ls_select_blocks(s, 1, 0, 0, 0.0, 0, 5, idx, cnt),           # k = 0
+        lambda: f.ls_select_blocks(s, 1, 0, cfg.n_blk + 1, 0.0, 0, 99, idx, cnt),
+        lambda: f.ls_select_blocks(s, 1, 0, 5, 0.0, 0, 4, idx, cnt),           # cap < k
+        lambda: f.ls_select_blocks(s, 2, 0, 30, 0.0, 1, 47, idx, cnt),         # union cap
+        lambda: f.ls_select_blocks(s, 1, 1, 1, 0.0, 0, 10, idx, cnt),          # threshold cap
+        lambda: f.ls_sparse_ffn_step(0, x, 1, idx, cnt, 0, 3, x),              # aliasing
+        lambda: f.ls_sparse_ffn_step(0, x, 1, idx, cnt, 4, 3, s),              # begin > end
+        lambda: f.ls_decode_step(x, 1, 0),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(lsffn.LsError) as e:
+            call()
+        assert e.value.status == lsffn.LS_E_INVAL, i
+    g = lsffn.Ffn(n_layers=2, d_model=64, d_ff=64, block=8, rank=64, dtype=lsffn.LS_F32)
+    with pytest.raises(lsffn.LsError) as e:
+        g.ls_predict(1, x, 1, s)                                # layer never set
+    assert e.value.status == lsffn.LS_E_STATE
+    with pytest.raises(lsffn.LsError) as e:
+        lsffn.Ffn(n_layers=1, d_model=100, d_ff=64, block=8, rank=64)
+    assert e.value.status == lsffn.LS_E_INVAL
+
+
+@pytest.mark.parametrize("cfg_name", ["llama2_7b_ffn", "llama2_13b_ffn", "mistral_7b_ffn"])
+def test_full_size_layers_sampled(cfg_name):
+    """Full-size layer shapes (2 layers of each stack), B=1, teacher-forced per layer."""
+    cfg = C[cfg_name].with_(n_layers=2)
+    f, ws = make_ffn(cfg)
+    x = lsgen.tokens(cfg, 0, 1, 1)[0]
+    x_in = dev_f32(x)
+    x_out = empty_f32(1, cfg.d_model)
+    scores = empty_f32(1, cfg.n_blk)
+    idx, cnt = empty_i32(cfg.k), empty_i32(1)
+    for l in range(cfg.n_layers):
+        f.ls_predict(l, x_in, 1, scores)
+        xi = host(x_in)[0]
+        ref_s = oracle.predict(ws[l].p1, ws[l].p2, oracle.mlp_input(xi, cfg.prenorm))
+        assert rel_l2(host(scores)[0], ref_s) <= SCORE_TOL
+        f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 0, cfg.k, idx, cnt)
+        blocks = host(idx)
+        ref_idx, _ = oracle.select(host(scores), k=cfg.k, cap=cfg.k)
+        assert np.array_equal(blocks, ref_idx[0])
+        f.ls_sparse_ffn_step(l, x_in, 1, idx, cnt, 0, cfg.k, x_out)
+        y = host(x_out).astype(np.float64) - xi[None, :]
+        _check_y(f, ws[l], cfg, xi[None, :], y, blocks, Y_TOL[cfg.dtype], (cfg_name, l))
+        x_in, x_out = x_out, x_in

@@ -1,0 +1,141 @@
+"""Host-side checks that need no GPU: the C-ABI library loads and exports every
+entry point its header declares, and the HBM block cache bookkeeping (LRU,
+never evicting a block of the current request, hit/miss accounting)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ls_ffn.h")
+CSRC = os.path.join(ROOT, "paper_2609_03079_amd", "csrc")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:ls_status|const char\*)\s+(ls_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("ls_ffn_create", "ls_predict", "ls_select_blocks", "ls_sparse_ffn_step",
+                     "ls_stream_weights", "ls_decode_step", "ls_ffn_set_layer", "ls_ffn_destroy",
+                     "ls_last_error"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2609_03079_amd as lsffn
+    if not os.path.exists(lsffn.LIB_PATH):
+        from paper_2609_03079_amd import build as b
+        b.build()
+    lib = ctypes.CDLL(lsffn.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert set(_declared_functions()) == set(lsffn.EXPORTS)
+    # the error text for a failed create is available without a context
+    lsffn.load()
+    desc = lsffn.LsFfnDesc(0, 64, 64, 8, 64, 1, 0, 0, 0, 0, 0, None, 0)
+    out = ctypes.c_void_p()
+    st = lsffn.load().ls_ffn_create(ctypes.byref(desc), ctypes.byref(out))
+    assert st == lsffn.LS_E_INVAL and not out.value
+    assert b"n_layers" in lsffn.load().ls_last_error(None)
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    import paper_2609_03079_amd as lsffn
+    monkeypatch.setattr(lsffn, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(lsffn, "_lib", None)
+    with pytest.raises(RuntimeError):
+        lsffn.load()
+
+
+@pytest.fixture(scope="module")
+def bc(tmp_path_factory):
+    out = tmp_path_factory.mktemp("bc") / "libbc.so"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-o", str(out),
+                    os.path.join(CSRC, "block_cache_capi.cpp")], check=True)
+    lib = ctypes.CDLL(str(out))
+    lib.bc_create.restype = ctypes.c_void_p
+    lib.bc_create.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int]
+    lib.bc_destroy.argtypes = [ctypes.c_void_p]
+    lib.bc_request.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.bc_slot_table.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    lib.bc_invalidate_layer.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    return lib
+
+
+class Cache:
+    def __init__(self, lib, slots, L, n_blk):
+        self.lib, self.L, self.n_blk = lib, L, n_blk
+        self.h = lib.bc_create(slots, L, n_blk)
+
+    def request(self, layer, blocks):
+        b = np.ascontiguousarray(blocks, np.int32)
+        counts = np.zeros(3, np.int64)
+        fills = np.zeros(3 * max(1, len(b)), np.int32)
+        nf = np.zeros(1, np.int32)
+        ok = self.lib.bc_request(self.h, layer, b.ctypes.data, len(b), counts.ctypes.data,
+                                 fills.ctypes.data, nf.ctypes.data)
+        return ok, counts.tolist(), fills[:3 * nf[0]].reshape(-1, 3).tolist()
+
+    def table(self, layer):
+        t = np.zeros(self.n_blk, np.int32)
+        self.lib.bc_slot_table(self.h, layer, t.ctypes.data)
+        return t
+
+
+def test_block_cache_accounting_and_lru(bc):
+    c = Cache(bc, 4, 2, 10)
+    ok, cnt, fills = c.request(0, [3, 1, 4])
+    assert ok and cnt == [0, 3, 0]
+    assert [f[:2] for f in fills] == [[0, 3], [1, 1], [2, 4]]  # misses in priority order
+    ok, cnt, _ = c.request(0, [1, 5])
+    assert ok and cnt == [1, 1, 0]
+    # cache full: {3,1,4,5}; LRU order oldest -> newest: 3, 4, 1, 5
+    ok, cnt, fills = c.request(1, [7])
+    assert ok and cnt == [0, 1, 1]
+    t0 = c.table(0)
+    assert t0[3] == -1 and t0[1] >= 0 and t0[4] >= 0 and t0[5] >= 0
+    # a request never evicts its own blocks, even when they are the least recent
+    ok, cnt, fills = c.request(0, [4, 9, 8])
+    assert ok and cnt == [1, 2, 2]
+    t0 = c.table(0)
+    assert t0[4] >= 0 and t0[9] >= 0 and t0[8] >= 0
+    slots = [s for s in t0 if s >= 0] + [s for s in c.table(1) if s >= 0]
+    assert len(slots) == len(set(slots)) == 4
+
+
+def test_block_cache_properties_random(bc):
+    rng = np.random.default_rng(0)
+    S, L, N = 7, 3, 12
+    c = Cache(bc, S, L, N)
+    for it in range(400):
+        layer = int(rng.integers(L))
+        n = int(rng.integers(0, S + 1))
+        req = rng.integers(0, N, size=n).astype(np.int32)  # duplicates allowed
+        before = c.table(layer).copy()
+        ok, (hits, misses, ev), fills = c.request(layer, req)
+        assert ok
+        assert hits + misses == n
+        assert misses == len(fills) == len(set(int(b) for b in req if before[b] < 0))
+        t = c.table(layer)
+        assert all(t[b] >= 0 for b in req)
+        assert [f[0] for f in fills] == sorted(f[0] for f in fills)
+        occupied = [s for l in range(L) for s in c.table(l) if s >= 0]
+        assert len(occupied) == len(set(occupied)) <= S
+    ok, _, _ = c.request(0, list(range(S + 1)))
+    assert not ok  # larger than the cache
+
+
+def test_block_cache_invalidate(bc):
+    c = Cache(bc, 3, 1, 5)
+    c.request(0, [0, 1])
+    bc.bc_invalidate_layer(c.h, 0)
+    assert np.all(c.table(0) == -1)
+    ok, cnt, _ = c.request(0, [0, 1, 2])
+    assert ok and cnt == [0, 3, 0]
