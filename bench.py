@@ -1,0 +1,198 @@
+"""Sparse-FFN decode benchmark on one MI355X.
+
+One step = one decode step of one token through every layer of the FFN stack:
+predictor (P1, P2) -> top-k block selection -> gate/up row gather + gating ->
+down projection + residual, all in the HIP kernels behind the C ABI.
+
+Workload (default): Llama-2-7B-shaped FFN stack, 32 layers, d_model 4096,
+d_ff 11008, fp16 weights, ReGLU with ~10% active neurons, rank-1024 predictor,
+64-neuron blocks, top 12% of blocks (k = 21 of 172), batch 1, fresh N(0,1)
+token per step; synthetic seeded weights of that shape.
+
+Prints ONE JSON line (see the "metric" contract): tokens/s, effective weight
+GB/s on the algorithmic bytes, the roofline of the dominant kernel measured
+with HIP events in the timed region, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+
+
+def algorithmic_bytes_per_layer(cfg, U: int, Z: int = 0) -> int:
+    """Bytes one layer must read: the U selected blocks' gate/up/down rows (minus Z blocks whose
+    down rows are skipped as all-zero), their gate bias, and the predictor factors."""
+    s = cfg.elem_bytes
+    ffn = U * cfg.block * cfg.d_model * 3 - Z * cfg.block * cfg.d_model
+    bias = U * cfg.block if cfg.gate_bias is not None else 0
+    pred = cfg.d_model * cfg.rank + cfg.rank * cfg.n_blk
+    return s * (ffn + bias + pred)
+
+
+def cpu_baseline(cfg, weights, xs, n_tokens: int):
+    """The CPU oracle (as it stands) on the first n_tokens decode steps of the same workload."""
+    import oracle
+    t0 = time.perf_counter()
+    for t in range(n_tokens):
+        x = xs[t, 0].copy()
+        for l in range(cfg.n_layers):
+            _, _, _, x = oracle.layer_step(weights[l], cfg, x)
+    dt = time.perf_counter() - t0
+    return {"value": n_tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n_tokens} decode steps x {cfg.n_layers} layers of the same workload "
+                      f"(B=1), fp64 plain-C oracle, single thread, {dt:.1f} s",
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--config", default="llama2_7b_ffn")
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle sample size (0: skip)")
+    ap.add_argument("--layers", type=int, default=0, help="override the layer count (testing)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(this build has no multi-GPU path).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    cfg = lsgen.CONFIGS[args.config]
+    if args.layers:
+        cfg = cfg.with_(n_layers=args.layers)
+    if cfg.host_resident:
+        print("bench.py measures HBM-resident stacks; use the streaming test for host residency",
+              file=sys.stderr)
+        return 2
+    B, K, W = args.batch, args.steps, args.warmup
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    t_setup = time.perf_counter()
+    f = lsffn.Ffn(n_layers=cfg.n_layers, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block,
+                  rank=cfg.rank, max_batch=B, dtype=cfg.dtype, act=cfg.act,
+                  prenorm_rms=int(cfg.prenorm), stream=stream)
+    keep_host = args.cpu_tokens > 0
+    weights = []
+    for l in range(cfg.n_layers):
+        w = lsgen.layer_weights(cfg, l)
+        f.ls_ffn_set_layer(l, w)
+        weights.append(w if keep_host else None)
+    xs = lsgen.tokens(cfg, 0, W + K, B)                      # [W+K, B, d] fp32
+    x_dev = torch.from_numpy(xs).to(dev)                      # inputs resident in HBM
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    for i in range(W):
+        f.ls_decode_step(x_dev[i], B, cfg.k)
+    torch.cuda.synchronize()
+
+    # timed region: K decode steps; kernel timing records HIP event pairs around each launch
+    f.ls_set_kernel_timing(True)
+    f.ls_kernel_timing(0, reset=True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(K):
+        f.ls_decode_step(x_dev[W + i], B, cfg.k)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    f.ls_set_kernel_timing(False)
+    gpu_ms = ev0.elapsed_time(ev1)
+    per_kernel = {}
+    for kid, name in ((lsffn.LS_K_PRENORM, "prenorm"), (lsffn.LS_K_PRED_P1, "pred_p1"),
+                      (lsffn.LS_K_PRED_P2, "pred_p2"), (lsffn.LS_K_SELECT, "select"),
+                      (lsffn.LS_K_GATEUP, "gateup"), (lsffn.LS_K_DOWN, "down"),
+                      (lsffn.LS_K_DECODE, "decode_fused")):
+        ms, n = f.ls_kernel_timing(kid)
+        if n:
+            per_kernel[name] = {"total_ms": ms, "launches": n, "avg_us": 1e3 * ms / n}
+
+    step_s = wall / K
+    tok_s = B * K / wall
+    if B != 1:
+        raise SystemExit("bench.py reports B=1 (the headline workload)")
+    U = cfg.k
+    bytes_layer = algorithmic_bytes_per_layer(cfg, U)
+    bytes_step = bytes_layer * cfg.n_layers
+    eff_gbs = bytes_step / step_s / 1e9
+
+    # dominant kernel: the one with the largest share of time; its algorithmic bytes per launch
+    dom = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])
+    s = cfg.elem_bytes
+    per_launch_bytes = {
+        "gateup": s * (U * cfg.block * cfg.d_model * 2 + (U * cfg.block if cfg.gate_bias else 0)),
+        "down": s * U * cfg.block * cfg.d_model,
+        "pred_p1": s * cfg.d_model * cfg.rank,
+        "pred_p2": s * cfg.rank * cfg.n_blk,
+        "decode_fused": bytes_step,
+    }
+    dom_name, dom_t = dom
+    dom_bytes = per_launch_bytes.get(dom_name)
+    roofline = None
+    if dom_bytes:
+        achieved = dom_bytes / (dom_t["avg_us"] * 1e-6) / 1e9
+        roofline = {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "bytes_per_launch": dom_bytes,
+                    "avg_launch_us": round(dom_t["avg_us"], 3)}
+
+    cpu = None
+    if args.cpu_tokens > 0:
+        cpu = cpu_baseline(cfg, weights, xs, min(args.cpu_tokens, W + K))
+
+    out = {
+        "metric": "sparse-FFN decode tokens/sec and effective weight GB/s (% HBM peak), 1 GPU",
+        "value": round(tok_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(1e3 * step_s, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": lsgen.DTYPE_NAMES[cfg.dtype],
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers, d_model {cfg.d_model}, "
+                               f"d_ff {cfg.d_ff}, block {cfg.block} (k={cfg.k} of {cfg.n_blk}), "
+                               f"rank {cfg.rank}, batch {B}",
+                   "global_batch": B, "seq_len": 1, "parallelism": "none (1 GPU)"},
+        "effective_weight_GBs": round(eff_gbs, 1),
+        "hbm_frac_of_peak": round(eff_gbs / HBM_PEAK_GBS, 4),
+        "algorithmic_bytes_per_step": bytes_step,
+        "gpu_event_ms": round(gpu_ms, 3),
+        "kernels": {k: {kk: round(vv, 3) if isinstance(vv, float) else vv for kk, vv in v.items()}
+                    for k, v in per_kernel.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

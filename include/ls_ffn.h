@@ -133,8 +133,9 @@ ls_status ls_select_blocks(ls_ffn* ctx, const float* scores, int32_t B, ls_sel_m
  *   begin == 0: x_acc = x_in + y;   begin > 0: x_acc += y            (Eq. 2)
  * so after the stages [0,e1), [e1,e2), ... x_acc holds the refined feature
  * x_tilde of Eq. 2.  x_in, x_acc: dev fp32 [B, d], must not alias.
- * count: dev int32 [1].  0 <= begin <= end.  Every idx entry in range must be a
- * valid block id (not checked on the device). */
+ * count: dev int32 [1].  0 <= begin <= end.  An entry that is not a valid
+ * block id (or, with host-resident weights, not in the block cache)
+ * contributes nothing. */
 ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int32_t B,
                              const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
                              float* x_acc);
@@ -159,6 +160,52 @@ ls_status ls_decode_step(ls_ffn* ctx, float* x, int32_t B, int32_t k);
  * of the most recent ls_sparse_ffn_step into dst (dev).  LS_E_INVAL if cap is
  * smaller than what the last step produced; *n_out receives n_sel * block. */
 ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_t* n_out);
+
+/* Per-kernel timing (tracing aid).  While enabled, every kernel launch the
+ * context makes is bracketed by a pair of HIP events recorded on the context's
+ * stream.  ls_kernel_timing synchronises the stream, folds the finished event
+ * pairs into per-kernel totals and returns the total milliseconds and launch
+ * count of one kernel id since the last reset; reset != 0 clears all totals.
+ * Kernel ids: 0 MLP input, 1 predictor projection, 2 predictor head,
+ * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step. */
+enum { LS_K_PRENORM = 0, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN,
+       LS_K_DECODE, LS_K_COUNT };
+ls_status ls_set_kernel_timing(ls_ffn* ctx, int32_t enable);
+ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* total_ms,
+                           int64_t* launches);
+
+/* Tuning knobs of ls_decode_step.
+ *  LS_CFG_DECODE_PATH: 0 auto (fused kernel when the shape allows it, else the
+ *    per-kernel sequence), 1 per-kernel sequence, 2 fused kernel only
+ *    (ls_decode_step then returns LS_E_UNSUPPORTED for shapes it cannot run).
+ *  LS_CFG_SPEC_BLOCKS: blocks of the next layer the fused kernel prefetches
+ *    speculatively (its top-kp by scores predicted from the current layer's
+ *    input, Eq. 2); 0 = automatic (k + ceil(k/4)).  Never changes results.
+ *  LS_CFG_TRACE_WG: -1 (default) off; otherwise the fused kernel records
+ *    per-layer phase timestamps of that workgroup (see ls_debug_phase_trace).
+ * LS_E_INVAL on an unknown key or value. */
+enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2 };
+ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
+
+/* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for
+ * `layer`: the layer input x_l (dev fp32 [d]; layer 0 is not kept, pass NULL)
+ * and the layer's predicted block scores (dev fp32 [n_blk]).  Either pointer
+ * may be NULL.  Valid until the next ls_decode_step.  LS_E_STATE if the last
+ * ls_decode_step did not run the fused kernel. */
+ls_status ls_debug_decode_trace(ls_ffn* ctx, int32_t layer, float* x_in, float* scores);
+
+/* Debug: phase timestamps of the traced workgroup from the last fused
+ * ls_decode_step, host int64 [n_layers][16] in wall-clock ticks (100 MHz):
+ * 0 layer start, 1 input ready, 2 z published, 3 all z, 4 scores published,
+ * 5 all scores, 6 slot map, 7 activations published, 8 all activations,
+ * 9 output published, 10 gate/up done (worker), 11 down done (worker),
+ * 12 keys barrier passed, 13 control wave ranked, 14 ranking barrier passed,
+ * 15 worker ranked.  Synchronises the stream.  *n receives n_layers * 16. */
+ls_status ls_debug_phase_trace(ls_ffn* ctx, int64_t* host_out, int64_t cap, int64_t* n);
+
+/* Wait for all work enqueued on the context's stream and report a device-side
+ * failure of the fused kernel (a bounded wait that timed out) as LS_E_DEVICE. */
+ls_status ls_ffn_sync(ls_ffn* ctx);
 
 /* Text of the last failure on ctx (or of the last failed ls_ffn_create when
  * ctx is NULL); valid until the next call on ctx. */

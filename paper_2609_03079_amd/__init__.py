@@ -27,7 +27,14 @@ LS_SEL_TOPK, LS_SEL_THRESHOLD = 0, 1
 
 EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", "ls_select_blocks",
            "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step",
-           "ls_debug_last_activations", "ls_last_error")
+           "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
+           "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
+           "ls_last_error")
+LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG = 0, 1, 2
+PHASES = ("layer_start", "input_ready", "z_published", "all_z", "scores_published", "all_scores",
+          "slot_map", "acts_published", "all_acts", "output_published", "gateup_done", "down_done",
+          "keys_barrier", "ctrl_ranked", "ranked_barrier", "worker_ranked")
+LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE = range(7)
 
 
 class LsFfnDesc(ctypes.Structure):
@@ -77,6 +84,13 @@ def load():
     lib.ls_stream_weights.argtypes = [P, I32, P, I32, I32, ctypes.POINTER(LsStreamStats)]
     lib.ls_decode_step.argtypes = [P, P, I32, I32]
     lib.ls_debug_last_activations.argtypes = [P, P, I64, ctypes.POINTER(I64)]
+    lib.ls_set_kernel_timing.argtypes = [P, I32]
+    lib.ls_kernel_timing.argtypes = [P, I32, I32, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(I64)]
+    lib.ls_configure.argtypes = [P, I32, I64]
+    lib.ls_ffn_sync.argtypes = [P]
+    lib.ls_debug_decode_trace.argtypes = [P, I32, P, P]
+    lib.ls_debug_phase_trace.argtypes = [P, P, I64, ctypes.POINTER(I64)]
     lib.ls_last_error.argtypes = [P]
     lib.ls_last_error.restype = ctypes.c_char_p
     for name in EXPORTS[:-1]:
@@ -165,6 +179,34 @@ class Ffn:
 
     def ls_decode_step(self, x, B: int, k: int) -> None:
         _check(self.lib, self.ctx, self.lib.ls_decode_step(self.ctx, _ptr(x), B, k))
+
+    def ls_configure(self, key: int, value: int) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_configure(self.ctx, key, int(value)))
+
+    def ls_debug_decode_trace(self, layer: int, x_in=None, scores=None) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_debug_decode_trace(self.ctx, layer, _ptr(x_in),
+                                                                  _ptr(scores)))
+
+    def ls_debug_phase_trace(self):
+        """Phase timestamps [n_layers, 12] (100 MHz ticks) of the traced workgroup."""
+        out = np.zeros((self.n_layers, len(PHASES)), np.int64)
+        n = ctypes.c_int64()
+        _check(self.lib, self.ctx, self.lib.ls_debug_phase_trace(self.ctx, out.ctypes.data, out.size,
+                                                                 ctypes.byref(n)))
+        return out
+
+    def ls_ffn_sync(self) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_ffn_sync(self.ctx))
+
+    def ls_set_kernel_timing(self, enable: bool) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_set_kernel_timing(self.ctx, int(bool(enable))))
+
+    def ls_kernel_timing(self, kernel: int, reset: bool = False):
+        """(total milliseconds, launches) of one kernel id since the last reset."""
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        _check(self.lib, self.ctx, self.lib.ls_kernel_timing(self.ctx, kernel, int(reset),
+                                                             ctypes.byref(ms), ctypes.byref(n)))
+        return ms.value, n.value
 
     def ls_debug_last_activations(self, dst) -> int:
         n = ctypes.c_int64()

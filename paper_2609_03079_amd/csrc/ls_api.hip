@@ -10,6 +10,7 @@
 #include <thread>
 
 #include "block_cache.h"
+#include "ls_decode.h"
 #include "ls_internal.h"
 
 using ls::Shape;
@@ -56,6 +57,31 @@ struct ls_ffn {
 
     std::vector<hipEvent_t> table_uploaded;  // per layer: last slot-table upload
 
+    // kernel timing
+    bool timing = false;
+    struct Pending {
+        int kernel;
+        hipEvent_t start, stop;
+    };
+    std::vector<Pending> pending;
+    std::vector<hipEvent_t> event_pool;
+    double kernel_ms[LS_K_COUNT] = {};
+    int64_t kernel_launches[LS_K_COUNT] = {};
+
+    // fused decode kernel
+    uint64_t* mailbox = nullptr;  // tagged exchange words (device, zero-initialised)
+    size_t mailbox_words = 0;
+    ls::LayerPtrs* layer_tab = nullptr;  // device [L]
+    std::vector<ls::LayerPtrs> layer_tab_host;
+    int* dev_err = nullptr;       // device error flag
+    uint32_t epoch = 0;
+    int n_wg = 0;                 // compute units
+    int decode_path = 0;          // LS_CFG_DECODE_PATH
+    bool last_fused = false;      // the last ls_decode_step ran the fused kernel
+    int trace_wg = -1;            // LS_CFG_TRACE_WG
+    uint64_t* trace = nullptr;    // device [L][kTracePoints]
+    int spec_blocks = 0;          // LS_CFG_SPEC_BLOCKS
+
     ls_status sticky = LS_OK;
     std::string err;
 };
@@ -98,6 +124,47 @@ ls_status check_ctx(ls_ffn* c) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+hipError_t take_event(ls_ffn* c, hipEvent_t* e) {
+    if (!c->event_pool.empty()) {
+        *e = c->event_pool.back();
+        c->event_pool.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(e);
+}
+
+// Launch `fn` (returning hipError_t); when timing is on, bracket it with an event pair.
+template <typename Fn>
+hipError_t timed(ls_ffn* c, int kernel, Fn&& fn) {
+    if (!c->timing) return fn();
+    hipEvent_t a, b;
+    hipError_t e = take_event(c, &a);
+    if (e != hipSuccess) return e;
+    e = take_event(c, &b);
+    if (e != hipSuccess) return e;
+    if ((e = hipEventRecord(a, c->stream)) != hipSuccess) return e;
+    if ((e = fn()) != hipSuccess) return e;
+    if ((e = hipEventRecord(b, c->stream)) != hipSuccess) return e;
+    c->pending.push_back({kernel, a, b});
+    return hipSuccess;
+}
+
+hipError_t fold_timing(ls_ffn* c) {
+    for (auto& p : c->pending) {
+        hipError_t e = hipEventSynchronize(p.stop);
+        if (e != hipSuccess) return e;
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, p.start, p.stop);
+        if (e != hipSuccess) return e;
+        c->kernel_ms[p.kernel] += ms;
+        c->kernel_launches[p.kernel] += 1;
+        c->event_pool.push_back(p.start);
+        c->event_pool.push_back(p.stop);
+    }
+    c->pending.clear();
+    return hipSuccess;
+}
+
 // Offsets inside one layer arena.
 struct LayerLayout {
     size_t blocks, bias, p1, p2, total;
@@ -109,8 +176,8 @@ LayerLayout layout_of(const Shape& s, size_t block_bytes) {
     L.blocks = 0;
     L.bias = align_up((size_t)s.n_blk * block_bytes, 256);
     L.p1 = align_up(L.bias + (size_t)s.F * es, 256);
-    L.p2 = align_up(L.p1 + (size_t)s.r * s.d * es, 256);
-    L.total = align_up(L.p2 + (size_t)s.n_blk * s.r * es, 256);
+    L.p2 = align_up(L.p1 + (size_t)s.G * s.p1_rpw * s.d * es, 256);
+    L.total = align_up(L.p2 + (size_t)s.G * s.p2_rpw * s.r * es, 256);
     return L;
 }
 
@@ -168,7 +235,9 @@ void free_all(ls_ffn* c) {
     for (auto p : c->arena) if (p) (void)hipFree(p);
     c->arena.clear();
     for (void* p : {(void*)c->h, (void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
-                    (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables})
+                    (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
+                    (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err,
+                    (void*)c->trace})
         if (p) (void)hipFree(p);
     if (c->staging) (void)hipHostFree(c->staging);
     if (c->host_blocks) (void)hipHostFree(c->host_blocks);
@@ -177,6 +246,11 @@ void free_all(ls_ffn* c) {
     if (c->compute_done) (void)hipEventDestroy(c->compute_done);
     if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
     for (auto e : c->table_uploaded) if (e) (void)hipEventDestroy(e);
+    for (auto& p : c->pending) {
+        (void)hipEventDestroy(p.start);
+        (void)hipEventDestroy(p.stop);
+    }
+    for (auto e : c->event_pool) (void)hipEventDestroy(e);
     delete c->bcache;
 }
 
@@ -209,13 +283,23 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
     s.block_elems = (size_t)3 * s.blk * s.d;
     c->block_bytes = s.block_elems * ls::elem_size(s.dtype);
     c->stream = static_cast<hipStream_t>(desc->stream);
+    {
+        hipDeviceProp_t prop;
+        if (hipGetDevice(&c->device) != hipSuccess || hipGetDeviceProperties(&prop, c->device) != hipSuccess) {
+            delete c;
+            return fail(nullptr, LS_E_DEVICE, "no HIP device");
+        }
+        c->n_wg = prop.multiProcessorCount;
+        s.G = c->n_wg;
+        s.p1_rpw = (s.r + s.G - 1) / s.G;
+        s.p2_rpw = (s.n_blk + s.G - 1) / s.G;
+    }
     const int L = desc->n_layers, B = desc->max_batch;
     auto bail = [&](ls_status code, const std::string& m) {
         free_all(c);
         delete c;
         return fail(nullptr, code, m);
     };
-    if (hipGetDevice(&c->device) != hipSuccess) return bail(LS_E_DEVICE, "no HIP device");
     const LayerLayout lay = layout_of(s, c->block_bytes);
     c->dev.resize(L);
     c->is_set.assign(L, 0);
@@ -284,6 +368,19 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
         (void)hipGetLastError();
         return bail(LS_E_NOMEM, "workspace allocation failed");
     }
+    {
+        c->mailbox_words = ls::fused_mailbox_words(s, L);
+        c->layer_tab_host.assign(L, ls::LayerPtrs{});
+        if (dmalloc(&c->mailbox, c->mailbox_words) != hipSuccess || dmalloc(&c->layer_tab, (size_t)L) != hipSuccess ||
+            dmalloc(&c->dev_err, 1) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(LS_E_NOMEM, "fused-kernel workspace allocation failed");
+        }
+        if (hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)) != hipSuccess ||
+            hipMemset(c->dev_err, 0, sizeof(int)) != hipSuccess ||
+            hipMemset(c->layer_tab, 0, (size_t)L * sizeof(ls::LayerPtrs)) != hipSuccess)
+            return bail(LS_E_DEVICE, "workspace initialisation failed");
+    }
     *out = c;
     return LS_OK;
 }
@@ -334,14 +431,30 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
     uint8_t* sm = c->staging + off_small;
     std::memset(sm, 0, lay.p1 - lay.bias);
     if (w->b_gate) std::memcpy(sm, w->b_gate, (size_t)s.F * es);
-    std::memcpy(sm + (lay.p1 - lay.bias), w->p1, (size_t)s.r * s.d * es);
-    std::memcpy(sm + (lay.p2 - lay.bias), w->p2, (size_t)s.n_blk * s.r * es);
+    // predictor rows in the grouped order (padding rows stay zero)
+    std::memset(sm + (lay.p1 - lay.bias), 0, lay.total - lay.p1);
+    for (int i = 0; i < s.r; ++i)
+        std::memcpy(sm + (lay.p1 - lay.bias) + ((size_t)(i % s.G) * s.p1_rpw + i / s.G) * s.d * es,
+                    static_cast<const uint8_t*>(w->p1) + (size_t)i * s.d * es, (size_t)s.d * es);
+    for (int i = 0; i < s.n_blk; ++i)
+        std::memcpy(sm + (lay.p2 - lay.bias) + ((size_t)(i % s.G) * s.p2_rpw + i / s.G) * s.r * es,
+                    static_cast<const uint8_t*>(w->p2) + (size_t)i * s.r * es, (size_t)s.r * es);
     LS_HIP(c, hipMemcpyAsync(c->arena[layer], c->staging, need, hipMemcpyHostToDevice, c->stream));
     LS_HIP(c, hipStreamSynchronize(c->stream));
     c->dev[layer].bias =
         w->b_gate ? c->arena[layer] + (c->desc.residency == LS_WEIGHTS_HBM ? lay.bias : 0) : nullptr;
     c->dev[layer].threshold = w->threshold;
     if (c->desc.residency == LS_WEIGHTS_HOST) c->bcache->invalidate_layer(layer);
+    {
+        ls::LayerPtrs lp{};
+        lp.blocks = c->dev[layer].blocks;
+        lp.bias = c->dev[layer].bias;
+        lp.p1 = static_cast<const uint8_t*>(c->dev[layer].p1);
+        lp.p2 = static_cast<const uint8_t*>(c->dev[layer].p2);
+        lp.threshold = w->threshold;
+        c->layer_tab_host[layer] = lp;
+        LS_HIP(c, hipMemcpy(c->layer_tab + layer, &lp, sizeof lp, hipMemcpyHostToDevice));
+    }
     c->is_set[layer] = 1;
     return LS_OK;
 }
@@ -354,9 +467,9 @@ ls_status ls_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, float*
     if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
     if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
     const Shape& s = c->shape;
-    LS_HIP(c, ls::launch_prenorm(s, x, B, c->h, c->stream));
-    LS_HIP(c, ls::launch_gemv_rows(s.dtype, c->dev[layer].p1, s.r, s.d, c->h, B, c->z, c->stream));
-    LS_HIP(c, ls::launch_gemv_rows(s.dtype, c->dev[layer].p2, s.n_blk, s.r, c->z, B, scores, c->stream));
+    LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, x, B, c->h, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, c->dev[layer].p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, c->dev[layer].p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, scores, c->stream); }));
     return LS_OK;
 }
 
@@ -376,8 +489,9 @@ ls_status ls_select_blocks(ls_ffn* c, const float* scores, int32_t B, ls_sel_mod
     } else if (cap < n) {
         return fail(c, LS_E_INVAL, "threshold selection needs cap >= n_blk");
     }
-    LS_HIP(c, ls::launch_select(scores, B, n, (int)mode, k, tau, union_batch ? 1 : 0, cap, idx, count,
-                                c->stream));
+    LS_HIP(c, timed(c, LS_K_SELECT, [&] {
+        return ls::launch_select(scores, B, n, (int)mode, k, tau, union_batch ? 1 : 0, cap, idx, count, c->stream);
+    }));
     return LS_OK;
 }
 
@@ -416,9 +530,9 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
         st = wait_stages(c, layer, begin, end);
         if (st != LS_OK) return st;
     }
-    LS_HIP(c, ls::launch_prenorm(s, x_in, B, c->h, c->stream));
-    LS_HIP(c, ls::launch_gateup(s, L, slot_table, c->h, B, idx, count, begin, end, c->a, c->stream));
-    LS_HIP(c, ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream));
+    LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, x_in, B, c->h, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, c->h, B, idx, count, begin, end, c->a, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream); }));
     if (c->desc.residency == LS_WEIGHTS_HOST) LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
     c->last_act_n = (int64_t)end * s.blk;
     c->last_act_B = B;
@@ -511,24 +625,156 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
         if (!c->is_set[l]) return fail(c, LS_E_STATE, "layer weights not set");
     if (c->desc.residency != LS_WEIGHTS_HBM)
         return fail(c, LS_E_UNSUPPORTED, "ls_decode_step needs HBM-resident weights; use the per-layer calls");
+    if (c->decode_path != 1) {
+        int kp = c->spec_blocks > 0 ? c->spec_blocks : k + (k + 3) / 4;
+        kp = std::min(kp, ls::fused_max_spec(s, c->n_wg));
+        kp = std::max(kp, k);
+        const ls::FusedSupport sup = ls::fused_supported(s, B, k, kp, c->n_wg, c->desc.n_layers);
+        if (sup.ok) {
+            if (c->epoch == 0xffffffffu) {  // epoch tags wrap: clear the mailboxes first
+                LS_HIP(c, hipStreamSynchronize(c->stream));
+                LS_HIP(c, hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)));
+                c->epoch = 0;
+            }
+            ls::FusedArgs a{};
+            a.layers = c->layer_tab;
+            a.L = c->desc.n_layers;
+            a.d = s.d;
+            a.r = s.r;
+            a.nb = s.n_blk;
+            a.blk = s.blk;
+            a.F = s.F;
+            a.k = k;
+            a.kp = kp;
+            a.prenorm = s.prenorm;
+            a.block_bytes = c->block_bytes;
+            a.x = x;
+            const size_t L = (size_t)c->desc.n_layers;
+            a.xmb = c->mailbox;
+            a.zmb = a.xmb + L * s.d;
+            a.smb = a.zmb + L * 2 * s.r;
+            a.amb = a.smb + L * 2 * s.n_blk;
+            a.tag = ++c->epoch;
+            a.err = c->dev_err;
+            a.trace = c->trace_wg >= 0 ? c->trace : nullptr;
+            a.trace_wg = c->trace_wg;
+            LS_HIP(c, timed(c, LS_K_DECODE, [&] { return ls::launch_decode_fused(s, a, c->n_wg, c->stream); }));
+            c->last_fused = true;
+            c->last_act_n = 0;
+            c->last_act_B = 0;
+            return LS_OK;
+        }
+        if (c->decode_path == 2) return fail(c, LS_E_UNSUPPORTED, std::string("fused decode: ") + sup.why);
+    }
+    c->last_fused = false;
     const int cap = B > 1 ? std::min(s.n_blk, B * k) : k;
     float* cur = x;
     float* nxt = c->xbuf;
     for (int l = 0; l < c->desc.n_layers; ++l) {
         const ls::LayerDev& L = c->dev[l];
-        LS_HIP(c, ls::launch_prenorm(s, cur, B, c->h, c->stream));
-        LS_HIP(c, ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, c->h, B, c->z, c->stream));
-        LS_HIP(c, ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, c->z, B, c->scores, c->stream));
-        LS_HIP(c, ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count,
-                                    c->stream));
-        LS_HIP(c, ls::launch_gateup(s, L, nullptr, c->h, B, c->idx, c->count, 0, cap, c->a, c->stream));
-        LS_HIP(c, ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->stream));
+        LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, cur, B, c->h, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, c->scores, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_SELECT, [&] {
+            return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count, c->stream);
+        }));
+        LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, nullptr, c->h, B, c->idx, c->count, 0, cap, c->a, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->stream); }));
         std::swap(cur, nxt);
     }
     if (cur != x)
         LS_HIP(c, hipMemcpyAsync(x, cur, (size_t)B * s.d * sizeof(float), hipMemcpyDeviceToDevice, c->stream));
     c->last_act_n = (int64_t)cap * s.blk;
     c->last_act_B = B;
+    return LS_OK;
+}
+
+ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (key == LS_CFG_DECODE_PATH) {
+        if (value < 0 || value > 2) return fail(c, LS_E_INVAL, "decode path must be 0, 1 or 2");
+        c->decode_path = (int)value;
+        return LS_OK;
+    }
+    if (key == LS_CFG_TRACE_WG) {
+        if (value < -1 || value >= c->n_wg) return fail(c, LS_E_INVAL, "trace workgroup out of range");
+        if (value >= 0 && !c->trace) {
+            const size_t n = (size_t)c->desc.n_layers * ls::kTracePoints;
+            LS_HIP(c, hipMalloc(reinterpret_cast<void**>(&c->trace), n * sizeof(uint64_t)));
+            LS_HIP(c, hipMemset(c->trace, 0, n * sizeof(uint64_t)));
+        }
+        c->trace_wg = (int)value;
+        return LS_OK;
+    }
+    if (key == LS_CFG_SPEC_BLOCKS) {
+        if (value < 0 || value > c->shape.n_blk) return fail(c, LS_E_INVAL, "speculative width out of range");
+        c->spec_blocks = (int)value;
+        return LS_OK;
+    }
+    return fail(c, LS_E_INVAL, "unknown configuration key");
+}
+
+ls_status ls_debug_decode_trace(ls_ffn* c, int32_t layer, float* x_in, float* scores) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!c->last_fused) return fail(c, LS_E_STATE, "the last ls_decode_step did not run the fused kernel");
+    const size_t L = (size_t)c->desc.n_layers;
+    const uint64_t* xmb = c->mailbox;
+    const uint64_t* smb = xmb + L * s.d + L * 2 * s.r;
+    if (x_in) {
+        if (layer == 0) return fail(c, LS_E_INVAL, "layer 0 input is the caller's own x");
+        LS_HIP(c, ls::launch_untag(xmb + (size_t)layer * s.d, s.d, x_in, c->stream));
+    }
+    if (scores) LS_HIP(c, ls::launch_untag(smb + (size_t)layer * 2 * s.n_blk, s.n_blk, scores, c->stream));
+    return LS_OK;
+}
+
+ls_status ls_debug_phase_trace(ls_ffn* c, int64_t* host_out, int64_t cap, int64_t* n) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (!host_out || !n) return fail(c, LS_E_INVAL, "null pointer");
+    const int64_t total = (int64_t)c->desc.n_layers * ls::kTracePoints;
+    *n = total;
+    if (!c->trace) return fail(c, LS_E_STATE, "tracing was never enabled (LS_CFG_TRACE_WG)");
+    if (cap < total) return fail(c, LS_E_INVAL, "cap too small");
+    LS_HIP(c, hipStreamSynchronize(c->stream));
+    LS_HIP(c, hipMemcpy(host_out, c->trace, (size_t)total * sizeof(int64_t), hipMemcpyDeviceToHost));
+    return LS_OK;
+}
+
+ls_status ls_ffn_sync(ls_ffn* c) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    LS_HIP(c, hipStreamSynchronize(c->stream));
+    int e = 0;
+    LS_HIP(c, hipMemcpy(&e, c->dev_err, sizeof e, hipMemcpyDeviceToHost));
+    if (e) return fail(c, LS_E_DEVICE, "a bounded wait in the fused decode kernel timed out");
+    return LS_OK;
+}
+
+ls_status ls_set_kernel_timing(ls_ffn* c, int32_t enable) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    c->timing = enable != 0;
+    return LS_OK;
+}
+
+ls_status ls_kernel_timing(ls_ffn* c, int32_t kernel, int32_t reset, double* total_ms,
+                           int64_t* launches) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (kernel < 0 || kernel >= LS_K_COUNT) return fail(c, LS_E_INVAL, "kernel id out of range");
+    LS_HIP(c, fold_timing(c));
+    if (total_ms) *total_ms = c->kernel_ms[kernel];
+    if (launches) *launches = c->kernel_launches[kernel];
+    if (reset)
+        for (int i = 0; i < LS_K_COUNT; ++i) {
+            c->kernel_ms[i] = 0.0;
+            c->kernel_launches[i] = 0;
+        }
     return LS_OK;
 }
 

@@ -1,0 +1,53 @@
+// ls_decode.h - the fused decode-step kernel (one persistent launch per token).
+#pragma once
+
+#include "ls_internal.h"
+
+namespace ls {
+
+// Device view of one layer for the fused kernel.
+struct LayerPtrs {
+    const uint8_t* blocks;  // n_blk blocks of block_bytes
+    const void* bias;       // [F] or null
+    const uint8_t* p1;      // [r, d]
+    const uint8_t* p2;      // [n_blk, r]
+    float threshold;
+    float pad_;
+};
+
+struct FusedArgs {
+    const LayerPtrs* layers;  // device [L]
+    int L, d, r, nb, blk, F, k, kp, prenorm;
+    size_t block_bytes;
+    float* x;                 // [d]: input at entry, output at exit
+    uint64_t* xmb;            // [L][d]      tagged x of every layer input (row 0: the input)
+    uint64_t* zmb;            // [L][2r]     tagged z (exact | speculative next layer)
+    uint64_t* smb;            // [L][2 n_blk] tagged scores (exact | speculative)
+    uint64_t* amb;            // [L][F]      tagged activations in priority-list order
+    uint32_t tag;             // launch epoch (>= 1)
+    int* err;                 // set to 1 when a wait exceeded its spin limit
+    uint64_t* trace;          // null, or [L][kTracePoints] wall-clock stamps of one workgroup
+    int trace_wg;
+};
+
+constexpr int kTracePoints = 16;
+
+// Shapes the fused kernel handles (others use the per-kernel path).
+struct FusedSupport {
+    bool ok;
+    const char* why;
+};
+FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int L);
+
+// Largest speculative width (blocks prefetched for the next layer) the fused kernel holds.
+int fused_max_spec(const Shape& s, int n_wg);
+
+// Number of 64-bit mailbox words the fused kernel needs for L layers.
+size_t fused_mailbox_words(const Shape& s, int L);
+
+// dst[i] = value bits of the tagged words src[0..n)
+hipError_t launch_untag(const uint64_t* src, int n, float* dst, hipStream_t st);
+
+hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st);
+
+}  // namespace ls

@@ -38,12 +38,16 @@ struct Shape {
     ls_act act;
     int prenorm;
     size_t block_elems;  // 3 * blk * d
+    // Predictor rows are stored grouped by workgroup: logical row i of P1 (P2) sits at
+    // storage row (i % G) * p1_rpw + i / G  ((i % G) * p2_rpw + i / G).
+    int G, p1_rpw, p2_rpw;
 };
 
 // ---- kernel launchers (ls_kernels.hip) -------------------------------------------------
 hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st);
-hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, const float* v, int B,
-                            float* out, hipStream_t st);
+// out[b, i] = W[s(i), :] . v[b, :] with s(i) = (i % G) * rpw + i / G (the grouped row order)
+hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G, int rpw,
+                            const float* v, int B, float* out, hipStream_t st);
 hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st);
 // slot_table: null in resident mode (block b lives at blocks + b*block_bytes); else

@@ -12,84 +12,11 @@
 //             selected blocks, so no partial sums leave the workgroup.
 //
 // Every reduction has a fixed order: results are bitwise reproducible.
+#include "ls_device.h"
 #include "ls_internal.h"
 
 namespace ls {
 namespace {
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-// ---- weight storage types: V elements per 16-byte vector, widened to fp32 -------------
-template <ls_dtype T>
-struct Wt;
-
-template <>
-struct Wt<LS_F32> {
-    static constexpr int V = 4;
-    static constexpr int kBytes = 4;
-    __device__ static inline void widen(const u32x4& r, float* o) {
-        o[0] = __uint_as_float(r.x);
-        o[1] = __uint_as_float(r.y);
-        o[2] = __uint_as_float(r.z);
-        o[3] = __uint_as_float(r.w);
-    }
-    __device__ static inline float scalar(const void* p, size_t i) {
-        return static_cast<const float*>(p)[i];
-    }
-};
-
-__device__ inline float half_bits_to_float(unsigned int bits16) {
-    unsigned short s = static_cast<unsigned short>(bits16);
-    return static_cast<float>(__builtin_bit_cast(_Float16, s));
-}
-
-template <>
-struct Wt<LS_F16> {
-    static constexpr int V = 8;
-    static constexpr int kBytes = 2;
-    __device__ static inline void widen(const u32x4& r, float* o) {
-        o[0] = half_bits_to_float(r.x & 0xffffu);
-        o[1] = half_bits_to_float(r.x >> 16);
-        o[2] = half_bits_to_float(r.y & 0xffffu);
-        o[3] = half_bits_to_float(r.y >> 16);
-        o[4] = half_bits_to_float(r.z & 0xffffu);
-        o[5] = half_bits_to_float(r.z >> 16);
-        o[6] = half_bits_to_float(r.w & 0xffffu);
-        o[7] = half_bits_to_float(r.w >> 16);
-    }
-    __device__ static inline float scalar(const void* p, size_t i) {
-        return half_bits_to_float(static_cast<const unsigned short*>(p)[i]);
-    }
-};
-
-template <>
-struct Wt<LS_BF16> {
-    static constexpr int V = 8;
-    static constexpr int kBytes = 2;
-    // bfloat16 is the upper half of a binary32: widening is a shift.
-    __device__ static inline void widen(const u32x4& r, float* o) {
-        o[0] = __uint_as_float(r.x << 16);
-        o[1] = __uint_as_float(r.x & 0xffff0000u);
-        o[2] = __uint_as_float(r.y << 16);
-        o[3] = __uint_as_float(r.y & 0xffff0000u);
-        o[4] = __uint_as_float(r.z << 16);
-        o[5] = __uint_as_float(r.z & 0xffff0000u);
-        o[6] = __uint_as_float(r.w << 16);
-        o[7] = __uint_as_float(r.w & 0xffff0000u);
-    }
-    __device__ static inline float scalar(const void* p, size_t i) {
-        return __uint_as_float(static_cast<unsigned int>(static_cast<const unsigned short*>(p)[i]) << 16);
-    }
-};
-
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-__device__ inline u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
 
 // ---- MLP input --------------------------------------------------------------------------
 // h = x (no prenorm) or h = x / sqrt(mean(x^2) + 1e-6).  One workgroup per token; the sum of
@@ -117,7 +44,8 @@ __global__ __launch_bounds__(256) void prenorm_kernel(const float* __restrict__ 
 // ---- GEMV over rows: out[b, row] = sum_c W[row, c] * v[b, c] ------------------------------
 template <ls_dtype T, int B>
 __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
-                                                        int cols, const float* __restrict__ v,
+                                                        int cols, int G, int rpw,
+                                                        const float* __restrict__ v,
                                                         float* __restrict__ out) {
     constexpr int V = Wt<T>::V;
     constexpr int U = 8;  // 16-byte loads in flight per lane
@@ -125,7 +53,8 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows) return;
     const int nchunk = cols / V;
-    const u32x4* wr = reinterpret_cast<const u32x4*>(W + (size_t)row * cols * Wt<T>::kBytes);
+    const int srow = (row % G) * rpw + row / G;
+    const u32x4* wr = reinterpret_cast<const u32x4*>(W + (size_t)srow * cols * Wt<T>::kBytes);
     float acc[B];
 #pragma unroll
     for (int b = 0; b < B; ++b) acc[b] = 0.f;
@@ -165,15 +94,6 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
 }
 
 // ---- block selection --------------------------------------------------------------------
-// Order-preserving map of a binary32 score to uint32: NaN -> 0 (below every number),
-// -0 -> +0, otherwise a monotone bit transform.  Ties are broken by the smaller index.
-__device__ inline uint32_t order_key(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
-    if (u == 0x80000000u) u = 0u;
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ scores, int B,
                                                       int n, int mode, int k, float tau,
                                                       int union_batch, int cap,
@@ -418,30 +338,30 @@ hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipSt
 }
 
 template <ls_dtype T>
-static hipError_t gemv_t(const void* W, int rows, int cols, const float* v, int B, float* out,
-                         hipStream_t st) {
+static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, const float* v, int B,
+                         float* out, hipStream_t st) {
     const dim3 grid((rows + 3) / 4), blk(256);
     const uint8_t* w = static_cast<const uint8_t*>(W);
     switch (B) {
-        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7>), grid, blk, 0, st, w, rows, cols, v, out); break;
-        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8>), grid, blk, 0, st, w, rows, cols, v, out); break;
+        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, const float* v, int B,
-                            float* out, hipStream_t st) {
+hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G, int rpw,
+                            const float* v, int B, float* out, hipStream_t st) {
     switch (t) {
-        case LS_F32: return gemv_t<LS_F32>(W, rows, cols, v, B, out, st);
-        case LS_F16: return gemv_t<LS_F16>(W, rows, cols, v, B, out, st);
-        case LS_BF16: return gemv_t<LS_BF16>(W, rows, cols, v, B, out, st);
+        case LS_F32: return gemv_t<LS_F32>(W, rows, cols, G, rpw, v, B, out, st);
+        case LS_F16: return gemv_t<LS_F16>(W, rows, cols, G, rpw, v, B, out, st);
+        case LS_BF16: return gemv_t<LS_BF16>(W, rows, cols, G, rpw, v, B, out, st);
     }
     return hipErrorInvalidValue;
 }
