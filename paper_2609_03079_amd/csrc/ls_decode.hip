@@ -11,7 +11,7 @@
 //
 // One workgroup per compute unit (cooperative launch, all resident).  Wave 0
 // of every workgroup is the control wave: it waits for values published by
-// other workgroups and publishes this workgroup's results.  Waves 1..7 are
+// other workgroups and publishes this workgroup's results.  Waves 1..3 are
 // worker waves: they hold prefetched weights in registers and compute.  The
 // control wave never has weight loads in flight, so its waits are not held up
 // by the in-order completion of the workers' streaming loads.
@@ -49,7 +49,7 @@ constexpr int kDnPer = 2;               // 16-byte down chunks per lane per posi
 constexpr int kMaxDn = kDnPos * kDnPer;
 constexpr int kMaxD = 4096;
 constexpr int kMaxR = 1024;
-constexpr int kMaxNb = 512;
+constexpr int kMaxNb = 256;
 constexpr int kMaxKp = 64;
 constexpr int kMaxA = 4096;             // k * block
 constexpr int kMaxRowsPerWg = 8;        // predictor rows per workgroup
@@ -201,51 +201,60 @@ __device__ __forceinline__ void z_rows(Smem& sm, const Geo g, int l, bool last, 
     }
 }
 
-// Number of keys among keys[j0 .. j0 + cnt) larger than K (16-byte LDS reads, two keys each).
-__device__ __forceinline__ int count_above(const uint64_t* keys, int j0, int cnt, uint64_t K) {
-    const ulonglong2* k2 = reinterpret_cast<const ulonglong2*>(keys + j0);
-    int c = 0;
-#pragma unroll 4
-    for (int j = 0; j < cnt / 2; ++j) {
-        const ulonglong2 kv = k2[j];
-        c += (kv.x > K) + (kv.y > K);
-    }
-    return c;
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
 }
 
-// Exact top-k of layer l into E and (unless last) the speculative top-kp of layer l+1
-// into Pn.  The rank of element i is the number of larger composite keys; every element's
-// scan is split between two adjacent lanes whose counts are added with a DPP pair swap.
-// All threads run the same number of rounds so the DPP sees full waves.
-__device__ __forceinline__ void rank_all(Smem& sm, const Geo g, bool last, int* Pn, int tid) {
-    const int nbp = (g.nb + 1) & ~1;  // even, the keys are padded with 0
-    const int half = nbp / 2;         // even split point (nbp/2 may be odd: handled below)
-    const int lists = last ? 1 : 2;
-    const int tasks = lists * 2 * nbp;
-    const int rounds = (tasks + kThreads - 1) / kThreads;
-    for (int r = 0; r < rounds; ++r) {
-        const int t = r * kThreads + tid;
-        const bool valid = t < tasks;
-        const int list = valid ? t / (2 * nbp) : 0;
-        const int rem = t % (2 * nbp);
-        const int i = rem >> 1, part = rem & 1;
-        const uint64_t* keys = sm.key[list];
-        int c = 0;
-        if (valid && i < g.nb) {
-            const uint64_t K = keys[i];
-            // part 0 scans [0, h0), part 1 scans [h0, nbp); h0 even for the paired reads
-            const int h0 = half & ~1;
-            c = part == 0 ? count_above(keys, 0, h0, K) : count_above(keys, h0, nbp - h0, K);
-        }
-        c += __builtin_amdgcn_update_dpp(0, c, 0xb1, 0xf, 0xf, false);  // quad_perm [1,0,3,2]
-        if (valid && part == 0 && i < g.nb) {
-            if (list == 0) {
-                if (c < g.k) sm.E[c] = i;
-            } else if (c < g.kp) {
-                Pn[c] = i;
-            }
-        }
+// Top-m set of one list, run by one wave without LDS traffic.  The priority order is the
+// composite key (order_key << 32 | ~index): larger first.  A bitwise search from the top
+// bit finds T, the m-th largest order key (the largest T with at least m keys >= T); the
+// set is every key > T plus the elements equal to T with the smallest indices.  Members
+// are written to out[] in index order (the set is what matters to the fused step; its
+// summation order is fixed by the slot map).  Needs 1 <= m <= n.
+__device__ __forceinline__ void top_set(const uint64_t* keys, int n, int m, int* out, int lane) {
+    constexpr int Q = kMaxNb / 64;
+    uint32_t ok[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int i = q * 64 + lane;
+        ok[q] = i < n ? (uint32_t)(keys[i] >> 32) : 0u;  // padding compares below every c >= 1
     }
+    uint32_t T = 0u;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t c = T | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) cnt += __popcll(__ballot(ok[q] >= c));
+        if (cnt >= m) T = c;
+    }
+    int gt = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) gt += __popcll(__ballot(ok[q] > T));
+    const int rem = m - gt;  // elements equal to T that are taken (>= 1)
+    const uint64_t below = (1ull << lane) - 1ull;
+    int eq_before = 0, mem_before = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int i = q * 64 + lane;
+        const bool valid = i < n;
+        const bool eq = valid && ok[q] == T;
+        const uint64_t eqb = __ballot(eq);
+        const bool mem = valid && (ok[q] > T || (eq && eq_before + __popcll(eqb & below) < rem));
+        const uint64_t memb = __ballot(mem);
+        if (mem) out[mem_before + __popcll(memb & below)] = i;
+        eq_before += __popcll(eqb);
+        mem_before += __popcll(memb);
+    }
+}
+
+// Exact top-k of layer l into E (wave 0) and, unless last, the speculative top-kp of layer
+// l+1 into Pn (wave 1).
+__device__ __forceinline__ void rank_all(Smem& sm, const Geo g, bool last, int* Pn, int wave,
+                                         int lane) {
+    if (wave == 0) top_set(sm.key[0], g.nb, g.k, sm.E, lane);
+    else if (wave == 1 && !last) top_set(sm.key[1], g.nb, g.kp, Pn, lane);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -332,7 +341,7 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         LS_STAMP(P, g, l, 5, lane == 0);
         lds_barrier();  // 7: keys ready
         LS_STAMP(P, g, l, 12, lane == 0);
-        rank_all(sm, g, last, Pn, lane);
+        rank_all(sm, g, last, Pn, 0, lane);
         LS_STAMP(P, g, l, 13, lane == 0);
         lds_barrier();  // 8: E and the speculative list ready
         LS_STAMP(P, g, l, 14, lane == 0);
@@ -416,7 +425,6 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
     constexpr int D = NC * V * 64;
     constexpr int CPR = D / V;
     const int wl = (wave - 1) * 64 + lane;
-    const int tid = wave * 64 + lane;
     const size_t row_bytes = (size_t)D * KB;
     const size_t down_off = 2 * (size_t)g.blk * row_bytes + (size_t)g.w * g.blk * kColTile * KB;
     const size_t bb = P.block_bytes;
@@ -517,7 +525,7 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         lds_barrier();  // 6
         if (l + 2 < g.L) load_p2(l + 2);
         lds_barrier();  // 7: keys ready
-        rank_all(sm, g, last, const_cast<int*>(Pn), tid);
+        rank_all(sm, g, last, const_cast<int*>(Pn), wave, lane);
         LS_STAMP(P, g, l, 15, wave == 1 && lane == 0);
         lds_barrier();  // 8
         lds_barrier();  // 9: slot map ready
