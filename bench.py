@@ -1,8 +1,9 @@
 """Sparse-FFN decode benchmark on one MI355X.
 
 One step = one decode step of one token through every layer of the FFN stack:
-predictor (P1, P2) -> top-k block selection -> gate/up row gather + gating ->
-down projection + residual, all in the HIP kernels behind the C ABI.
+predictor (the fp32 product P2 P1 when that is smaller than the two factors) ->
+top-k block selection -> gate/up row gather + gating -> down projection +
+residual, all in the HIP kernels behind the C ABI.
 
 Workload (default): Llama-2-7B-shaped FFN stack, 32 layers, d_model 4096,
 d_ff 11008, fp16 weights, ReGLU with ~10% active neurons, rank-1024 predictor,
@@ -29,14 +30,21 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 
 
+def predictor_bytes(cfg) -> int:
+    """Bytes of one layer's predictor as the library stores it: the fp32 product P2 P1
+    [n_blk, d] when that is no larger than the factors P1 [r, d] and P2 [n_blk, r]."""
+    folded = 4 * cfg.n_blk * cfg.d_model
+    factored = cfg.elem_bytes * (cfg.rank * cfg.d_model + cfg.n_blk * cfg.rank)
+    return min(folded, factored)
+
+
 def algorithmic_bytes_per_layer(cfg, U: int, Z: int = 0) -> int:
     """Bytes one layer must read: the U selected blocks' gate/up/down rows (minus Z blocks whose
-    down rows are skipped as all-zero), their gate bias, and the predictor factors."""
+    down rows are skipped as all-zero), their gate bias, and the predictor."""
     s = cfg.elem_bytes
     ffn = U * cfg.block * cfg.d_model * 3 - Z * cfg.block * cfg.d_model
     bias = U * cfg.block if cfg.gate_bias is not None else 0
-    pred = cfg.d_model * cfg.rank + cfg.rank * cfg.n_blk
-    return s * (ffn + bias + pred)
+    return s * (ffn + bias) + predictor_bytes(cfg)
 
 
 def cpu_baseline(cfg, weights, xs, n_tokens: int):
@@ -144,7 +152,8 @@ def main() -> int:
     per_launch_bytes = {
         "gateup": s * (U * cfg.block * cfg.d_model * 2 + (U * cfg.block if cfg.gate_bias else 0)),
         "down": s * U * cfg.block * cfg.d_model,
-        "pred_p1": s * cfg.d_model * cfg.rank,
+        "pred_p1": predictor_bytes(cfg) if predictor_bytes(cfg) < s * (cfg.d_model * cfg.rank + cfg.rank * cfg.n_blk)
+                   else s * cfg.d_model * cfg.rank,
         "pred_p2": s * cfg.rank * cfg.n_blk,
         "decode_fused": bytes_step,
     }

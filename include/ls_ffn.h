@@ -108,8 +108,13 @@ ls_status ls_ffn_set_layer(ls_ffn* ctx, int32_t layer, const ls_layer_weights* w
 /* Release everything the context owns.  Synchronises the stream. */
 ls_status ls_ffn_destroy(ls_ffn* ctx);
 
-/* Predictor (Sec. 3.3.3): h = prenorm(x); z = P1 h; scores = P2 z.
- * x: dev fp32 [B, d]; scores: dev fp32 [B, n_blk].  1 <= B <= max_batch. */
+/* Predictor (Sec. 3.3.3): h = prenorm(x); scores = P2 (P1 h).
+ * x: dev fp32 [B, d]; scores: dev fp32 [B, n_blk].  1 <= B <= max_batch.
+ * When the product is no larger than the factors (4 n_blk d bytes against
+ * (r d + n_blk r) weight-type bytes) the context keeps Pf = P2 P1, formed once
+ * by ls_ffn_set_layer with fp64 accumulation and rounded to fp32, and applies
+ * it as one GEMV; otherwise it applies P1, then P2.  Either way the scores are
+ * the same function of x up to fp32 rounding. */
 ls_status ls_predict(ls_ffn* ctx, int32_t layer, const float* x, int32_t B, float* scores);
 
 /* Block selection over dev fp32 scores [B, n_blk] (priority list, Sec. 2.1).
@@ -166,7 +171,8 @@ ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_
  * stream.  ls_kernel_timing synchronises the stream, folds the finished event
  * pairs into per-kernel totals and returns the total milliseconds and launch
  * count of one kernel id since the last reset; reset != 0 clears all totals.
- * Kernel ids: 0 MLP input, 1 predictor projection, 2 predictor head,
+ * Kernel ids: 0 MLP input, 1 predictor projection (or the folded predictor),
+ * 2 predictor head (not launched when the predictor is folded),
  * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step. */
 enum { LS_K_PRENORM = 0, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN,
        LS_K_DECODE, LS_K_COUNT };
@@ -180,7 +186,8 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    (ls_decode_step then returns LS_E_UNSUPPORTED for shapes it cannot run).
  *  LS_CFG_SPEC_BLOCKS: blocks of the next layer the fused kernel prefetches
  *    speculatively (its top-kp by scores predicted from the current layer's
- *    input, Eq. 2); 0 = automatic (k + ceil(k/4)).  Never changes results.
+ *    input, Eq. 2); 0 = automatic (2k, or fewer when the kernel's neuron slots
+ *    hold fewer).  Never changes results.
  *  LS_CFG_TRACE_WG: -1 (default) off; otherwise the fused kernel records
  *    per-layer phase timestamps of that workgroup (see ls_debug_phase_trace).
  * LS_E_INVAL on an unknown key or value. */
@@ -196,11 +203,11 @@ ls_status ls_debug_decode_trace(ls_ffn* ctx, int32_t layer, float* x_in, float* 
 
 /* Debug: phase timestamps of the traced workgroup from the last fused
  * ls_decode_step, host int64 [n_layers][16] in wall-clock ticks (100 MHz):
- * 0 layer start, 1 input ready, 2 z published, 3 all z, 4 scores published,
- * 5 all scores, 6 slot map, 7 activations published, 8 all activations,
- * 9 output published, 10 gate/up done (worker), 11 down done (worker),
- * 12 keys barrier passed, 13 control wave ranked, 14 ranking barrier passed,
- * 15 worker ranked.  Synchronises the stream.  *n receives n_layers * 16. */
+ * 0 layer start, 1 input ready, 2 scores published, 3 all scores,
+ * 4 keys barrier passed, 5 control wave ranked, 6 slot map,
+ * 7 activations published, 8 all activations, 9 output published,
+ * 10 miss gate/up done (worker), 11 down done (worker), 12 worker ranked,
+ * 13 speculative gate/up done (worker), 14-15 unused (0).  Synchronises the stream.  *n receives n_layers * 16. */
 ls_status ls_debug_phase_trace(ls_ffn* ctx, int64_t* host_out, int64_t cap, int64_t* n);
 
 /* Wait for all work enqueued on the context's stream and report a device-side

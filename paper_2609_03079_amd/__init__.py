@@ -31,9 +31,9 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
 LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG = 0, 1, 2
-PHASES = ("layer_start", "input_ready", "z_published", "all_z", "scores_published", "all_scores",
-          "slot_map", "acts_published", "all_acts", "output_published", "gateup_done", "down_done",
-          "keys_barrier", "ctrl_ranked", "ranked_barrier", "worker_ranked")
+PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "keys_barrier",
+          "ctrl_ranked", "slot_map", "acts_published", "all_acts", "output_published", "gateup_done",
+          "down_done", "worker_ranked", "early_gateup_done", "spare14", "spare15")
 LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE = range(7)
 
 
@@ -188,7 +188,7 @@ class Ffn:
                                                                   _ptr(scores)))
 
     def ls_debug_phase_trace(self):
-        """Phase timestamps [n_layers, 12] (100 MHz ticks) of the traced workgroup."""
+        """Phase timestamps [n_layers, 16] (100 MHz ticks) of the traced workgroup (see PHASES)."""
         out = np.zeros((self.n_layers, len(PHASES)), np.int64)
         n = ctypes.c_int64()
         _check(self.lib, self.ctx, self.lib.ls_debug_phase_trace(self.ctx, out.ctypes.data, out.size,

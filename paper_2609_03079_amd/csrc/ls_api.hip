@@ -22,10 +22,10 @@ struct ls_ffn {
     hipStream_t stream = nullptr;
     hipStream_t copy_stream = nullptr;
     size_t block_bytes = 0;
-    size_t layer_bytes = 0;  // blocks + bias + p1 + p2 (resident arena of one layer)
+    size_t layer_bytes = 0;  // blocks + bias + predictor (resident arena of one layer)
 
     // per layer
-    std::vector<uint8_t*> arena;  // device: [blocks][bias][p1][p2]  (resident mode)
+    std::vector<uint8_t*> arena;  // device: [blocks][bias][predictor]  (resident mode)
     std::vector<ls::LayerDev> dev;
     std::vector<uint8_t> is_set;
 
@@ -165,9 +165,10 @@ hipError_t fold_timing(ls_ffn* c) {
     return hipSuccess;
 }
 
-// Offsets inside one layer arena.
+// Offsets inside one layer arena.  The predictor region holds either the folded fp32
+// product [n_blk, d] (pf) or the two factors in the grouped row order (p1, then p2).
 struct LayerLayout {
-    size_t blocks, bias, p1, p2, total;
+    size_t blocks, bias, p1, p2, pf, total;
 };
 
 LayerLayout layout_of(const Shape& s, size_t block_bytes) {
@@ -175,9 +176,13 @@ LayerLayout layout_of(const Shape& s, size_t block_bytes) {
     LayerLayout L{};
     L.blocks = 0;
     L.bias = align_up((size_t)s.n_blk * block_bytes, 256);
-    L.p1 = align_up(L.bias + (size_t)s.F * es, 256);
-    L.p2 = align_up(L.p1 + (size_t)s.G * s.p1_rpw * s.d * es, 256);
-    L.total = align_up(L.p2 + (size_t)s.G * s.p2_rpw * s.r * es, 256);
+    L.p1 = L.p2 = L.pf = align_up(L.bias + (size_t)s.F * es, 256);
+    if (s.fold) {
+        L.total = align_up(L.pf + (size_t)s.n_blk * s.d * sizeof(float), 256);
+    } else {
+        L.p2 = align_up(L.p1 + (size_t)s.G * s.p1_rpw * s.d * es, 256);
+        L.total = align_up(L.p2 + (size_t)s.G * s.p2_rpw * s.r * es, 256);
+    }
     return L;
 }
 
@@ -294,6 +299,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
         s.p1_rpw = (s.r + s.G - 1) / s.G;
         s.p2_rpw = (s.n_blk + s.G - 1) / s.G;
     }
+    s.fold = ls::predictor_folds(s.d, s.r, s.n_blk, s.dtype);
     const int L = desc->n_layers, B = desc->max_batch;
     auto bail = [&](ls_status code, const std::string& m) {
         free_all(c);
@@ -315,6 +321,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             c->dev[l].bias = c->arena[l] + lay.bias;
             c->dev[l].p1 = c->arena[l] + lay.p1;
             c->dev[l].p2 = c->arena[l] + lay.p2;
+            c->dev[l].pf = reinterpret_cast<const float*>(c->arena[l] + lay.pf);
         }
     } else {
         // predictors and bias stay resident in HBM; the blocks live in pinned host memory and
@@ -331,6 +338,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             c->dev[l].bias = c->arena[l];
             c->dev[l].p1 = c->arena[l] + (lay.p1 - lay.bias);
             c->dev[l].p2 = c->arena[l] + (lay.p2 - lay.bias);
+            c->dev[l].pf = reinterpret_cast<const float*>(c->arena[l] + (lay.pf - lay.bias));
         }
         const size_t host_bytes = (size_t)L * s.n_blk * c->block_bytes;
         if (hipHostMalloc(reinterpret_cast<void**>(&c->host_blocks), host_bytes, hipHostMallocDefault) != hipSuccess) {
@@ -361,7 +369,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             if (hipEventCreateWithFlags(&c->table_uploaded[l], hipEventDisableTiming) != hipSuccess)
                 return bail(LS_E_DEVICE, "event creation failed");
     }
-    if (dmalloc(&c->h, (size_t)B * s.d) != hipSuccess || dmalloc(&c->z, (size_t)B * s.r) != hipSuccess ||
+    if (dmalloc(&c->h, (size_t)B * s.d) != hipSuccess || dmalloc(&c->z, (size_t)B * (s.fold ? 1 : s.r)) != hipSuccess ||
         dmalloc(&c->scores, (size_t)B * s.n_blk) != hipSuccess ||
         dmalloc(&c->idx, (size_t)B * s.n_blk) != hipSuccess || dmalloc(&c->count, (size_t)B) != hipSuccess ||
         dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess) {
@@ -405,7 +413,10 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
         return fail(c, LS_E_INVAL, "null weight pointer");
     const size_t es = ls::elem_size(s.dtype);
     const LayerLayout lay = layout_of(s, c->block_bytes);
-    const size_t need = c->desc.residency == LS_WEIGHTS_HBM ? lay.total : lay.total - lay.bias;
+    // staged bytes: blocks (resident mode), bias and the factored predictor; the folded
+    // predictor is formed on the device instead
+    const size_t staged_end = s.fold ? lay.pf : lay.total;
+    const size_t need = c->desc.residency == LS_WEIGHTS_HBM ? staged_end : staged_end - lay.bias;
     if (!c->staging || c->staging_bytes < need) {
         if (c->staging) (void)hipHostFree(c->staging);
         c->staging = nullptr;
@@ -431,16 +442,36 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
     uint8_t* sm = c->staging + off_small;
     std::memset(sm, 0, lay.p1 - lay.bias);
     if (w->b_gate) std::memcpy(sm, w->b_gate, (size_t)s.F * es);
-    // predictor rows in the grouped order (padding rows stay zero)
-    std::memset(sm + (lay.p1 - lay.bias), 0, lay.total - lay.p1);
-    for (int i = 0; i < s.r; ++i)
-        std::memcpy(sm + (lay.p1 - lay.bias) + ((size_t)(i % s.G) * s.p1_rpw + i / s.G) * s.d * es,
-                    static_cast<const uint8_t*>(w->p1) + (size_t)i * s.d * es, (size_t)s.d * es);
-    for (int i = 0; i < s.n_blk; ++i)
-        std::memcpy(sm + (lay.p2 - lay.bias) + ((size_t)(i % s.G) * s.p2_rpw + i / s.G) * s.r * es,
-                    static_cast<const uint8_t*>(w->p2) + (size_t)i * s.r * es, (size_t)s.r * es);
+    if (!s.fold) {
+        // predictor rows in the grouped order (padding rows stay zero)
+        std::memset(sm + (lay.p1 - lay.bias), 0, lay.total - lay.p1);
+        for (int i = 0; i < s.r; ++i)
+            std::memcpy(sm + (lay.p1 - lay.bias) + ((size_t)(i % s.G) * s.p1_rpw + i / s.G) * s.d * es,
+                        static_cast<const uint8_t*>(w->p1) + (size_t)i * s.d * es, (size_t)s.d * es);
+        for (int i = 0; i < s.n_blk; ++i)
+            std::memcpy(sm + (lay.p2 - lay.bias) + ((size_t)(i % s.G) * s.p2_rpw + i / s.G) * s.r * es,
+                        static_cast<const uint8_t*>(w->p2) + (size_t)i * s.r * es, (size_t)s.r * es);
+    }
     LS_HIP(c, hipMemcpyAsync(c->arena[layer], c->staging, need, hipMemcpyHostToDevice, c->stream));
     LS_HIP(c, hipStreamSynchronize(c->stream));
+    if (s.fold) {
+        // P2 P1 on the device (fp64 accumulation), written into the predictor region
+        const size_t p1_bytes = (size_t)s.r * s.d * es, p2_bytes = (size_t)s.n_blk * s.r * es;
+        uint8_t* tmp = nullptr;
+        if (hipMalloc(reinterpret_cast<void**>(&tmp), p1_bytes + p2_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(c, LS_E_NOMEM, "device allocation for the predictor fold failed");
+        }
+        hipError_t e = hipMemcpy(tmp, w->p1, p1_bytes, hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(tmp + p1_bytes, w->p2, p2_bytes, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = ls::launch_fold_predictor(s.dtype, tmp, tmp + p1_bytes, s.r, s.d, s.n_blk,
+                                          const_cast<float*>(c->dev[layer].pf), c->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+        const hipError_t ef = hipFree(tmp);
+        LS_HIP(c, e);
+        LS_HIP(c, ef);
+    }
     c->dev[layer].bias =
         w->b_gate ? c->arena[layer] + (c->desc.residency == LS_WEIGHTS_HBM ? lay.bias : 0) : nullptr;
     c->dev[layer].threshold = w->threshold;
@@ -449,13 +480,24 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
         ls::LayerPtrs lp{};
         lp.blocks = c->dev[layer].blocks;
         lp.bias = c->dev[layer].bias;
-        lp.p1 = static_cast<const uint8_t*>(c->dev[layer].p1);
-        lp.p2 = static_cast<const uint8_t*>(c->dev[layer].p2);
+        lp.pf = c->dev[layer].pf;
         lp.threshold = w->threshold;
         c->layer_tab_host[layer] = lp;
         LS_HIP(c, hipMemcpy(c->layer_tab + layer, &lp, sizeof lp, hipMemcpyHostToDevice));
     }
     c->is_set[layer] = 1;
+    return LS_OK;
+}
+
+// scores = P2 (P1 h) from c->h: one GEMV over the folded rows, or the two factors in turn.
+static ls_status predictor_gemv(ls_ffn* c, const ls::LayerDev& L, int B, float* scores) {
+    const Shape& s = c->shape;
+    if (s.fold) {
+        LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(LS_F32, L.pf, s.n_blk, s.d, 1, s.n_blk, c->h, B, scores, c->stream); }));
+        return LS_OK;
+    }
+    LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, scores, c->stream); }));
     return LS_OK;
 }
 
@@ -468,9 +510,7 @@ ls_status ls_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, float*
     if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
     const Shape& s = c->shape;
     LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, x, B, c->h, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, c->dev[layer].p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, c->dev[layer].p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, scores, c->stream); }));
-    return LS_OK;
+    return predictor_gemv(c, c->dev[layer], B, scores);
 }
 
 ls_status ls_select_blocks(ls_ffn* c, const float* scores, int32_t B, ls_sel_mode mode, int32_t k,
@@ -626,7 +666,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
     if (c->desc.residency != LS_WEIGHTS_HBM)
         return fail(c, LS_E_UNSUPPORTED, "ls_decode_step needs HBM-resident weights; use the per-layer calls");
     if (c->decode_path != 1) {
-        int kp = c->spec_blocks > 0 ? c->spec_blocks : k + (k + 3) / 4;
+        int kp = c->spec_blocks > 0 ? c->spec_blocks : 2 * k;
         kp = std::min(kp, ls::fused_max_spec(s, c->n_wg));
         kp = std::max(kp, k);
         const ls::FusedSupport sup = ls::fused_supported(s, B, k, kp, c->n_wg, c->desc.n_layers);
@@ -640,7 +680,6 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             a.layers = c->layer_tab;
             a.L = c->desc.n_layers;
             a.d = s.d;
-            a.r = s.r;
             a.nb = s.n_blk;
             a.blk = s.blk;
             a.F = s.F;
@@ -651,8 +690,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             a.x = x;
             const size_t L = (size_t)c->desc.n_layers;
             a.xmb = c->mailbox;
-            a.zmb = a.xmb + L * s.d;
-            a.smb = a.zmb + L * 2 * s.r;
+            a.smb = a.xmb + L * s.d;
             a.amb = a.smb + L * 2 * s.n_blk;
             a.tag = ++c->epoch;
             a.err = c->dev_err;
@@ -673,8 +711,8 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
     for (int l = 0; l < c->desc.n_layers; ++l) {
         const ls::LayerDev& L = c->dev[l];
         LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, cur, B, c->h, c->stream); }));
-        LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
-        LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, c->scores, c->stream); }));
+        st = predictor_gemv(c, L, B, c->scores);
+        if (st != LS_OK) return st;
         LS_HIP(c, timed(c, LS_K_SELECT, [&] {
             return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count, c->stream);
         }));
@@ -723,7 +761,7 @@ ls_status ls_debug_decode_trace(ls_ffn* c, int32_t layer, float* x_in, float* sc
     if (!c->last_fused) return fail(c, LS_E_STATE, "the last ls_decode_step did not run the fused kernel");
     const size_t L = (size_t)c->desc.n_layers;
     const uint64_t* xmb = c->mailbox;
-    const uint64_t* smb = xmb + L * s.d + L * 2 * s.r;
+    const uint64_t* smb = xmb + L * s.d;
     if (x_in) {
         if (layer == 0) return fail(c, LS_E_INVAL, "layer 0 input is the caller's own x");
         LS_HIP(c, ls::launch_untag(xmb + (size_t)layer * s.d, s.d, x_in, c->stream));

@@ -9,21 +9,19 @@ namespace ls {
 struct LayerPtrs {
     const uint8_t* blocks;  // n_blk blocks of block_bytes
     const void* bias;       // [F] or null
-    const uint8_t* p1;      // [r, d]
-    const uint8_t* p2;      // [n_blk, r]
+    const float* pf;        // [n_blk, d] folded predictor P2 P1
     float threshold;
     float pad_;
 };
 
 struct FusedArgs {
     const LayerPtrs* layers;  // device [L]
-    int L, d, r, nb, blk, F, k, kp, prenorm;
+    int L, d, nb, blk, F, k, kp, prenorm;
     size_t block_bytes;
     float* x;                 // [d]: input at entry, output at exit
     uint64_t* xmb;            // [L][d]      tagged x of every layer input (row 0: the input)
-    uint64_t* zmb;            // [L][2r]     tagged z (exact | speculative next layer)
     uint64_t* smb;            // [L][2 n_blk] tagged scores (exact | speculative)
-    uint64_t* amb;            // [L][F]      tagged activations in priority-list order
+    uint64_t* amb;            // [L][2F]     tagged activations: list positions, then misses
     uint32_t tag;             // launch epoch (>= 1)
     int* err;                 // set to 1 when a wait exceeded its spin limit
     uint64_t* trace;          // null, or [L][kTracePoints] wall-clock stamps of one workgroup

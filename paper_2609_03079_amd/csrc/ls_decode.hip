@@ -23,10 +23,12 @@
 // mailbox rows, so no value is overwritten within a launch.  Every wait is
 // bounded: on timeout an error flag is set and the kernel runs to completion.
 //
+// The predictor runs in its folded form Pf = P2 P1 (fp32 [n_blk, d], Sec. 3.3.3 with the
+// projection and the head applied as one matrix), so a layer needs three exchanges.
+//
 // Per layer l (all reductions in a fixed order):
 //   X   h_l = prenorm(x_l)                     (x_l from the previous layer)
-//   Z   z_l = P1_l h_l, z~_{l+1} = P1_{l+1} h_l (rows of this workgroup)
-//   S   s_l = P2_l z_l, s~_{l+1} = P2_{l+1} z~   (block scores of this workgroup)
+//   S   s_l = Pf_l h_l, s~_{l+1} = Pf_{l+1} h_l (block scores of this workgroup's rows)
 //   SEL E_l = topk(s_l, k); P_{l+1} = topk(s~_{l+1}, kp)  (every workgroup)
 //   GU  a_j for the neurons of E_l held in this workgroup's slots
 //   D   y over E_l for this workgroup's 16-column tile; x_{l+1} = x_l + y
@@ -42,18 +44,17 @@ constexpr int kThreads = 256;           // one wave per SIMD: each wave may use 
 constexpr int kWaves = kThreads / 64;
 constexpr int kWorkers = kWaves - 1;    // worker waves 1..3
 constexpr int kWL = kWorkers * 64;      // worker lanes
-constexpr int kSlots = 2;               // neuron slots per worker wave
-constexpr int kMaxP1 = 11;              // P1 wave-chunks (64 x 16 B) per worker wave (per layer)
+constexpr int kSlots = 3;               // neuron slots per worker wave
 constexpr int kDnPos = 8;               // speculative list positions per worker wave
 constexpr int kDnPer = 2;               // 16-byte down chunks per lane per position
 constexpr int kMaxDn = kDnPos * kDnPer;
+constexpr int kMaxDnTot = kDnPos * kWorkers;  // down positions held per workgroup
 constexpr int kMaxD = 4096;
-constexpr int kMaxR = 1024;
 constexpr int kMaxNb = 256;
 constexpr int kMaxKp = 64;
 constexpr int kMaxA = 4096;             // k * block
-constexpr int kMaxRowsPerWg = 8;        // predictor rows per workgroup
-constexpr int kMaxScoresPerWg = 4;
+constexpr int kMaxSRows = 1;            // folded predictor rows (block scores) per workgroup
+constexpr int kPfPer = (kMaxD / 4 + kWL - 1) / kWL;  // 16-byte chunks of one row per worker lane
 constexpr int kMaxLayers = 128;
 constexpr unsigned kSpinLimit = 1u << 18;  // ~0.3 s of polling per wait
 
@@ -104,6 +105,31 @@ __device__ __forceinline__ void wait_words(const uint64_t* src, int n, uint32_t 
     }
 }
 
+// Same, for words at arbitrary addresses: addr(u) is this lane's u-th word; only the first
+// `used` (wave-uniform) of the W loads are issued.
+template <int W, typename Addr>
+__device__ __forceinline__ void wait_gather(Addr addr, int used, uint32_t tag, int lane, int* err,
+                                            uint64_t (&v)[W]) {
+    const uint64_t* a[W];
+#pragma unroll
+    for (int u = 0; u < W; ++u) a[u] = addr(u);
+    for (unsigned spins = 0;; ++spins) {
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            if (u < used) v[u] = mb_load(a[u]);
+        bool done = true;
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            if (u < used) done &= (uint32_t)(v[u] >> 32) == tag;
+        if (__all(done)) break;
+        if (spins > kSpinLimit) {
+            if (lane == 0) atomicOr(err, 1);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
 __device__ __forceinline__ float word_value(uint64_t w) { return __uint_as_float((uint32_t)w); }
 
 // Keep a prefetched register in its storage type until this point: without it the compiler
@@ -133,93 +159,52 @@ __device__ __forceinline__ float dot_chunk(const u32x4& raw_in, const float* x) 
 }
 
 struct Smem {
-    u32x4 p1s[2][kMaxP1 * kWorkers * 64];  // this workgroup's P1 rows of two layers (by parity)
+    f32x4 pfs[2][kMaxSRows][kMaxD / 4];  // this workgroup's folded predictor rows, two layers
     LayerPtrs lt[kMaxLayers];  // the layer table (LDS reads keep weight loads off the wait path)
-    u32x4 p2s[2][kWL];         // this workgroup's P2 rows of two layers (by parity)
     float hs[kMaxD];
     float xt[kColTile];
-    float zres[2 * kMaxRowsPerWg];
-    float zall[2 * 1024];
-    float sp[2][kWL];
-    float sres[2 * kMaxScoresPerWg];
-    alignas(16) uint64_t key[2][kMaxNb + 2];  // composite keys, padded with 0 to even length
+    float sp[kWorkers][2 * kMaxSRows];  // per-wave partial scores (exact rows, then speculative)
+    uint32_t key[2][kMaxNb];   // order keys of the exact and the speculative scores
     int E[kMaxKp];
     int Plist[2][kMaxKp];
-    int slot_entry[kMaxKp];
-    int slot_miss[kMaxKp];
-    int missE[kMaxKp];
+    int hole_miss[kMaxKp];   // speculative position -> miss it recomputes, or -1
+    int missE[kMaxKp];       // miss m -> E entry
+    int act_at[kMaxKp];      // E entry -> first activation word in the layer's mailbox row
+    int dn_entry[kMaxDnTot]; // down position -> E entry it serves, or -1
+    int dn_load[kMaxDnTot];  // 1: the down position's registers must be loaded for its entry
+    int needE[kMaxKp];
     int posE[kMaxNb];   // block -> position in E, or -1
     int posP[kMaxNb];   // block -> position in the current speculative list, or -1
-    float a_loc[kWorkers * kSlots];
-    int a_pos[kWorkers * kSlots];
-    float aall[kMaxA];
+    float aall[kMaxA];  // activations of E in entry order
     float dpart[kWL];
 };
 
 // Static shape of one launch, shared by both roles.
 struct Geo {
-    int w, G, L, r, nb, blk, k, kp, F;
-    int RPW, P1C, CPR2, SPW, P2C, NPC, RPWmax, SPWmax;
+    int w, G, L, nb, blk, k, kp, F;
+    int SPW;  // folded predictor rows of this workgroup: rows w, w + G, ... below n_blk
+    int CH;   // 16-byte chunks of one folded row (d / 4)
+    int NPC;  // 16-byte chunks of one block's down piece for one column tile
+    int DN;   // down positions in use: min(kp, kMaxDnTot)
+    int AW;   // activation words per layer: list positions, then misses
+    int miss_base;
     bool has_tile;
     uint32_t tag;
 };
 
-// Row sums shared by all eight waves: rows [0, rows) of the exact set and, unless
-// skip_spec, of the speculative set (stored set_stride apart); lane-strided partial
-// sums then a butterfly, a fixed order.
-__device__ __forceinline__ void reduce_rows(const float* part, int set_stride, int rows, int per_row,
-                                            bool skip_spec, float* res, int wave, int lane) {
-    for (int m2 = wave; m2 < 2 * rows; m2 += kWaves) {
-        const int set = m2 / rows, m = m2 % rows;
-        if (set == 1 && skip_spec) continue;
-        const float* src = part + (size_t)set * set_stride + (size_t)m * per_row;
-        float acc = 0.f;
-        for (int c = lane; c < per_row; c += 64) acc += src[c];
-        acc = wave_sum_dpp(acc);
-        if (lane == 0) res[m2] = acc;
-    }
-}
-
-// Predictor projection rows of this workgroup, shared by all waves: row m (of RPW) of the
-// exact set (layer l) and, unless last, of the speculative set (layer l+1), from the P1 rows
-// staged in LDS and h; wave v takes rows v, v+4, ...; results in zres[set * RPW + m].
-template <ls_dtype T, int CPR>
-__device__ __forceinline__ void z_rows(Smem& sm, const Geo g, int l, bool last, int wave, int lane) {
-    constexpr int V = Wt<T>::V;
-    for (int m2 = wave; m2 < 2 * g.RPW; m2 += kWaves) {
-        const int set = m2 / g.RPW, m = m2 % g.RPW;
-        if (set == 1 && last) continue;
-        const u32x4* row = sm.p1s[(l + set) & 1] + m * CPR;
-        float acc = 0.f;
-#pragma unroll
-        for (int i = 0; i < CPR / 64; ++i) {
-            const int c = lane + 64 * i;
-            acc += dot_chunk<T>(row[c], sm.hs + c * V);
-        }
-        acc = wave_sum_dpp(acc);
-        if (lane == 0) sm.zres[m2] = acc;
-    }
-}
-
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
-    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
-    return ((uint64_t)hi << 32) | lo;
-}
-
 // Top-m set of one list, run by one wave without LDS traffic.  The priority order is the
-// composite key (order_key << 32 | ~index): larger first.  A bitwise search from the top
+// order key (larger first), ties to the smaller index.  A bitwise search from the top
 // bit finds T, the m-th largest order key (the largest T with at least m keys >= T); the
 // set is every key > T plus the elements equal to T with the smallest indices.  Members
 // are written to out[] in index order (the set is what matters to the fused step; its
 // summation order is fixed by the slot map).  Needs 1 <= m <= n.
-__device__ __forceinline__ void top_set(const uint64_t* keys, int n, int m, int* out, int lane) {
+__device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int* out, int lane) {
     constexpr int Q = kMaxNb / 64;
     uint32_t ok[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int i = q * 64 + lane;
-        ok[q] = i < n ? (uint32_t)(keys[i] >> 32) : 0u;  // padding compares below every c >= 1
+        ok[q] = i < n ? keys[i] : 0u;  // padding compares below every c >= 1
     }
     uint32_t T = 0u;
     for (int bit = 31; bit >= 0; --bit) {
@@ -287,39 +272,19 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             }
         }
         LS_STAMP(P, g, l, 1, lane == 0);
-        lds_barrier();  // 1: h ready (and this layer's P1 rows staged)
-        z_rows<T, D / V>(sm, g, l, last, 0, lane);
-        lds_barrier();  // 2: z rows of this workgroup ready
-        for (int m2 = lane; m2 < 2 * g.RPW; m2 += 64) {
-            const int set = m2 / g.RPW, m = m2 % g.RPW;
-            if (set == 1 && last) continue;
-            mb_store(P.zmb + (size_t)l * 2 * g.r + set * g.r + (g.w + g.G * m), g.tag, sm.zres[m2]);
-        }
-        LS_STAMP(P, g, l, 2, lane == 0);
-        // S: z of every workgroup (exact, then speculative)
-        {
-            const int n = last ? g.r : 2 * g.r;
-            uint64_t v[2 * kMaxR / 64];
-            wait_words<2 * kMaxR / 64>(P.zmb + (size_t)l * 2 * g.r, n, g.tag, lane, P.err, v);
+        lds_barrier();  // 1: h ready (and the folded rows of layers l, l+1 staged)
+        lds_barrier();  // 2: partial scores ready
+        if (lane < 2 * g.SPW) {
+            const int set = lane / g.SPW, m = lane % g.SPW;
+            if (set == 0 || !last) {
+                float sc = 0.f;
 #pragma unroll
-            for (int u = 0; u < 2 * kMaxR / 64; ++u) {
-                const int i = u * 64 + lane;
-                if (i < n) sm.zall[i] = word_value(v[u]);
+                for (int v = 0; v < kWorkers; ++v) sc += sm.sp[v][set * kMaxSRows + m];
+                mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, sc);
             }
         }
-        LS_STAMP(P, g, l, 3, lane == 0);
-        lds_barrier();  // 4: z of every workgroup ready
-        lds_barrier();  // 5: S partials ready
-        reduce_rows(&sm.sp[0][0], kWL, g.SPW, g.CPR2, last, sm.sres, 0, lane);
-        lds_barrier();  // 6: scores reduced
-        for (int m2 = lane; m2 < 2 * g.SPW; m2 += 64) {
-            const int set = m2 / g.SPW, m = m2 % g.SPW;
-            if (set == 1 && last) continue;
-            mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, sm.sres[m2]);
-        }
-        LS_STAMP(P, g, l, 4, lane == 0);
-        // SEL: scores of every block (exact, then speculative) as composite keys
-        // order_key(s) << 32 | ~index: distinct, larger = earlier in the priority order
+        LS_STAMP(P, g, l, 2, lane == 0);
+        // SEL: order keys of every block's score (exact, then speculative)
         {
             const int n = last ? g.nb : 2 * g.nb;
             uint64_t v[2 * kMaxNb / 64];
@@ -328,82 +293,92 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             for (int u = 0; u < 2 * kMaxNb / 64; ++u) {
                 const int i = u * 64 + lane;
                 if (i < n) {
-                    const int list = i >= g.nb, b = i - list * g.nb;
-                    sm.key[list][b] = ((uint64_t)order_key(word_value(v[u])) << 32) |
-                                      (uint64_t)(0xffffffffu - (uint32_t)b);
+                    const int list = i >= g.nb;
+                    sm.key[list][i - list * g.nb] = order_key(word_value(v[u]));
                 }
             }
-            if (lane < 2) {  // pad to even length: below every real key
-                sm.key[0][g.nb + lane] = 0ull;
-                sm.key[1][g.nb + lane] = 0ull;
-            }
         }
-        LS_STAMP(P, g, l, 5, lane == 0);
-        lds_barrier();  // 7: keys ready
-        LS_STAMP(P, g, l, 12, lane == 0);
+        LS_STAMP(P, g, l, 3, lane == 0);
+        lds_barrier();  // 3: keys ready
+        LS_STAMP(P, g, l, 4, lane == 0);
         rank_all(sm, g, last, Pn, 0, lane);
-        LS_STAMP(P, g, l, 13, lane == 0);
-        lds_barrier();  // 8: E and the speculative list ready
-        LS_STAMP(P, g, l, 14, lane == 0);
-        if (l == 0) {
-            sm.slot_entry[lane] = lane < g.k ? lane : -1;
-            sm.slot_miss[lane] = 1;
-            Pc[lane] = lane < g.k ? sm.E[lane] : -1;
-        } else {
-            // block -> position tables of E and of the current speculative list
+        LS_STAMP(P, g, l, 5, lane == 0);
+        lds_barrier();  // 4: E and the speculative list ready
+        // Slot maps.  Activations: an E block found in the speculative list Pc was computed
+        // at its list position (early, before the selection); the others ("misses") are
+        // recomputed by the slots of holes (list positions whose block is not in E) and
+        // published after the list, at word miss_base + m * blk.  Down pieces: positions
+        // [0, DN) hold the prefetched pieces of Pc[0, DN); E blocks not among them are
+        // loaded into the holes of that range.
+        {
+            const bool spec = l > 0;
             for (int b = lane; b < g.nb; b += 64) {
                 sm.posE[b] = -1;
                 sm.posP[b] = -1;
             }
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
             if (lane < g.k) sm.posE[sm.E[lane]] = lane;
-            if (lane < g.kp) sm.posP[Pc[lane]] = lane;
+            if (spec && lane < g.kp) sm.posP[Pc[lane]] = lane;
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
-            const int ie = lane < g.kp ? sm.posE[Pc[lane]] : -1;
-            const bool miss = lane < g.k && sm.posP[sm.E[lane]] < 0;
-            const bool hole = lane < g.kp && ie < 0;
-            const uint64_t mm = __ballot(miss), hm = __ballot(hole);
             const uint64_t below = (1ull << lane) - 1ull;
-            if (miss) sm.missE[__popcll(mm & below)] = lane;
+            const int pp = lane < g.k ? sm.posP[sm.E[lane]] : -1;  // -1 when !spec
+            const bool miss = lane < g.k && pp < 0;
+            const uint64_t mm = __ballot(miss);
+            const int M = __popcll(mm), mr = __popcll(mm & below);
+            if (miss) sm.missE[mr] = lane;
+            if (lane < g.k) sm.act_at[lane] = miss ? g.miss_base + mr * g.blk : pp * g.blk;
+            const int pe = spec && lane < g.kp ? sm.posE[Pc[lane]] : -1;
+            const bool hole = lane < g.kp && pe < 0;
+            const uint64_t hm = __ballot(hole);
+            const int hr = __popcll(hm & below);
+            sm.hole_miss[lane] = hole && hr < M ? hr : -1;
+            // down positions
+            const bool need = lane < g.k && (miss || pp >= g.DN);
+            const uint64_t nm = __ballot(need);
+            if (need) sm.needE[__popcll(nm & below)] = lane;
+            const bool dhole = lane < g.DN && pe < 0;
+            const uint64_t dm = __ballot(dhole);
+            const int dr = __popcll(dm & below);
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
-            int se = -1, ms = 0;
-            if (lane < g.kp) {
-                if (!hole) {
-                    se = ie;
-                } else {
-                    const int hr = __popcll(hm & below);
-                    if (hr < __popcll(mm)) {
-                        se = sm.missE[hr];
-                        ms = 1;
+            if (lane < kMaxDnTot) {
+                int de = -1, dl = 0;
+                if (lane < g.DN) {
+                    if (!dhole) de = pe;
+                    else if (dr < __popcll(nm)) {
+                        de = sm.needE[dr];
+                        dl = 1;
                     }
                 }
+                sm.dn_entry[lane] = de;
+                sm.dn_load[lane] = dl;
             }
-            sm.slot_entry[lane] = se;
-            sm.slot_miss[lane] = ms;
         }
         LS_STAMP(P, g, l, 6, lane == 0);
-        lds_barrier();  // 9: slot map ready
-        lds_barrier();  // 10: activations of this workgroup ready
-        LS_STAMP(P, g, l, 7, lane == 0);
-        if (lane < kWorkers * kSlots && sm.a_pos[lane] >= 0)
-            mb_store(P.amb + (size_t)l * g.F + sm.a_pos[lane], g.tag, sm.a_loc[lane]);
-        // D: activations of every workgroup, in priority-list order
+        lds_barrier();  // 5: slot maps ready
+        // activations of E, gathered from the words of every workgroup
         {
             const int n = g.k * g.blk;
-            for (int base = 0; base < n; base += 32 * 64) {
-                uint64_t v[32];
-                wait_words<32>(P.amb + (size_t)l * g.F + base, min(n - base, 32 * 64), g.tag, lane,
-                               P.err, v);
+            const uint64_t* row = P.amb + (size_t)l * g.AW;
+            for (int base = 0; base < n; base += 16 * 64) {
+                uint64_t v[16];
+                const int* at = sm.act_at;
+                const int blk = g.blk;
+                wait_gather<16>(
+                    [&](int u) {
+                        const int f = min(base + u * 64 + lane, n - 1);
+                        return row + at[f / blk] + f % blk;
+                    },
+                    (n - base + 63) / 64, g.tag, lane, P.err, v);
 #pragma unroll
-                for (int u = 0; u < 32; ++u) {
+                for (int u = 0; u < 16; ++u) {
                     const int i = base + u * 64 + lane;
                     if (i < n) sm.aall[i] = word_value(v[u]);
                 }
             }
         }
         LS_STAMP(P, g, l, 8, lane == 0);
-        lds_barrier();  // 11: activations of every workgroup ready
-        lds_barrier();  // 12: down partials ready
+        lds_barrier();  // 6: activations of every workgroup ready
+        lds_barrier();  // 7: down partials ready
         LS_STAMP(P, g, l, 9, lane == 0);
         if (g.has_tile && lane < kColTile) {
             float y = 0.f;
@@ -416,23 +391,23 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
 }
 
 // ---------------------------------------------------------------------------------------
-// Worker waves: registers hold the predictor factors of the next two layers and the
+// Worker waves: registers hold the folded predictor rows of a later layer and the
 // speculatively prefetched blocks of the next layer.
 template <ls_dtype T, ls_act A, int NC>
 __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const Geo g, int wave, int lane) {
     constexpr int V = Wt<T>::V;
     constexpr int KB = Wt<T>::kBytes;
     constexpr int D = NC * V * 64;
-    constexpr int CPR = D / V;
     const int wl = (wave - 1) * 64 + lane;
     const size_t row_bytes = (size_t)D * KB;
     const size_t down_off = 2 * (size_t)g.blk * row_bytes + (size_t)g.w * g.blk * kColTile * KB;
     const size_t bb = P.block_bytes;
     const u32x4 zero4 = {0u, 0u, 0u, 0u};
-    // pr: P1 rows in flight (one layer), moved to LDS one layer after they were requested
-    u32x4 pr[kMaxP1], p2r = zero4, gg[kSlots][NC], uu[kSlots][NC], dn[kMaxDn];
+    // pfr: folded predictor rows in flight (one layer), moved to LDS one layer after they
+    // were requested; chunk c = wl + kWL*j of row m sits in pfr[m * kPfPer + j]
+    u32x4 pfr[kMaxSRows * kPfPer], gg[kSlots][NC], uu[kSlots][NC], dn[kMaxDn];
 #pragma unroll
-    for (int j = 0; j < kMaxP1; ++j) pr[j] = zero4;
+    for (int j = 0; j < kMaxSRows * kPfPer; ++j) pfr[j] = zero4;
 #pragma unroll
     for (int sl = 0; sl < kSlots; ++sl)
 #pragma unroll
@@ -440,32 +415,34 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
 #pragma unroll
     for (int j = 0; j < kMaxDn; ++j) dn[j] = zero4;
 
-    // P1 and P2 rows are stored grouped by owning workgroup (row w + G*m at storage row
-    // w*RPW + m), so this workgroup's rows are one contiguous range.
-    const size_t p1_off = (size_t)g.w * g.RPWmax * row_bytes;
-    const size_t p2_off = (size_t)g.w * g.SPWmax * g.r * KB;
-    // P1: wave-chunk wc = (wave-1) + 7j covers 64 consecutive 16-byte chunks of row wc / (CPR/64)
-    auto load_p1 = [&](int layer) {
-        const uint8_t* base = sm.lt[layer].p1 + p1_off;
+    auto load_pf = [&](int layer) {
 #pragma unroll
-        for (int j = 0; j < kMaxP1; ++j) {
-            const int wc = (wave - 1) + kWorkers * j;
-            if (wc < g.P1C) pr[j] = gload_u(base, (uint32_t)(wc * 64 + lane) * 16u);
+        for (int m = 0; m < kMaxSRows; ++m) {
+            if (m < g.SPW) {
+                const float* row = sm.lt[layer].pf + (size_t)(g.w + g.G * m) * D;
+#pragma unroll
+                for (int j = 0; j < kPfPer; ++j) {
+                    const int c = wl + kWL * j;
+                    if (c < g.CH) pfr[m * kPfPer + j] = gload_u(row, (uint32_t)c * 16u);
+                }
+            }
         }
     };
-    auto stash_p1 = [&](int layer) {  // pr -> LDS buffer of `layer`
-        u32x4* dst = sm.p1s[layer & 1];
+    auto stash_pf = [&](int layer) {  // pfr -> LDS buffer of `layer`
 #pragma unroll
-        for (int j = 0; j < kMaxP1; ++j) {
-            const int wc = (wave - 1) + kWorkers * j;
-            if (wc < g.P1C) dst[wc * 64 + lane] = pr[j];
+        for (int m = 0; m < kMaxSRows; ++m) {
+            if (m < g.SPW) {
+#pragma unroll
+                for (int j = 0; j < kPfPer; ++j) {
+                    const int c = wl + kWL * j;
+                    if (c < g.CH) {
+                        const u32x4 v = pin(pfr[m * kPfPer + j]);
+                        sm.pfs[layer & 1][m][c] = f32x4{__uint_as_float(v.x), __uint_as_float(v.y),
+                                                        __uint_as_float(v.z), __uint_as_float(v.w)};
+                    }
+                }
+            }
         }
-    };
-    auto load_p2 = [&](int layer) {
-        if (wl < g.P2C) p2r = gload_u(sm.lt[layer].p2 + p2_off, (uint32_t)wl * 16u);
-    };
-    auto stash_p2 = [&](int layer) {
-        if (wl < g.P2C) sm.p2s[layer & 1][wl] = p2r;
     };
     // neuron slot sl of this wave: workgroup slot index i = (wave-1) + kWorkers*sl,
     // global slot t = w + G*i (list position t / blk, neuron t % blk)
@@ -490,100 +467,198 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
             if (lane + 64 * i < g.NPC) dn[jp * kDnPer + i] = gload_u(base, (uint32_t)(lane + 64 * i) * 16u);
     };
 
-    load_p1(0);
-    load_p2(0);
+    // activations of the slots in `use` (wave-uniform bit mask) from their rows in gg/uu:
+    // slot sl holds neuron q[sl] of block b[sl]; every lane gets the results.  One
+    // slot at a time, with several partial sums per row for instruction-level parallelism.
+    auto gate_up = [&](int layer, unsigned use, const int (&b)[kSlots], const int (&q)[kSlots],
+                       float (&a)[kSlots]) {
+        constexpr int NA = 4;  // partial sums per row
+        // this lane's part of h: all LDS reads in flight together, reused by every slot
+        f32x4 hr[NC][V / 4];
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+#pragma unroll
+            for (int i = 0; i < V / 4; ++i)
+                hr[j][i] = reinterpret_cast<const f32x4*>(sm.hs + (lane + 64 * j) * V)[i];
+        float gs[kSlots], us[kSlots];
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+            gs[sl] = us[sl] = 0.f;
+            if (use & (1u << sl)) {
+                float ga[NA], ua[NA];
+#pragma unroll
+                for (int i = 0; i < NA; ++i) ga[i] = ua[i] = 0.f;
+#pragma unroll
+                for (int j = 0; j < NC; ++j) {
+                    float wg[V], wu[V];
+                    Wt<T>::widen(pin(gg[sl][j]), wg);
+                    Wt<T>::widen(pin(uu[sl][j]), wu);
+#pragma unroll
+                    for (int i = 0; i < V / 4; ++i) {
+                        const float hx[4] = {hr[j][i].x, hr[j][i].y, hr[j][i].z, hr[j][i].w};
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            const int v = 4 * i + c;
+                            ga[v % NA] = fmaf(wg[v], hx[c], ga[v % NA]);
+                            ua[v % NA] = fmaf(wu[v], hx[c], ua[v % NA]);
+                        }
+                    }
+                    if (j % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bounded live registers
+                }
+                gs[sl] = (ga[0] + ga[1]) + (ga[2] + ga[3]);
+                us[sl] = (ua[0] + ua[1]) + (ua[2] + ua[3]);
+            }
+        }
+        const void* bias = sm.lt[layer].bias;
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+            if (use & (1u << sl)) {
+                const float g0 = wave_sum_dpp(gs[sl]) +
+                                 (bias ? Wt<T>::scalar(bias, (size_t)b[sl] * g.blk + q[sl]) : 0.f);
+                const float u0 = wave_sum_dpp(us[sl]);
+                if (A == LS_ACT_REGLU) {
+                    a[sl] = fmaxf(g0, 0.f) * u0;
+                } else {
+                    const float sg = g0 / (1.f + expf(-g0));
+                    a[sl] = fabsf(sg) > sm.lt[layer].threshold ? sg * u0 : 0.f;
+                }
+            }
+        }
+    };
+
+    int slot_t[kSlots];  // global slot index of each of this wave's slots
+#pragma unroll
+    for (int sl = 0; sl < kSlots; ++sl) slot_t[sl] = g.w + g.G * ((wave - 1) + kWorkers * sl);
+
+    load_pf(0);
 
     for (int l = 0; l < g.L; ++l) {
         const bool last = l == g.L - 1;
+        const int* Pc = sm.Plist[l & 1];
         const int* Pn = sm.Plist[(l + 1) & 1];
-        // P1 and P2 rows of layer l+1 (requested one layer ago) go to LDS before Z needs them
+        // folded rows of layer l+1 (requested one layer ago) go to LDS before S needs them
         if (l == 0) {
-            stash_p1(0);
-            stash_p2(0);
+            stash_pf(0);
             if (g.L > 1) {
-                load_p1(1);
-                load_p2(1);
-                stash_p1(1);
-                stash_p2(1);
+                load_pf(1);
+                stash_pf(1);
             }
         } else if (!last) {
-            stash_p1(l + 1);
-            stash_p2(l + 1);
+            stash_pf(l + 1);
         }
         lds_barrier();  // 1: h ready
-        z_rows<T, CPR>(sm, g, l, last, wave, lane);
-        lds_barrier();  // 2
-        if (l + 2 < g.L) load_p1(l + 2);
-        lds_barrier();  // 4: z of every workgroup ready
-        if (wl < g.P2C) {
-            const int c = wl % g.CPR2;
-            sm.sp[0][wl] = dot_chunk<T>(sm.p2s[l & 1][wl], sm.zall + c * V);
-            if (!last) sm.sp[1][wl] = dot_chunk<T>(sm.p2s[(l + 1) & 1][wl], sm.zall + g.r + c * V);
-        }
-        lds_barrier();  // 5
-        reduce_rows(&sm.sp[0][0], kWL, g.SPW, g.CPR2, last, sm.sres, wave, lane);
-        lds_barrier();  // 6
-        if (l + 2 < g.L) load_p2(l + 2);
-        lds_barrier();  // 7: keys ready
-        rank_all(sm, g, last, const_cast<int*>(Pn), wave, lane);
-        LS_STAMP(P, g, l, 15, wave == 1 && lane == 0);
-        lds_barrier();  // 8
-        lds_barrier();  // 9: slot map ready
-        // GU
+        // S partials: exact rows (layer l) and speculative rows (layer l+1) against h
+        {
+            float acc[2 * kMaxSRows];
 #pragma unroll
-        for (int sl = 0; sl < kSlots; ++sl) {
-            const int i = (wave - 1) + kWorkers * sl, t = g.w + g.G * i;
-            float a_val = 0.f;
-            int a_at = -1;
-            if (t < g.kp * g.blk) {
-                const int p = t / g.blk, q = t % g.blk;
-                const int e = sm.slot_entry[p];
-                if (e >= 0) {
-                    const int b = sm.E[e];
-                    if (sm.slot_miss[p]) load_gu(sl, l, b, q);
-                    float gs = 0.f, us = 0.f;
+            for (int m2 = 0; m2 < 2 * kMaxSRows; ++m2) acc[m2] = 0.f;
+            const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.hs);
 #pragma unroll
-                    for (int j = 0; j < NC; ++j) {
-                        const float* hx = sm.hs + (lane + 64 * j) * V;
-                        gs += dot_chunk<T>(gg[sl][j], hx);
-                        us += dot_chunk<T>(uu[sl][j], hx);
-                        __builtin_amdgcn_sched_barrier(0);
+            for (int j = 0; j < kPfPer; ++j) {
+                const int c = wl + kWL * j;
+                if (c < g.CH) {
+                    const f32x4 hv = h4[c];
+#pragma unroll
+                    for (int set = 0; set < 2; ++set) {
+#pragma unroll
+                        for (int m = 0; m < kMaxSRows; ++m) {
+                            if (m < g.SPW && (set == 0 || !last)) {
+                                const f32x4 pv = sm.pfs[(l + set) & 1][m][c];
+                                float a = acc[set * kMaxSRows + m];
+                                a = fmaf(pv.x, hv.x, a);
+                                a = fmaf(pv.y, hv.y, a);
+                                a = fmaf(pv.z, hv.z, a);
+                                a = fmaf(pv.w, hv.w, a);
+                                acc[set * kMaxSRows + m] = a;
+                            }
+                        }
                     }
-                    const void* bias = sm.lt[l].bias;
-                    gs = wave_sum(gs) + (bias ? Wt<T>::scalar(bias, (size_t)b * g.blk + q) : 0.f);
-                    us = wave_sum(us);
-                    if (A == LS_ACT_REGLU) {
-                        a_val = fmaxf(gs, 0.f) * us;
-                    } else {
-                        const float sg = gs / (1.f + expf(-gs));
-                        a_val = fabsf(sg) > sm.lt[l].threshold ? sg * us : 0.f;
-                    }
-                    a_at = e * g.blk + q;
                 }
             }
-            if (lane == 0) {
-                sm.a_loc[i] = a_val;
-                sm.a_pos[i] = a_at;
+#pragma unroll
+            for (int m2 = 0; m2 < 2 * kMaxSRows; ++m2) {
+                const float t = wave_sum_dpp(acc[m2]);
+                if (lane == 0) sm.sp[wave - 1][m2] = t;
             }
         }
-        LS_STAMP(P, g, l, 10, wave == 1 && lane == 0);
-        lds_barrier();  // 10
-        if (!last) {
+        lds_barrier();  // 2: partial scores ready
+        // early GU: every speculative position held in this wave's slots (prefetched during
+        // the previous layer), published at its list position while the selection runs
+        if (l > 0) {
+            unsigned use = 0;
+            int bs[kSlots], qs[kSlots];
+            float as[kSlots];
 #pragma unroll
             for (int sl = 0; sl < kSlots; ++sl) {
-                const int t = g.w + g.G * ((wave - 1) + kWorkers * sl);
-                if (t < g.kp * g.blk) load_gu(sl, l + 1, Pn[t / g.blk], t % g.blk);
+                const int t = slot_t[sl];
+                bs[sl] = t < g.kp * g.blk ? Pc[t / g.blk] : 0;
+                qs[sl] = t % g.blk;
+                if (t < g.kp * g.blk) use |= 1u << sl;
             }
+            LS_STAMP(P, g, l, 14, wave == 1 && lane == 0);
+            gate_up(l, use, bs, qs, as);
+#pragma unroll
+            for (int sl = 0; sl < kSlots; ++sl)
+                if ((use & (1u << sl)) && lane == 0) mb_store(P.amb + (size_t)l * g.AW + slot_t[sl], g.tag, as[sl]);
         }
-        lds_barrier();  // 11: activations of every workgroup ready
+        LS_STAMP(P, g, l, 13, wave == 1 && lane == 0);
+        // folded rows of layer l+2 (after the early GU: its waits must not cover these loads)
+        if (l + 2 < g.L) load_pf(l + 2);
+        lds_barrier();  // 3: keys ready
+        rank_all(sm, g, last, const_cast<int*>(Pn), wave, lane);
+        LS_STAMP(P, g, l, 12, wave == 1 && lane == 0);
+        lds_barrier();  // 4
+        lds_barrier();  // 5: slot maps ready
+        // down pieces of E blocks that are not among the prefetched positions
         if (g.has_tile) {
-            float acc = 0.f;
 #pragma unroll
             for (int jp = 0; jp < kDnPos; ++jp) {
                 const int p = (wave - 1) + kWorkers * jp;
-                const int e = p < g.kp ? sm.slot_entry[p] : -1;
+                if (p < g.DN && sm.dn_load[p]) load_down_pos(l, sm.E[sm.dn_entry[p]], jp);
+            }
+        }
+        LS_STAMP(P, g, l, 15, wave == 1 && lane == 0);
+        // misses: the slots of a hole recompute one E block that the list missed
+        {
+            unsigned use = 0;
+            int bs[kSlots], qs[kSlots], ms[kSlots];
+            float as[kSlots];
+#pragma unroll
+            for (int sl = 0; sl < kSlots; ++sl) {
+                const int t = slot_t[sl];
+                ms[sl] = t < g.kp * g.blk ? sm.hole_miss[t / g.blk] : -1;
+                bs[sl] = ms[sl] >= 0 ? sm.E[sm.missE[ms[sl]]] : 0;
+                qs[sl] = t % g.blk;
+                if (ms[sl] >= 0) {
+                    use |= 1u << sl;
+                    load_gu(sl, l, bs[sl], qs[sl]);
+                }
+            }
+            if (use) {
+                gate_up(l, use, bs, qs, as);
+#pragma unroll
+                for (int sl = 0; sl < kSlots; ++sl)
+                    if ((use & (1u << sl)) && lane == 0)
+                        mb_store(P.amb + (size_t)l * g.AW + g.miss_base + ms[sl] * g.blk + qs[sl], g.tag, as[sl]);
+            }
+        }
+        // gate/up rows of the next layer's speculative list (known since the selection)
+        if (!last) {
+#pragma unroll
+            for (int sl = 0; sl < kSlots; ++sl) {
+                const int t = slot_t[sl];
+                if (t < g.kp * g.blk) load_gu(sl, l + 1, Pn[t / g.blk], t % g.blk);
+            }
+        }
+        LS_STAMP(P, g, l, 10, wave == 1 && lane == 0);
+        lds_barrier();  // 6: activations of every workgroup ready
+        if (g.has_tile) {
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jp = 0; jp < kDnPos; ++jp) {
+                const int p = (wave - 1) + kWorkers * jp;
+                const int e = p < g.DN ? sm.dn_entry[p] : -1;
                 if (e >= 0) {
-                    if (sm.slot_miss[p]) load_down_pos(l, sm.E[e], jp);
 #pragma unroll
                     for (int i = 0; i < kDnPer; ++i) {
                         const int cc = lane + 64 * i;
@@ -592,21 +667,23 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
                             Wt<T>::widen(pin(dn[jp * kDnPer + i]), wv);
                             const float* ap = sm.aall + e * g.blk + (cc / kColTile) * V;
 #pragma unroll
-                            for (int v = 0; v < V; ++v) acc = fmaf(ap[v], wv[v], acc);
+                            for (int v = 0; v < V; ++v) acc[v & 3] = fmaf(ap[v], wv[v], acc[v & 3]);
                         }
                     }
                 }
-                __builtin_amdgcn_sched_barrier(0);
             }
-            sm.dpart[wl] = acc;
+            sm.dpart[wl] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
         }
         LS_STAMP(P, g, l, 11, wave == 1 && lane == 0);
-        lds_barrier();  // 12
-        if (!last && g.has_tile) {
+        lds_barrier();  // 7
+        // down pieces of the next layer's speculative list
+        if (!last) {
+            if (g.has_tile) {
 #pragma unroll
-            for (int jp = 0; jp < kDnPos; ++jp) {
-                const int p = (wave - 1) + kWorkers * jp;
-                if (p < g.kp) load_down_pos(l + 1, Pn[p], jp);
+                for (int jp = 0; jp < kDnPos; ++jp) {
+                    const int p = (wave - 1) + kWorkers * jp;
+                    if (p < g.DN) load_down_pos(l + 1, Pn[p], jp);
+                }
             }
         }
     }
@@ -623,19 +700,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
     g.w = blockIdx.x;
     g.G = gridDim.x;
     g.L = P.L;
-    g.r = P.r;
     g.nb = P.nb;
     g.blk = P.blk;
     g.k = P.k;
     g.kp = P.kp;
     g.F = P.F;
-    g.RPW = g.w < g.r ? (g.r - 1 - g.w) / g.G + 1 : 0;
-    g.RPWmax = (g.r + g.G - 1) / g.G;
-    g.SPWmax = (g.nb + g.G - 1) / g.G;
-    g.P1C = g.RPW * (D / V) / 64;  // 64-lane wave-chunks of this workgroup's rows
-    g.CPR2 = g.r / V;
     g.SPW = g.w < g.nb ? (g.nb - 1 - g.w) / g.G + 1 : 0;
-    g.P2C = g.SPW * g.CPR2;
+    g.CH = D / 4;
+    g.DN = min(g.kp, kMaxDnTot);
+    g.miss_base = g.kp * g.blk;
+    g.AW = (g.kp + g.k) * g.blk;
     g.NPC = g.blk * KB;
     g.has_tile = g.w < D / kColTile;
     g.tag = P.tag;
@@ -691,30 +765,25 @@ FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int
     if (L > kMaxLayers) return {false, "more than 128 layers"};
     if (s.d % (V * 64) || (s.d / (V * 64) != 2 && s.d / (V * 64) != 8)) return {false, "d_model"};
     if (s.d > kMaxD || s.d / kColTile > n_wg) return {false, "d_model too large for one tile per workgroup"};
-    if (s.r > kMaxR || s.r % V) return {false, "rank"};
-    const int rpw = (s.r + n_wg - 1) / n_wg;
-    if (rpw > kMaxRowsPerWg || rpw * (s.d / V) / 64 > kMaxP1 * kWorkers) return {false, "rank rows per workgroup"};
-    const int spw = (s.n_blk + n_wg - 1) / n_wg;
-    if (spw > kMaxScoresPerWg || spw * (s.r / V) > kWL) return {false, "scores per workgroup"};
-    if ((s.d / V) % 64) return {false, "d_model"};
+    if (!s.fold) return {false, "predictor kept factored (its product would be larger)"};
+    if ((s.n_blk + n_wg - 1) / n_wg > kMaxSRows) return {false, "predictor rows per workgroup"};
     if (s.n_blk > kMaxNb) return {false, "n_blk"};
     if (k < 1 || kp < k || kp > kMaxKp || kp > s.n_blk) return {false, "k / speculative width"};
-    (void)0;
     if ((long)kp * s.blk > (long)kWorkers * kSlots * n_wg) return {false, "neuron slots"};
-    if (s.blk * KB > 64 * kDnPer || kp > kDnPos * kWorkers) return {false, "down chunks"};
+    if (s.blk * KB > 64 * kDnPer || k > kMaxDnTot) return {false, "down chunks"};
     if ((long)k * s.blk > kMaxA) return {false, "k * block"};
     return {true, ""};
 }
 
 int fused_max_spec(const Shape& s, int n_wg) {
     const long by_slots = (long)kWorkers * kSlots * n_wg / s.blk;
-    long m = std::min<long>(by_slots, (long)kDnPos * kWorkers);
-    m = std::min<long>(m, kMaxKp);
+    const long m = std::min<long>(by_slots, kMaxKp);
     return (int)std::min<long>(m, s.n_blk);
 }
 
 size_t fused_mailbox_words(const Shape& s, int L) {
-    return (size_t)L * ((size_t)s.d + 2 * (size_t)s.r + 2 * (size_t)s.n_blk + (size_t)s.F);
+    // per layer: x, scores (exact | speculative), activations (list positions | misses)
+    return (size_t)L * ((size_t)s.d + 2 * (size_t)s.n_blk + 2 * (size_t)s.F);
 }
 
 hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st) {

@@ -27,8 +27,9 @@ inline int vec_elems(ls_dtype t) { return 16 / elem_size(t); }
 struct LayerDev {
     const uint8_t* blocks = nullptr;  // n_blk blocks of block_bytes (resident mode)
     const void* bias = nullptr;       // [F] or null
-    const void* p1 = nullptr;         // [r, d]
-    const void* p2 = nullptr;         // [n_blk, r]
+    const void* p1 = nullptr;         // [r, d] in the grouped row order (factored predictor)
+    const void* p2 = nullptr;         // [n_blk, r] in the grouped row order (factored predictor)
+    const float* pf = nullptr;        // [n_blk, d] fp32 product P2 P1 (folded predictor)
     float threshold = 0.f;
 };
 
@@ -41,13 +42,25 @@ struct Shape {
     // Predictor rows are stored grouped by workgroup: logical row i of P1 (P2) sits at
     // storage row (i % G) * p1_rpw + i / G  ((i % G) * p2_rpw + i / G).
     int G, p1_rpw, p2_rpw;
+    // 1: the predictor is kept as the fp32 product P2 P1 (one n_blk x d GEMV), chosen
+    // when that matrix is no larger than the two factors in the weight type.
+    int fold;
 };
+
+// Fold decision: the product costs 4 n_blk d bytes, the factors (r d + n_blk r) elem bytes.
+inline int predictor_folds(int d, int r, int n_blk, ls_dtype t) {
+    return 4.0 * n_blk * d <= (double)elem_size(t) * ((double)r * d + (double)n_blk * r) ? 1 : 0;
+}
 
 // ---- kernel launchers (ls_kernels.hip) -------------------------------------------------
 hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st);
 // out[b, i] = W[s(i), :] . v[b, :] with s(i) = (i % G) * rpw + i / G (the grouped row order)
 hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G, int rpw,
                             const float* v, int B, float* out, hipStream_t st);
+// out[i, j] = sum_m P2[i, m] P1[m, j] (fp64 accumulation in m order, rounded once to
+// fp32); P1 [r, d], P2 [n_blk, r] row-major in the weight type.
+hipError_t launch_fold_predictor(ls_dtype t, const void* P1, const void* P2, int r, int d, int n_blk,
+                                 float* out, hipStream_t st);
 hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st);
 // slot_table: null in resident mode (block b lives at blocks + b*block_bytes); else

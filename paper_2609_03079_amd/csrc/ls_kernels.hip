@@ -366,6 +366,56 @@ hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G
     return hipErrorInvalidValue;
 }
 
+// Folding the predictor factors: a workgroup owns 8 rows of the product and 256 columns;
+// the 8 x 64 tile of P2 for the current m-range is shared through LDS.
+template <ls_dtype T>
+__global__ __launch_bounds__(256) void fold_predictor_kernel(const void* __restrict__ P1,
+                                                             const void* __restrict__ P2, int r,
+                                                             int d, int n_blk,
+                                                             float* __restrict__ out) {
+    constexpr int R = 8, M = 64;
+    __shared__ double p2s[R][M];
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    const int i0 = blockIdx.y * R;
+    double acc[R];
+#pragma unroll
+    for (int ii = 0; ii < R; ++ii) acc[ii] = 0.0;
+    for (int m0 = 0; m0 < r; m0 += M) {
+        for (int t = threadIdx.x; t < R * M; t += 256) {
+            const int ii = t / M, m = m0 + t % M;
+            p2s[ii][t % M] = (i0 + ii < n_blk && m < r) ? (double)Wt<T>::scalar(P2, (size_t)(i0 + ii) * r + m) : 0.0;
+        }
+        __syncthreads();
+        if (j < d) {
+            const int mend = min(M, r - m0);
+            for (int mm = 0; mm < mend; ++mm) {
+                const double pv = (double)Wt<T>::scalar(P1, (size_t)(m0 + mm) * d + j);
+#pragma unroll
+                for (int ii = 0; ii < R; ++ii) acc[ii] = fma(p2s[ii][mm], pv, acc[ii]);
+            }
+        }
+        __syncthreads();
+    }
+    if (j < d) {
+#pragma unroll
+        for (int ii = 0; ii < R; ++ii)
+            if (i0 + ii < n_blk) out[(size_t)(i0 + ii) * d + j] = (float)acc[ii];
+    }
+}
+
+hipError_t launch_fold_predictor(ls_dtype t, const void* P1, const void* P2, int r, int d, int n_blk,
+                                 float* out, hipStream_t st) {
+    if (r < 1 || d < 1 || n_blk < 1) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((d + 255) / 256), (unsigned)((n_blk + 7) / 8)), blk(256);
+    switch (t) {
+        case LS_F32: hipLaunchKernelGGL(fold_predictor_kernel<LS_F32>, grid, blk, 0, st, P1, P2, r, d, n_blk, out); break;
+        case LS_F16: hipLaunchKernelGGL(fold_predictor_kernel<LS_F16>, grid, blk, 0, st, P1, P2, r, d, n_blk, out); break;
+        case LS_BF16: hipLaunchKernelGGL(fold_predictor_kernel<LS_BF16>, grid, blk, 0, st, P1, P2, r, d, n_blk, out); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st) {
     int threads = ((n_blk + 63) / 64) * 64;
