@@ -47,6 +47,30 @@ def algorithmic_bytes_per_layer(cfg, U: int, Z: int = 0) -> int:
     return s * (ffn + bias) + predictor_bytes(cfg)
 
 
+def measured_traffic(kernel: str, cfg, n_layers_default: bool):
+    """HBM bytes per launch of `kernel` on this workload from the committed rocprofv3 counter
+    summary (profiles/<kernel>_<workload>.md), or None when there is none, the workload differs,
+    or the kernel's sources changed since the counters were taken (their sha256 differs)."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{cfg.name}.md")
+    if not n_layers_default or not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_t = re.search(r"traffic_bytes_per_launch: (\d+)", text)
+    m_h = re.search(r"source_sha256: ([0-9a-f]+)", text)
+    m_s = re.search(r"sources: (.+)", text)
+    if not (m_t and m_h and m_s):
+        return None
+    h = hashlib.sha256()
+    for rel in m_s.group(1).split():
+        full = os.path.join(ROOT, rel)
+        if not os.path.exists(full):
+            return None
+        h.update(open(full, "rb").read())
+    return int(m_t.group(1)) if h.hexdigest() == m_h.group(1) else None
+
+
 def cpu_baseline(cfg, weights, xs, n_tokens: int):
     """The CPU oracle (as it stands) on the first n_tokens decode steps of the same workload."""
     import oracle
@@ -71,6 +95,14 @@ def main() -> int:
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle sample size (0: skip)")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (testing)")
+    ap.add_argument("--path", choices=("auto", "kernels", "fused"), default="auto",
+                    help="decode path: fused kernel when supported (auto), per-kernel sequence, fused only")
+    ap.add_argument("--launch", choices=("cooperative", "plain"), default="plain",
+                    help="fused-kernel launch: a plain launch of the one-workgroup-per-CU grid on the idle "
+                         "device (default; the launch rocprofv3 can trace) or hipLaunchCooperativeKernel")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the benchmark: copy MIB MiB device-to-device 4 times (the known-size "
+                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -79,6 +111,16 @@ def main() -> int:
 
     import numpy as np
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        a = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(4):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_per_launch": n}))
+        return 0
 
     import lsgen
     import paper_2609_03079_amd as lsffn
@@ -99,6 +141,8 @@ def main() -> int:
     f = lsffn.Ffn(n_layers=cfg.n_layers, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block,
                   rank=cfg.rank, max_batch=B, dtype=cfg.dtype, act=cfg.act,
                   prenorm_rms=int(cfg.prenorm), stream=stream)
+    f.ls_configure(lsffn.LS_CFG_DECODE_PATH, {"auto": 0, "kernels": 1, "fused": 2}[args.path])
+    f.ls_configure(lsffn.LS_CFG_COOPERATIVE, int(args.launch == "cooperative"))
     keep_host = args.cpu_tokens > 0
     weights = []
     for l in range(cfg.n_layers):
@@ -164,7 +208,8 @@ def main() -> int:
         achieved = dom_bytes / (dom_t["avg_us"] * 1e-6) / 1e9
         roofline = {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": None, "bytes_per_launch": dom_bytes,
+                    "traffic": measured_traffic(dom_name, cfg, args.layers in (0, lsgen.CONFIGS[args.config].n_layers)),
+                    "bytes_per_launch": dom_bytes,
                     "avg_launch_us": round(dom_t["avg_us"], 3)}
 
     cpu = None
@@ -187,7 +232,8 @@ def main() -> int:
         "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers, d_model {cfg.d_model}, "
                                f"d_ff {cfg.d_ff}, block {cfg.block} (k={cfg.k} of {cfg.n_blk}), "
                                f"rank {cfg.rank}, batch {B}",
-                   "global_batch": B, "seq_len": 1, "parallelism": "none (1 GPU)"},
+                   "global_batch": B, "seq_len": 1, "parallelism": "none (1 GPU)",
+                   "decode_path": args.path, "launch": args.launch},
         "effective_weight_GBs": round(eff_gbs, 1),
         "hbm_frac_of_peak": round(eff_gbs / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_step": bytes_step,

@@ -188,10 +188,16 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    speculatively (its top-kp by scores predicted from the current layer's
  *    input, Eq. 2); 0 = automatic (2k, or fewer when the kernel's neuron slots
  *    hold fewer).  Never changes results.
+ *  LS_CFG_COOPERATIVE: 1 (default) launch the fused kernel with
+ *    hipLaunchCooperativeKernel, which guarantees that its one-workgroup-per-
+ *    compute-unit grid is resident at once; 0 a plain launch of the same grid
+ *    (residency then depends on the device being otherwise idle; every wait in
+ *    the kernel is bounded, so a workgroup that never starts makes the step fail
+ *    with LS_E_DEVICE at ls_ffn_sync instead of hanging).
  *  LS_CFG_TRACE_WG: -1 (default) off; otherwise the fused kernel records
  *    per-layer phase timestamps of that workgroup (see ls_debug_phase_trace).
  * LS_E_INVAL on an unknown key or value. */
-enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2 };
+enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3 };
 ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
 
 /* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for

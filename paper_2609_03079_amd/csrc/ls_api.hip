@@ -81,6 +81,7 @@ struct ls_ffn {
     int trace_wg = -1;            // LS_CFG_TRACE_WG
     uint64_t* trace = nullptr;    // device [L][kTracePoints]
     int spec_blocks = 0;          // LS_CFG_SPEC_BLOCKS
+    int cooperative = 1;          // LS_CFG_COOPERATIVE
 
     ls_status sticky = LS_OK;
     std::string err;
@@ -696,7 +697,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             a.err = c->dev_err;
             a.trace = c->trace_wg >= 0 ? c->trace : nullptr;
             a.trace_wg = c->trace_wg;
-            LS_HIP(c, timed(c, LS_K_DECODE, [&] { return ls::launch_decode_fused(s, a, c->n_wg, c->stream); }));
+            LS_HIP(c, timed(c, LS_K_DECODE, [&] { return ls::launch_decode_fused(s, a, c->n_wg, c->cooperative != 0, c->stream); }));
             c->last_fused = true;
             c->last_act_n = 0;
             c->last_act_B = 0;
@@ -743,6 +744,11 @@ ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
             LS_HIP(c, hipMemset(c->trace, 0, n * sizeof(uint64_t)));
         }
         c->trace_wg = (int)value;
+        return LS_OK;
+    }
+    if (key == LS_CFG_COOPERATIVE) {
+        if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "cooperative must be 0 or 1");
+        c->cooperative = (int)value;
         return LS_OK;
     }
     if (key == LS_CFG_SPEC_BLOCKS) {

@@ -46,6 +46,8 @@ size_t fused_mailbox_words(const Shape& s, int L);
 // dst[i] = value bits of the tagged words src[0..n)
 hipError_t launch_untag(const uint64_t* src, int n, float* dst, hipStream_t st);
 
-hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st);
+// cooperative: hipLaunchCooperativeKernel (guaranteed co-residency), else a plain launch
+hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, bool cooperative,
+                               hipStream_t st);
 
 }  // namespace ls

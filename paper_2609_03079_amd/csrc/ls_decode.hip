@@ -731,7 +731,7 @@ __global__ void tag_input_kernel(const float* __restrict__ x, int n, uint32_t ta
 }
 
 template <ls_dtype T, ls_act A>
-hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st) {
+hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hipStream_t st) {
     const int V = Wt<T>::V;
     const int nc = s.d / (V * 64);
     void* fn;
@@ -743,7 +743,8 @@ hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st
     if (e != hipSuccess) return e;
     FusedArgs copy = a;
     void* args[] = {&copy};
-    return hipLaunchCooperativeKernel(fn, dim3(n_wg), dim3(kThreads), args, 0, st);
+    if (coop) return hipLaunchCooperativeKernel(fn, dim3(n_wg), dim3(kThreads), args, 0, st);
+    return hipLaunchKernel(fn, dim3(n_wg), dim3(kThreads), args, 0, st);
 }
 
 __global__ void untag_kernel(const uint64_t* __restrict__ src, int n, float* __restrict__ dst) {
@@ -786,12 +787,12 @@ size_t fused_mailbox_words(const Shape& s, int L) {
     return (size_t)L * ((size_t)s.d + 2 * (size_t)s.n_blk + 2 * (size_t)s.F);
 }
 
-hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, hipStream_t st) {
+hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hipStream_t st) {
     const bool relu = s.act == LS_ACT_REGLU;
     switch (s.dtype) {
-        case LS_F32: return relu ? launch_t<LS_F32, LS_ACT_REGLU>(s, a, n_wg, st) : launch_t<LS_F32, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, st);
-        case LS_F16: return relu ? launch_t<LS_F16, LS_ACT_REGLU>(s, a, n_wg, st) : launch_t<LS_F16, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, st);
-        case LS_BF16: return relu ? launch_t<LS_BF16, LS_ACT_REGLU>(s, a, n_wg, st) : launch_t<LS_BF16, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, st);
+        case LS_F32: return relu ? launch_t<LS_F32, LS_ACT_REGLU>(s, a, n_wg, coop, st) : launch_t<LS_F32, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, coop, st);
+        case LS_F16: return relu ? launch_t<LS_F16, LS_ACT_REGLU>(s, a, n_wg, coop, st) : launch_t<LS_F16, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, coop, st);
+        case LS_BF16: return relu ? launch_t<LS_BF16, LS_ACT_REGLU>(s, a, n_wg, coop, st) : launch_t<LS_BF16, LS_ACT_SWIGLU_THRESH>(s, a, n_wg, coop, st);
     }
     return hipErrorInvalidValue;
 }

@@ -129,3 +129,23 @@ def test_fused_unsupported_shape_reports_and_auto_falls_back():
     with pytest.raises(lsffn.LsError) as e:
         f.ls_debug_decode_trace(1, scores=empty_f32(cfg.n_blk))
     assert e.value.status == lsffn.LS_E_STATE
+
+
+def test_plain_launch_matches_cooperative_bitwise():
+    cfg = FUSED["llama2_7b_4l"]
+    f, ws = _fused_ffn(cfg)
+    xs = lsgen.tokens(cfg, 5, 3, 1)
+    outs = []
+    for coop in (1, 0):
+        f.ls_configure(lsffn.LS_CFG_COOPERATIVE, coop)
+        o = []
+        for t in range(3):
+            x = dev_f32(xs[t])
+            f.ls_decode_step(x, 1, cfg.k)
+            o.append(host(x)[0].copy())
+        f.ls_ffn_sync()
+        outs.append(np.stack(o))
+    assert np.array_equal(outs[0], outs[1])
+    with pytest.raises(lsffn.LsError) as e:
+        f.ls_configure(lsffn.LS_CFG_COOPERATIVE, 2)
+    assert e.value.status == lsffn.LS_E_INVAL
