@@ -1,0 +1,111 @@
+"""GPU tests of the host-resident mode (ls_stream_weights).
+
+Blocks copied from pinned host memory into a bounded HBM cache, in priority
+order and in stages, must give bitwise the same layer output as HBM-resident
+weights for the same priority list: the summation order follows the list and
+never the cache slot a block landed in.  Also checks the cache accounting
+(hits + misses = n, bytes = misses x block bytes, repeated requests hit), the
+capacity error, and that a list entry whose block is not resident contributes
+nothing.  The oracle's sparse FFN on the same list bounds the values.
+"""
+import numpy as np
+import pytest
+
+import lsgen
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_03079_amd as lsffn  # noqa: E402
+from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2  # noqa: E402
+
+# A scaled-down 70B-shaped host-resident stack: 32 blocks of 128 neurons (768 KiB each),
+# 12 cache slots, so three layers of 8-block lists force evictions.
+CFG = lsgen.CONFIGS["llama2_70b_stream"].with_(n_layers=3, d_model=1024, d_ff=4096, block=128,
+                                                 rank=256)
+SLOTS = 12
+BLOCK_BYTES = 3 * CFG.block * CFG.d_model * CFG.elem_bytes
+
+
+def _pair():
+    ws = [lsgen.layer_weights(CFG, l) for l in range(CFG.n_layers)]
+    fr, _ = make_ffn(CFG, weights=ws)
+    fh, _ = make_ffn(CFG, weights=ws, residency=lsffn.LS_WEIGHTS_HOST,
+                     hbm_cache_bytes=SLOTS * BLOCK_BYTES)
+    return fr, fh, ws
+
+
+def _priority_list(f, layer, x, n):
+    scores = empty_f32(1, CFG.n_blk)
+    f.ls_predict(layer, x, 1, scores)
+    idx, cnt = empty_i32(n), empty_i32(1)
+    f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, n, 0.0, 0, n, idx, cnt)
+    return idx, cnt
+
+
+def _staged(f, layer, x, idx, cnt, n, K):
+    out = empty_f32(1, CFG.d_model)
+    for s in range(K):
+        lo, hi = s * n // K, (s + 1) * n // K
+        f.ls_sparse_ffn_step(layer, x, 1, idx, cnt, lo, hi, out)
+    return out
+
+
+@pytest.mark.parametrize("K", [1, 3])
+def test_streamed_equals_resident_bitwise(K):
+    fr, fh, ws = _pair()
+    n = 8
+    for t in range(2):
+        x = dev_f32(lsgen.tokens(CFG, t, 1, 1)[0])
+        for l in range(CFG.n_layers):
+            idx, cnt = _priority_list(fr, l, x, n)
+            idx_h = host(idx)
+            st = fh.ls_stream_weights(l, idx_h, n_stages=K)
+            assert st.hits + st.misses == n
+            assert st.bytes == st.misses * BLOCK_BYTES
+            y_h = _staged(fh, l, x, idx, cnt, n, K)
+            y_r = _staged(fr, l, x, idx, cnt, n, K)
+            a, b = host(y_h), host(y_r)
+            assert np.array_equal(a, b), (t, l, K)
+            x_np = host(x)[0].astype(np.float64)
+            y_ref = oracle.sparse_ffn(ws[l], oracle.mlp_input(host(x)[0], CFG.prenorm), idx_h,
+                                      CFG.block, CFG.act, ws[l].threshold)
+            assert rel_l2(a[0] - x_np, y_ref) <= Y_TOL[CFG.dtype]
+            x = y_h
+    fh.ls_ffn_sync()
+
+
+def test_cache_accounting_hits_capacity_and_invalidation():
+    fr, fh, ws = _pair()
+    blocks = np.arange(0, 20, 2, dtype=np.int32)  # 10 blocks
+    st = fh.ls_stream_weights(0, blocks, n_stages=2)
+    assert (st.hits, st.misses, st.bytes) == (0, 10, 10 * BLOCK_BYTES)
+    st = fh.ls_stream_weights(0, blocks[::-1], n_stages=1)   # same set, other order: all hits
+    assert (st.hits, st.misses, st.bytes, st.evictions) == (10, 0, 0, 0)
+    st = fh.ls_stream_weights(1, np.array([3, 5, 7, 9], np.int32))  # 2 free slots: 2 evictions
+    assert (st.hits, st.misses, st.evictions) == (0, 4, 2)
+    with pytest.raises(lsffn.LsError) as e:
+        fh.ls_stream_weights(2, np.arange(SLOTS + 1, dtype=np.int32))
+    assert e.value.status == lsffn.LS_E_CAPACITY
+    fh.ls_ffn_set_layer(1, ws[1])  # new weights for layer 1: its cached blocks are stale
+    st = fh.ls_stream_weights(1, np.array([3, 5], np.int32))
+    assert st.misses == 2
+    fh.ls_ffn_sync()
+
+
+def test_entries_not_resident_contribute_nothing():
+    fr, fh, ws = _pair()
+    x = dev_f32(lsgen.tokens(CFG, 4, 1, 1)[0])
+    idx, cnt = _priority_list(fr, 0, x, 6)
+    idx_h = host(idx)
+    fh.ls_stream_weights(0, idx_h[:4])          # only the first four become resident
+    y_h = _staged(fh, 0, x, idx, cnt, 6, 1)     # the list still names six blocks
+    idx4 = torch.from_numpy(idx_h[:4].copy()).to("cuda:0")
+    cnt4 = torch.tensor([4], dtype=torch.int32, device="cuda:0")
+    y_r = _staged(fr, 0, x, idx4, cnt4, 4, 1)
+    assert np.array_equal(host(y_h), host(y_r))
+    fh.ls_ffn_sync()
