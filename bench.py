@@ -86,6 +86,150 @@ def cpu_baseline(cfg, weights, xs, n_tokens: int):
             "cpu": platform.processor() or platform.machine()}
 
 
+def overlap_from_trace(d: str) -> dict:
+    """Copy/compute overlap from a rocprofv3 csv trace: the time during which a host-to-device
+    copy and a kernel are both active, over the kernels' busy time (interval unions)."""
+    import csv
+    import glob
+
+    def intervals(pattern):
+        out = []
+        for path in glob.glob(os.path.join(d, "**", pattern), recursive=True):
+            for r in csv.DictReader(open(path)):
+                out.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+        out.sort()
+        merged = []
+        for a, b in out:
+            if merged and a <= merged[-1][1]:
+                merged[-1][1] = max(merged[-1][1], b)
+            else:
+                merged.append([a, b])
+        return merged
+
+    k = intervals("*kernel_trace.csv")
+    c = intervals("*memory_copy_trace.csv")
+    busy_k = sum(b - a for a, b in k)
+    busy_c = sum(b - a for a, b in c)
+    both, j = 0, 0
+    for a, b in k:
+        while j < len(c) and c[j][1] <= a:
+            j += 1
+        jj = j
+        while jj < len(c) and c[jj][0] < b:
+            both += max(0, min(b, c[jj][1]) - max(a, c[jj][0]))
+            jj += 1
+    return {"kernel_busy_ms": busy_k / 1e6, "copy_busy_ms": busy_c / 1e6, "both_ms": both / 1e6,
+            "overlap_of_kernel_time": both / busy_k if busy_k else None}
+
+
+def bench_streaming(args, cfg) -> int:
+    """Host-resident stack: per layer predict -> select -> ls_stream_weights (misses copied from
+    pinned host memory in priority order, in stages) -> staged sparse steps that wait per stage.
+    The HBM cache holds the same fraction of all blocks as the full workload's budget."""
+    import numpy as np
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    full_blocks = cfg.n_layers * cfg.n_blk
+    L = args.layers or 6
+    cfg = cfg.with_(n_layers=L)
+    block_bytes = 3 * cfg.block * cfg.d_model * cfg.elem_bytes
+    cache_frac = cfg.hbm_cache_bytes / (full_blocks * block_bytes)
+    slots = max(cfg.k, int(cache_frac * L * cfg.n_blk))
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    t_setup = time.perf_counter()
+    f = lsffn.Ffn(n_layers=L, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank,
+                  max_batch=1, dtype=cfg.dtype, act=cfg.act, residency=lsffn.LS_WEIGHTS_HOST,
+                  prenorm_rms=int(cfg.prenorm), hbm_cache_bytes=slots * block_bytes, stream=stream)
+    weights = []
+    for l in range(L):
+        w = lsgen.layer_weights(cfg, l)
+        f.ls_ffn_set_layer(l, w)
+        weights.append(w if args.cpu_tokens > 0 else None)
+    W, K, S = args.warmup, args.steps, args.stages
+    xs = torch.from_numpy(lsgen.tokens(cfg, 0, W + K, 1)).to(dev)
+    scores = torch.empty(1, cfg.n_blk, dtype=torch.float32, device=dev)
+    idx = torch.empty(cfg.k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    xa = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
+    xb = torch.empty_like(xa)
+    # pinned host -> HBM peak of one large copy, the ceiling of this path
+    src = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(4):
+        dst.copy_(src, non_blocking=True)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    h2d_gbs = 4 * (1 << 30) / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    setup_s = time.perf_counter() - t_setup
+
+    totals = {"hits": 0, "misses": 0, "bytes": 0}
+
+    def step(x0, count):
+        xa.copy_(x0)
+        cur, nxt = xa, xb
+        for l in range(L):
+            f.ls_predict(l, cur, 1, scores)
+            f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 0, cfg.k, idx, cnt)
+            idx_h = idx.cpu().numpy()  # the host resolves hits and orders the copies
+            st = f.ls_stream_weights(l, idx_h, n_stages=S)
+            if count:
+                totals["hits"] += st.hits
+                totals["misses"] += st.misses
+                totals["bytes"] += st.bytes
+            for s_ in range(S):
+                lo, hi = s_ * cfg.k // S, (s_ + 1) * cfg.k // S
+                if hi > lo or s_ == 0:
+                    f.ls_sparse_ffn_step(l, cur, 1, idx, cnt, lo, hi, nxt)
+            cur, nxt = nxt, cur
+        return cur
+
+    for i in range(W):
+        step(xs[i], False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(xs[W + i], True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    copy_gbs = totals["bytes"] / wall / 1e9
+    n_req = totals["hits"] + totals["misses"]
+    cpu = None
+    if args.cpu_tokens > 0:
+        cpu = cpu_baseline(cfg, weights, lsgen.tokens(cfg, 0, W + K, 1), min(args.cpu_tokens, W + K))
+    out = {
+        "metric": "sparse-FFN decode tokens/sec and effective weight GB/s (% HBM peak), 1 GPU",
+        "value": round(K / wall, 3), "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(1e3 * wall / K, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": lsgen.DTYPE_NAMES[cfg.dtype], "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {L} of 80 layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, "
+                               f"block {cfg.block} (k={cfg.k} of {cfg.n_blk}), rank {cfg.rank}, batch 1, "
+                               f"host-resident blocks, HBM cache {slots} slots ({100 * cache_frac:.1f}% of "
+                               f"the blocks), {S} copy stages per layer",
+                   "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)", "decode_path": "kernels"},
+        "streaming": {"hit_rate": round(totals["hits"] / n_req, 4) if n_req else None,
+                      "copied_GB_per_token": round(totals["bytes"] / K / 1e9, 4),
+                      "copy_GBs": round(copy_gbs, 2), "h2d_peak_GBs": round(h2d_gbs, 2)},
+        "roofline": {"bound": "host_link", "kernel": "hipMemcpyAsync (pinned host -> HBM)",
+                     "achieved": round(copy_gbs, 2), "peak": round(h2d_gbs, 2), "unit": "GB/s",
+                     "frac": round(copy_gbs / h2d_gbs, 4), "traffic": None},
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +244,11 @@ def main() -> int:
     ap.add_argument("--launch", choices=("cooperative", "plain"), default="plain",
                     help="fused-kernel launch: a plain launch of the one-workgroup-per-CU grid on the idle "
                          "device (default; the launch rocprofv3 can trace) or hipLaunchCooperativeKernel")
+    ap.add_argument("--stages", type=int, default=8,
+                    help="host-resident workloads: copy stages per layer (events the compute waits on)")
+    ap.add_argument("--overlap-from-trace", default="", metavar="DIR",
+                    help="instead of the benchmark: copy/compute overlap from a rocprofv3 kernel + "
+                         "memory-copy trace (csv) in DIR")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark: copy MIB MiB device-to-device 4 times (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -108,6 +257,10 @@ def main() -> int:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               f"(this build has no multi-GPU path).", file=sys.stderr)
         return 2
+
+    if args.overlap_from_trace:
+        print(json.dumps(overlap_from_trace(args.overlap_from_trace)))
+        return 0
 
     import numpy as np
     import torch
@@ -129,9 +282,7 @@ def main() -> int:
     if args.layers:
         cfg = cfg.with_(n_layers=args.layers)
     if cfg.host_resident:
-        print("bench.py measures HBM-resident stacks; use the streaming test for host residency",
-              file=sys.stderr)
-        return 2
+        return bench_streaming(args, cfg)
     B, K, W = args.batch, args.steps, args.warmup
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
