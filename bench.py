@@ -71,18 +71,56 @@ def measured_traffic(kernel: str, cfg, n_layers_default: bool):
     return int(m_t.group(1)) if h.hexdigest() == m_h.group(1) else None
 
 
-def cpu_baseline(cfg, weights, xs, n_tokens: int):
-    """The CPU oracle (as it stands) on the first n_tokens decode steps of the same workload."""
+def mean_union_size(f, cfg, xs, B: int, lsffn, torch) -> float:
+    """Mean number of blocks per layer (the union over the B tokens) over the given steps,
+    replayed through ls_predict / ls_select_blocks / ls_sparse_ffn_step."""
+    dev = xs.device
+    scores = torch.empty(B, cfg.n_blk, dtype=torch.float32, device=dev)
+    cap = min(cfg.n_blk, B * cfg.k)
+    idx = torch.empty(cap, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    xa = torch.empty(B, cfg.d_model, dtype=torch.float32, device=dev)
+    xb = torch.empty_like(xa)
+    total, n = 0, 0
+    for t in range(xs.shape[0]):
+        xa.copy_(xs[t])
+        cur, nxt = xa, xb
+        for l in range(cfg.n_layers):
+            f.ls_predict(l, cur, B, scores)
+            f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+            f.ls_sparse_ffn_step(l, cur, B, idx, cnt, 0, cap, nxt)
+            total += int(cnt.item())
+            n += 1
+            cur, nxt = nxt, cur
+    return total / n
+
+
+def cpu_baseline(cfg, weights, xs, n_tokens: int, B: int = 1):
+    """The CPU oracle (as it stands) on the first n_tokens decode steps of the same workload:
+    at B = 1 its C layer step, at B > 1 its predictor, union selection and sparse FFN per token."""
+    import numpy as np
+
     import oracle
     t0 = time.perf_counter()
     for t in range(n_tokens):
-        x = xs[t, 0].copy()
+        if B == 1:
+            x = xs[t, 0].copy()
+            for l in range(cfg.n_layers):
+                _, _, _, x = oracle.layer_step(weights[l], cfg, x)
+            continue
+        x = xs[t, :B].astype(np.float64)
         for l in range(cfg.n_layers):
-            _, _, _, x = oracle.layer_step(weights[l], cfg, x)
+            w = weights[l]
+            h = np.stack([oracle.mlp_input(x[b], cfg.prenorm) for b in range(B)])
+            s = np.stack([oracle.predict(w.p1, w.p2, h[b]) for b in range(B)]).astype(np.float32)
+            idx, cnt = oracle.select(s, k=cfg.k, union_batch=True, cap=min(cfg.n_blk, B * cfg.k))
+            blocks = idx[:cnt[0]]
+            x = np.stack([x[b] + oracle.sparse_ffn(w, h[b], blocks, cfg.block, cfg.act, w.threshold)
+                          for b in range(B)]).astype(np.float32).astype(np.float64)
     dt = time.perf_counter() - t0
-    return {"value": n_tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+    return {"value": B * n_tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n_tokens} decode steps x {cfg.n_layers} layers of the same workload "
-                      f"(B=1), fp64 plain-C oracle, single thread, {dt:.1f} s",
+                      f"(B={B}), fp64 oracle, single thread, {dt:.1f} s",
             "cpu": platform.processor() or platform.machine()}
 
 
@@ -150,6 +188,7 @@ def bench_streaming(args, cfg) -> int:
         w = lsgen.layer_weights(cfg, l)
         f.ls_ffn_set_layer(l, w)
         weights.append(w if args.cpu_tokens > 0 else None)
+        print(f"set-up: {l + 1}/{L} layers", file=sys.stderr, flush=True)
     W, K, S = args.warmup, args.steps, args.stages
     xs = torch.from_numpy(lsgen.tokens(cfg, 0, W + K, 1)).to(dev)
     scores = torch.empty(1, cfg.n_blk, dtype=torch.float32, device=dev)
@@ -300,6 +339,8 @@ def main() -> int:
         w = lsgen.layer_weights(cfg, l)
         f.ls_ffn_set_layer(l, w)
         weights.append(w if keep_host else None)
+        if (l + 1) % 8 == 0:
+            print(f"set-up: {l + 1}/{cfg.n_layers} layers", file=sys.stderr, flush=True)
     xs = lsgen.tokens(cfg, 0, W + K, B)                      # [W+K, B, d] fp32
     x_dev = torch.from_numpy(xs).to(dev)                      # inputs resident in HBM
     torch.cuda.synchronize()
@@ -334,19 +375,21 @@ def main() -> int:
 
     step_s = wall / K
     tok_s = B * K / wall
-    if B != 1:
-        raise SystemExit("bench.py reports B=1 (the headline workload)")
-    U = cfg.k
-    bytes_layer = algorithmic_bytes_per_layer(cfg, U)
-    bytes_step = bytes_layer * cfg.n_layers
+    if B == 1:
+        U = float(cfg.k)
+    else:
+        # union sizes of the timed steps: an untimed replay through the per-call entry points
+        # (ls_decode_step equals their composition) with the same inputs
+        U = mean_union_size(f, cfg, x_dev[W:W + K], B, lsffn, torch)
+    bytes_step = int(round(sum(algorithmic_bytes_per_layer(cfg, U) for _ in range(cfg.n_layers))))
     eff_gbs = bytes_step / step_s / 1e9
 
     # dominant kernel: the one with the largest share of time; its algorithmic bytes per launch
     dom = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])
     s = cfg.elem_bytes
     per_launch_bytes = {
-        "gateup": s * (U * cfg.block * cfg.d_model * 2 + (U * cfg.block if cfg.gate_bias else 0)),
-        "down": s * U * cfg.block * cfg.d_model,
+        "gateup": int(s * (U * cfg.block * cfg.d_model * 2 + (U * cfg.block if cfg.gate_bias else 0))),
+        "down": int(s * U * cfg.block * cfg.d_model),
         "pred_p1": predictor_bytes(cfg) if predictor_bytes(cfg) < s * (cfg.d_model * cfg.rank + cfg.rank * cfg.n_blk)
                    else s * cfg.d_model * cfg.rank,
         "pred_p2": s * cfg.rank * cfg.n_blk,
@@ -365,7 +408,7 @@ def main() -> int:
 
     cpu = None
     if args.cpu_tokens > 0:
-        cpu = cpu_baseline(cfg, weights, xs, min(args.cpu_tokens, W + K))
+        cpu = cpu_baseline(cfg, weights, xs, min(args.cpu_tokens, W + K), B)
 
     out = {
         "metric": "sparse-FFN decode tokens/sec and effective weight GB/s (% HBM peak), 1 GPU",
@@ -388,6 +431,7 @@ def main() -> int:
         "effective_weight_GBs": round(eff_gbs, 1),
         "hbm_frac_of_peak": round(eff_gbs / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_step": bytes_step,
+        "blocks_per_layer": round(U, 2),
         "gpu_event_ms": round(gpu_ms, 3),
         "kernels": {k: {kk: round(vv, 3) if isinstance(vv, float) else vv for kk, vv in v.items()}
                     for k, v in per_kernel.items()},

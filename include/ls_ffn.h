@@ -194,10 +194,15 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    (residency then depends on the device being otherwise idle; every wait in
  *    the kernel is bounded, so a workgroup that never starts makes the step fail
  *    with LS_E_DEVICE at ls_ffn_sync instead of hanging).
+ *  LS_CFG_BATCH_MFMA: 1 (default) batches of 4 or more tokens run the
+ *    gate/up and down kernels on the matrix cores when the weights are 16-bit
+ *    and the block is a multiple of 32 (activations split into 16-bit hi and lo
+ *    parts, fp32 accumulation); 0 always uses the vector-ALU kernels.
  *  LS_CFG_TRACE_WG: -1 (default) off; otherwise the fused kernel records
  *    per-layer phase timestamps of that workgroup (see ls_debug_phase_trace).
  * LS_E_INVAL on an unknown key or value. */
-enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3 };
+enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3,
+       LS_CFG_BATCH_MFMA = 4 };
 ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
 
 /* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for

@@ -30,7 +30,7 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
-LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE = 0, 1, 2, 3
+LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA = range(5)
 PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "keys_barrier",
           "ctrl_ranked", "slot_map", "acts_published", "all_acts", "output_published", "gateup_done",
           "down_done", "worker_ranked", "early_gateup_done", "spare14", "spare15")

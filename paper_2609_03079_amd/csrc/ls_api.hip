@@ -746,6 +746,11 @@ ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
         c->trace_wg = (int)value;
         return LS_OK;
     }
+    if (key == LS_CFG_BATCH_MFMA) {
+        if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "batch MFMA must be 0 or 1");
+        c->shape.batch_mfma = (int)value;
+        return LS_OK;
+    }
     if (key == LS_CFG_COOPERATIVE) {
         if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "cooperative must be 0 or 1");
         c->cooperative = (int)value;

@@ -45,7 +45,12 @@ struct Shape {
     // 1: the predictor is kept as the fp32 product P2 P1 (one n_blk x d GEMV), chosen
     // when that matrix is no larger than the two factors in the weight type.
     int fold;
+    // 1: batches of kMfmaMinBatch or more tokens use the matrix-core gate/up and down
+    // kernels when the shape allows (16-bit weights, block a multiple of 32).
+    int batch_mfma = 1;
 };
+
+constexpr int kMfmaMinBatch = 4;
 
 // Fold decision: the product costs 4 n_blk d bytes, the factors (r d + n_blk r) elem bytes.
 inline int predictor_folds(int d, int r, int n_blk, ls_dtype t) {
@@ -71,5 +76,14 @@ hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                        int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
+
+// ---- matrix-core variants for B >= kMfmaMinBatch (ls_mfma.hip) ---------------------------
+bool mfma_path(const Shape& s, int B);
+hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                              const float* h, int B, const int32_t* idx, const int32_t* count,
+                              int begin, int end, float* a_buf, hipStream_t st);
+hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                            const float* a_buf, int B, const int32_t* idx, const int32_t* count,
+                            int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
 
 }  // namespace ls

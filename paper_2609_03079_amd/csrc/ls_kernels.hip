@@ -455,6 +455,8 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
 hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* h, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, float* a_buf, hipStream_t st) {
+    if (s.batch_mfma && mfma_path(s, B))
+        return launch_gateup_mfma(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st);
     const bool relu = s.act == LS_ACT_REGLU;
     switch (s.dtype) {
         case LS_F32:
@@ -497,6 +499,8 @@ static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                        int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+    if (s.batch_mfma && mfma_path(s, B))
+        return launch_down_mfma(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
     switch (s.dtype) {
         case LS_F32: return down_t<LS_F32>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
         case LS_F16: return down_t<LS_F16>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);

@@ -1,0 +1,280 @@
+// ls_mfma.hip - batched (B >= 4) gate/up and down kernels on the matrix cores of gfx950.
+//
+// With B tokens the gather GEMVs become small dense contractions: for a group of
+// 16 neurons, [16 x d] weight rows times [d x B] activations.  These kernels run them as
+// v_mfma_f32_16x16x32_{f16,bf16}: the weights are the A operand, loaded straight from
+// their rows (one 16-byte load per lane per step), and the activations are the B operand,
+// padded with zeros to 16 token columns.  Activations are fp32, so each one is split into
+// a 16-bit "hi" part and the 16-bit rounding of the remainder ("lo"); W.hi + W.lo carries
+// about 22 (f16) or 16 (bf16) significant bits of the activation, with fp32
+// accumulation in the matrix cores.  Results match the VALU kernels to fp32 rounding
+// (Eq. 1 of the paper, union over tokens as for the VALU path).
+//
+// Lane layout of v_mfma_f32_16x16x32 (lane l, i < 8 / i < 4):
+//   A[l % 16][8 (l / 16) + i],  B[8 (l / 16) + i][l % 16],  C[4 (l / 16) + i][l % 16].
+#include "ls_device.h"
+#include "ls_internal.h"
+
+namespace ls {
+namespace {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+// fp32 -> bfloat16 bits, round to nearest even (NaN stays a quiet NaN)
+__device__ inline unsigned short bf16_rne(float x) {
+    const unsigned u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (unsigned short)((u >> 16) | 0x40u);
+    return (unsigned short)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+// Split 8 fp32 values into hi and lo 16-bit operands of type T.
+template <ls_dtype T>
+struct Split;
+
+template <>
+struct Split<LS_F16> {
+    typedef f16x8 vec;
+    __device__ static inline void run(const float* x, vec& hi, vec& lo) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const _Float16 h = (_Float16)x[i];
+            hi[i] = h;
+            lo[i] = (_Float16)(x[i] - (float)h);
+        }
+    }
+    __device__ static inline vec from_raw(const u32x4& r) {
+        vec v;
+        __builtin_memcpy(&v, &r, 16);
+        return v;
+    }
+    __device__ static inline f32x4v mfma(const vec& a, const vec& b, const f32x4v& c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <>
+struct Split<LS_BF16> {
+    typedef s16x8 vec;
+    __device__ static inline void run(const float* x, vec& hi, vec& lo) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const unsigned short h = bf16_rne(x[i]);
+            hi[i] = (short)h;
+            lo[i] = (short)bf16_rne(x[i] - __uint_as_float((unsigned)h << 16));
+        }
+    }
+    __device__ static inline vec from_raw(const u32x4& r) {
+        vec v;
+        __builtin_memcpy(&v, &r, 16);
+        return v;
+    }
+    __device__ static inline f32x4v mfma(const vec& a, const vec& b, const f32x4v& c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+__device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
+    int c = *count;
+    c = c < 0 ? 0 : (c > n_blk ? n_blk : c);
+    return end < c ? end : c;
+}
+
+constexpr int kWaves = 4;
+constexpr int kUnroll = 4;  // K steps in flight per wave
+
+// One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry); the 4 waves split
+// the d / 32 K steps.  a_buf[tok * F + e * blk + q] as the VALU kernel writes it.
+template <ls_dtype T, ls_act A>
+__global__ __launch_bounds__(256) void gateup_mfma_kernel(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const void* __restrict__ bias, float thresh, const float* __restrict__ h, int B, int d, int blk,
+    int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
+    int end, float* __restrict__ a_buf) {
+    using S = Split<T>;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int groups_per_entry = blk / 16;
+    const int e = begin + (int)blockIdx.x / groups_per_entry;
+    const int r0 = ((int)blockIdx.x % groups_per_entry) * 16;
+    if (e >= list_end_m(count, end, n_blk)) return;
+    const int b = idx[e];
+    const int slot = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
+    if (slot < 0) {  // invalid id or block not in the cache: the entry contributes nothing
+        if (threadIdx.x < 16 * B) {
+            const int tok = threadIdx.x / 16, r = threadIdx.x % 16;
+            a_buf[(size_t)tok * F + (size_t)e * blk + r0 + r] = 0.f;
+        }
+        return;
+    }
+    const size_t row_bytes = (size_t)d * 2;
+    const uint8_t* base = blocks + (size_t)slot * block_bytes;
+    const int row = r0 + (lane & 15);
+    const uint8_t* grow = base + (size_t)row * row_bytes;
+    const uint8_t* urow = base + (size_t)(blk + row) * row_bytes;
+    const int tok = lane & 15;
+    const bool tok_ok = tok < B;
+    const float* hrow = h + (size_t)(tok_ok ? tok : 0) * d;
+    const int ksteps = d / 32;
+    f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = wave; k0 < ksteps; k0 += kWaves * kUnroll) {
+        u32x4 rg[kUnroll], ru[kUnroll];
+        f32x4 hx[kUnroll][2];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int ks = k0 + kWaves * u;
+            const int kk = ks * 32 + 8 * (lane >> 4);  // this lane's 8 K values
+            const bool ok = ks < ksteps;
+            rg[u] = ok ? ld_stream(reinterpret_cast<const u32x4*>(grow + (size_t)kk * 2)) : u32x4{0u, 0u, 0u, 0u};
+            ru[u] = ok ? ld_stream(reinterpret_cast<const u32x4*>(urow + (size_t)kk * 2)) : u32x4{0u, 0u, 0u, 0u};
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+            hx[u][0] = ok && tok_ok ? reinterpret_cast<const f32x4*>(hrow + kk)[0] : z;
+            hx[u][1] = ok && tok_ok ? reinterpret_cast<const f32x4*>(hrow + kk)[1] : z;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const float xv[8] = {hx[u][0].x, hx[u][0].y, hx[u][0].z, hx[u][0].w,
+                                 hx[u][1].x, hx[u][1].y, hx[u][1].z, hx[u][1].w};
+            typename S::vec hi, lo;
+            S::run(xv, hi, lo);
+            const typename S::vec wg = S::from_raw(rg[u]), wu = S::from_raw(ru[u]);
+            cg = S::mfma(wg, hi, cg);
+            cg = S::mfma(wg, lo, cg);
+            cu = S::mfma(wu, hi, cu);
+            cu = S::mfma(wu, lo, cu);
+        }
+    }
+    // lane l holds rows 4 (l / 16) + i, token l % 16 of this wave's partial sums
+    __shared__ float pg[kWaves][16][16], pu[kWaves][16][16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        pg[wave][4 * (lane >> 4) + i][lane & 15] = cg[i];
+        pu[wave][4 * (lane >> 4) + i][lane & 15] = cu[i];
+    }
+    __syncthreads();
+    if (threadIdx.x < 16 * B) {
+        const int t = threadIdx.x / 16, r = threadIdx.x % 16;
+        const float g = ((pg[0][r][t] + pg[1][r][t]) + pg[2][r][t]) + pg[3][r][t] +
+                        (bias ? Wt<T>::scalar(bias, (size_t)b * blk + r0 + r) : 0.f);
+        const float u = ((pu[0][r][t] + pu[1][r][t]) + pu[2][r][t]) + pu[3][r][t];
+        float a;
+        if (A == LS_ACT_REGLU) {
+            a = fmaxf(g, 0.f) * u;
+        } else {
+            const float sg = g / (1.f + expf(-g));
+            a = fabsf(sg) > thresh ? sg * u : 0.f;
+        }
+        a_buf[(size_t)t * F + (size_t)e * blk + r0 + r] = a;
+    }
+}
+
+// One workgroup per 16-column tile of y; the waves split the list entries.  The down piece
+// of a block for one tile is [blk/8][16][8]: K step s of an entry is the contiguous kilobyte
+// of chunks 64 s .. 64 s + 63, exactly one A fragment.
+template <ls_dtype T>
+__global__ __launch_bounds__(256) void down_mfma_kernel(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const float* __restrict__ a_buf, int B, int F, int d, int blk, int n_blk,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
+    const float* __restrict__ x_in, float* __restrict__ x_acc) {
+    using S = Split<T>;
+    const int tile = blockIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n_end = list_end_m(count, end, n_blk);
+    const size_t down_off = (size_t)2 * blk * d * 2 + (size_t)tile * blk * kColTile * 2;
+    const int ksteps = blk / 32;
+    const int tok = lane & 15;
+    const bool tok_ok = tok < B;
+    f32x4v c = {0.f, 0.f, 0.f, 0.f};
+    for (int e = begin + wave; e < n_end; e += kWaves) {
+        const int b = idx[e];
+        const int slot = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
+        if (slot < 0) continue;  // contributes nothing
+        const u32x4* piece = reinterpret_cast<const u32x4*>(blocks + (size_t)slot * block_bytes + down_off);
+        const float* arow = a_buf + (size_t)(tok_ok ? tok : 0) * F + (size_t)e * blk;
+        for (int s0 = 0; s0 < ksteps; s0 += kUnroll) {
+            u32x4 w[kUnroll];
+            f32x4 av[kUnroll][2];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int s = s0 + u;
+                const bool ok = s < ksteps;
+                w[u] = ok ? ld_stream(piece + 64 * s + lane) : u32x4{0u, 0u, 0u, 0u};
+                const int n0 = 32 * s + 8 * (lane >> 4);
+                const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+                av[u][0] = ok && tok_ok ? reinterpret_cast<const f32x4*>(arow + n0)[0] : z;
+                av[u][1] = ok && tok_ok ? reinterpret_cast<const f32x4*>(arow + n0)[1] : z;
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const float xv[8] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w,
+                                     av[u][1].x, av[u][1].y, av[u][1].z, av[u][1].w};
+                typename S::vec hi, lo;
+                S::run(xv, hi, lo);
+                const typename S::vec wv = S::from_raw(w[u]);
+                c = S::mfma(wv, hi, c);
+                c = S::mfma(wv, lo, c);
+            }
+        }
+    }
+    // lane l holds columns 4 (l / 16) + i of the tile for token l % 16
+    __shared__ float part[kWaves][16][16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[wave][4 * (lane >> 4) + i][lane & 15] = c[i];
+    __syncthreads();
+    if (threadIdx.x < 16 * B) {
+        const int t = threadIdx.x / 16, col = threadIdx.x % 16;
+        const float y = ((part[0][col][t] + part[1][col][t]) + part[2][col][t]) + part[3][col][t];
+        const size_t m = (size_t)t * d + (size_t)tile * kColTile + col;
+        x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
+    }
+}
+
+}  // namespace
+
+bool mfma_path(const Shape& s, int B) {
+    return B >= kMfmaMinBatch && B <= 16 && s.dtype != LS_F32 && s.blk % 32 == 0 && s.d % 32 == 0;
+}
+
+hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                              const float* h, int B, const int32_t* idx, const int32_t* count,
+                              int begin, int end, float* a_buf, hipStream_t st) {
+    const long groups = (long)(end - begin) * (s.blk / 16);
+    if (groups <= 0) return hipSuccess;
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+    const dim3 grid((unsigned)groups), blk(256);
+    const bool relu = s.act == LS_ACT_REGLU;
+#define LS_GUM(TT, AA)                                                                           \
+    hipLaunchKernelGGL((gateup_mfma_kernel<TT, AA>), grid, blk, 0, st, L.blocks, bb, slot_table, \
+                       L.bias, L.threshold, h, B, s.d, s.blk, s.n_blk, s.F, idx, count, begin,  \
+                       end, a_buf)
+    if (s.dtype == LS_F16) {
+        if (relu) LS_GUM(LS_F16, LS_ACT_REGLU);
+        else LS_GUM(LS_F16, LS_ACT_SWIGLU_THRESH);
+    } else if (s.dtype == LS_BF16) {
+        if (relu) LS_GUM(LS_BF16, LS_ACT_REGLU);
+        else LS_GUM(LS_BF16, LS_ACT_SWIGLU_THRESH);
+    } else {
+        return hipErrorInvalidValue;
+    }
+#undef LS_GUM
+    return hipGetLastError();
+}
+
+hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
+                            const float* a_buf, int B, const int32_t* idx, const int32_t* count,
+                            int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+    const dim3 grid(s.d / kColTile), blk(256);
+    if (s.dtype == LS_F16)
+        hipLaunchKernelGGL(down_mfma_kernel<LS_F16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
+                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+    else if (s.dtype == LS_BF16)
+        hipLaunchKernelGGL(down_mfma_kernel<LS_BF16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
+                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace ls

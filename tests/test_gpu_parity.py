@@ -31,6 +31,9 @@ SMALL = {
                                              rank=128, keep_pct=50),
     "f32_stack": C["c1_reglu_512"].with_(n_layers=3, prenorm=True, d_model=320, d_ff=960,
                                          block=40, rank=64),
+    # 16-bit weights, block a multiple of 32: batches of 4+ run on the matrix cores
+    "f16_b64": C["llama2_7b_ffn"].with_(n_layers=2, d_model=640, d_ff=1728, block=64, rank=192,
+                                        keep_pct=30),
 }
 
 
@@ -125,7 +128,7 @@ def test_select_bit_exact(B, kind, n_blk):
 
 
 @pytest.mark.parametrize("name", list(SMALL))
-@pytest.mark.parametrize("B", [1, 3])
+@pytest.mark.parametrize("B", [1, 3, 4, 8])
 def test_sparse_step_teacher_forced(name, B):
     cfg = SMALL[name]
     f, ws = make_ffn(cfg, max_batch=B)
@@ -329,3 +332,30 @@ def test_full_size_layers_sampled(cfg_name):
         y = host(x_out).astype(np.float64) - xi[None, :]
         _check_y(f, ws[l], cfg, xi[None, :], y, blocks, Y_TOL[cfg.dtype], (cfg_name, l))
         x_in, x_out = x_out, x_in
+
+
+@pytest.mark.parametrize("name", ["f16_b64", "bf16_swiglu"])
+@pytest.mark.parametrize("B", [4, 8])
+def test_batch_matrix_core_path_matches_vector_path(name, B):
+    """The matrix-core kernels (B >= 4) against the vector-ALU kernels on the same union list:
+    both accumulate in fp32, the activations enter the matrix cores as hi + lo 16-bit parts."""
+    cfg = SMALL[name]
+    f, ws = make_ffn(cfg, max_batch=B)
+    xs = lsgen.tokens(cfg, 11, 1, B)[0]
+    x_in = dev_f32(xs)
+    scores = empty_f32(B, cfg.n_blk)
+    cap = min(cfg.n_blk, B * cfg.k)
+    idx, cnt = empty_i32(cap), empty_i32(1)
+    f.ls_predict(0, x_in, B, scores)
+    f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+    ys = []
+    for mfma in (1, 0):
+        f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, mfma)
+        x_out = empty_f32(B, cfg.d_model)
+        f.ls_sparse_ffn_step(0, x_in, B, idx, cnt, 0, cap, x_out)
+        ys.append(host(x_out).astype(np.float64) - xs.astype(np.float64))
+    tol = 1e-5 if cfg.act == lsgen.ACT_REGLU else Y_TOL[cfg.dtype]
+    for b in range(B):
+        assert rel_l2(ys[0][b], ys[1][b]) <= tol, (name, B, b, rel_l2(ys[0][b], ys[1][b]))
+    with pytest.raises(lsffn.LsError):
+        f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, 2)
