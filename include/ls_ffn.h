@@ -171,7 +171,9 @@ ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_
  * stream.  ls_kernel_timing synchronises the stream, folds the finished event
  * pairs into per-kernel totals and returns the total milliseconds and launch
  * count of one kernel id since the last reset; reset != 0 clears all totals.
- * Kernel ids: 0 MLP input, 1 predictor projection (or the folded predictor),
+ * Kernel ids: 0 MLP input (the RMS prenorm is computed inside the predictor and
+ * gate/up kernels, so nothing is launched under this id), 1 predictor projection
+ * (or the folded predictor),
  * 2 predictor head (not launched when the predictor is folded),
  * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step. */
 enum { LS_K_PRENORM = 0, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN,

@@ -30,7 +30,6 @@ struct ls_ffn {
     std::vector<uint8_t> is_set;
 
     // workspaces (device)
-    float* h = nullptr;       // [maxB, d]
     float* z = nullptr;       // [maxB, r]
     float* scores = nullptr;  // [maxB, n_blk]
     int32_t* idx = nullptr;   // [maxB, n_blk]
@@ -240,7 +239,7 @@ ls_status validate_desc(const ls_ffn_desc* d) {
 void free_all(ls_ffn* c) {
     for (auto p : c->arena) if (p) (void)hipFree(p);
     c->arena.clear();
-    for (void* p : {(void*)c->h, (void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
+    for (void* p : {(void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
                     (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
                     (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err,
                     (void*)c->trace})
@@ -370,7 +369,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             if (hipEventCreateWithFlags(&c->table_uploaded[l], hipEventDisableTiming) != hipSuccess)
                 return bail(LS_E_DEVICE, "event creation failed");
     }
-    if (dmalloc(&c->h, (size_t)B * s.d) != hipSuccess || dmalloc(&c->z, (size_t)B * (s.fold ? 1 : s.r)) != hipSuccess ||
+    if (dmalloc(&c->z, (size_t)B * (s.fold ? 1 : s.r)) != hipSuccess ||
         dmalloc(&c->scores, (size_t)B * s.n_blk) != hipSuccess ||
         dmalloc(&c->idx, (size_t)B * s.n_blk) != hipSuccess || dmalloc(&c->count, (size_t)B) != hipSuccess ||
         dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess) {
@@ -490,15 +489,17 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
     return LS_OK;
 }
 
-// scores = P2 (P1 h) from c->h: one GEMV over the folded rows, or the two factors in turn.
-static ls_status predictor_gemv(ls_ffn* c, const ls::LayerDev& L, int B, float* scores) {
+// scores = P2 (P1 h) for the layer input x (h = its RMS prenorm, applied inside the first
+// GEMV): one GEMV over the folded rows, or the two factors in turn.
+static ls_status predictor_gemv(ls_ffn* c, const ls::LayerDev& L, const float* x, int B, float* scores) {
     const Shape& s = c->shape;
+    const bool rms = s.prenorm != 0;
     if (s.fold) {
-        LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(LS_F32, L.pf, s.n_blk, s.d, 1, s.n_blk, c->h, B, scores, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(LS_F32, L.pf, s.n_blk, s.d, 1, s.n_blk, x, B, rms, scores, c->stream); }));
         return LS_OK;
     }
-    LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, s.G, s.p1_rpw, c->h, B, c->z, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, scores, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_PRED_P1, [&] { return ls::launch_gemv_rows(s.dtype, L.p1, s.r, s.d, s.G, s.p1_rpw, x, B, rms, c->z, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_PRED_P2, [&] { return ls::launch_gemv_rows(s.dtype, L.p2, s.n_blk, s.r, s.G, s.p2_rpw, c->z, B, false, scores, c->stream); }));
     return LS_OK;
 }
 
@@ -509,9 +510,7 @@ ls_status ls_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, float*
     if (!x || !scores) return fail(c, LS_E_INVAL, "null pointer");
     if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
     if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
-    const Shape& s = c->shape;
-    LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, x, B, c->h, c->stream); }));
-    return predictor_gemv(c, c->dev[layer], B, scores);
+    return predictor_gemv(c, c->dev[layer], x, B, scores);
 }
 
 ls_status ls_select_blocks(ls_ffn* c, const float* scores, int32_t B, ls_sel_mode mode, int32_t k,
@@ -571,8 +570,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
         st = wait_stages(c, layer, begin, end);
         if (st != LS_OK) return st;
     }
-    LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, x_in, B, c->h, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, c->h, B, idx, count, begin, end, c->a, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, x_in, B, idx, count, begin, end, c->a, c->stream); }));
     LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream); }));
     if (c->desc.residency == LS_WEIGHTS_HOST) LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
     c->last_act_n = (int64_t)end * s.blk;
@@ -711,13 +709,12 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
     float* nxt = c->xbuf;
     for (int l = 0; l < c->desc.n_layers; ++l) {
         const ls::LayerDev& L = c->dev[l];
-        LS_HIP(c, timed(c, LS_K_PRENORM, [&] { return ls::launch_prenorm(s, cur, B, c->h, c->stream); }));
-        st = predictor_gemv(c, L, B, c->scores);
+        st = predictor_gemv(c, L, cur, B, c->scores);
         if (st != LS_OK) return st;
         LS_HIP(c, timed(c, LS_K_SELECT, [&] {
             return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count, c->stream);
         }));
-        LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, nullptr, c->h, B, c->idx, c->count, 0, cap, c->a, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, nullptr, cur, B, c->idx, c->count, 0, cap, c->a, c->stream); }));
         LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->stream); }));
         std::swap(cur, nxt);
     }

@@ -93,6 +93,9 @@ __device__ inline float wave_sum_dpp(float v) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
+// RMS prenorm scale of a vector of d elements whose squares sum to ss
+__device__ inline float rms_scale(float ss, int d) { return 1.f / sqrtf(ss / (float)d + 1e-6f); }
+
 __device__ inline float wave_sum(float v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);

@@ -58,10 +58,13 @@ inline int predictor_folds(int d, int r, int n_blk, ls_dtype t) {
 }
 
 // ---- kernel launchers (ls_kernels.hip) -------------------------------------------------
-hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st);
-// out[b, i] = W[s(i), :] . v[b, :] with s(i) = (i % G) * rpw + i / G (the grouped row order)
+// The MLP input h = x / sqrt(mean(x^2) + 1e-6) is never materialised: a kernel that reads x
+// for a dot product also sums x^2 and scales the dot product (h.w = scale * (x.w)).
+//
+// out[b, i] = c_b * W[s(i), :] . v[b, :] with s(i) = (i % G) * rpw + i / G (the grouped row
+// order); c_b = the RMS scale of v[b, :] when rms, else 1.
 hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G, int rpw,
-                            const float* v, int B, float* out, hipStream_t st);
+                            const float* v, int B, bool rms, float* out, hipStream_t st);
 // out[i, j] = sum_m P2[i, m] P1[m, j] (fp64 accumulation in m order, rounded once to
 // fp32); P1 [r, d], P2 [n_blk, r] row-major in the weight type.
 hipError_t launch_fold_predictor(ls_dtype t, const void* P1, const void* P2, int r, int d, int n_blk,
@@ -70,8 +73,9 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st);
 // slot_table: null in resident mode (block b lives at blocks + b*block_bytes); else
 // device int32 [n_blk] giving the cache slot of block b, relative to `blocks`.
+// x: the layer input [B, d]; the RMS scale is applied when s.prenorm
 hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
-                         const float* h, int B, const int32_t* idx, const int32_t* count,
+                         const float* x, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, float* a_buf, hipStream_t st);
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
@@ -80,7 +84,7 @@ hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_ta
 // ---- matrix-core variants for B >= kMfmaMinBatch (ls_mfma.hip) ---------------------------
 bool mfma_path(const Shape& s, int B);
 hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
-                              const float* h, int B, const int32_t* idx, const int32_t* count,
+                              const float* x, int B, const int32_t* idx, const int32_t* count,
                               int begin, int end, float* a_buf, hipStream_t st);
 hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                             const float* a_buf, int B, const int32_t* idx, const int32_t* count,

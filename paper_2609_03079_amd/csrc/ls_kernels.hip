@@ -18,56 +18,35 @@
 namespace ls {
 namespace {
 
-// ---- MLP input --------------------------------------------------------------------------
-// h = x (no prenorm) or h = x / sqrt(mean(x^2) + 1e-6).  One workgroup per token; the sum of
-// squares is reduced in a fixed order (per-thread strided sums, wave butterfly, then waves
-// in index order).
-__global__ __launch_bounds__(256) void prenorm_kernel(const float* __restrict__ x, int d, int rms,
-                                                      float* __restrict__ h) {
-    const int b = blockIdx.x;
-    const float* xb = x + (size_t)b * d;
-    float* hb = h + (size_t)b * d;
-    float scale = 1.f;
-    if (rms) {
-        __shared__ float part[4];
-        float ss = 0.f;
-        for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xb[i], xb[i], ss);
-        ss = wave_sum(ss);
-        if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
-        __syncthreads();
-        float tot = ((part[0] + part[1]) + part[2]) + part[3];
-        scale = 1.f / sqrtf(tot / (float)d + 1e-6f);
-    }
-    for (int i = threadIdx.x; i < d; i += 256) hb[i] = xb[i] * scale;
-}
-
-// ---- GEMV over rows: out[b, row] = sum_c W[row, c] * v[b, c] ------------------------------
-template <ls_dtype T, int B>
+// ---- GEMV over rows: out[b, row] = c_b * sum_c W[row, c] * v[b, c] ------------------------
+// c_b = rms_scale of v[b, :] when RMS (the MLP input of a prenorm stack), else 1.
+template <ls_dtype T, int B, bool RMS>
 __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
                                                         int cols, int G, int rpw,
                                                         const float* __restrict__ v,
                                                         float* __restrict__ out) {
+    // one workgroup per row; its 4 waves split the row's 16-byte chunks, then a fixed-order
+    // sum of the 4 wave totals
     constexpr int V = Wt<T>::V;
-    constexpr int U = 8;  // 16-byte loads in flight per lane
-    const int lane = threadIdx.x & 63;
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= rows) return;
+    constexpr int U = 4;  // 16-byte loads in flight per lane
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int row = blockIdx.x;
     const int nchunk = cols / V;
     const int srow = (row % G) * rpw + row / G;
     const u32x4* wr = reinterpret_cast<const u32x4*>(W + (size_t)srow * cols * Wt<T>::kBytes);
-    float acc[B];
+    float acc[B], ss[B];
 #pragma unroll
-    for (int b = 0; b < B; ++b) acc[b] = 0.f;
-    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+    for (int b = 0; b < B; ++b) acc[b] = ss[b] = 0.f;
+    for (int c0 = threadIdx.x; c0 < nchunk; c0 += 256 * U) {
         u32x4 raw[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
+            const int c = c0 + u * 256;
             raw[u] = c < nchunk ? ld_stream(wr + c) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
+            const int c = c0 + u * 256;
             if (c < nchunk) {
                 float w[V];
                 Wt<T>::widen(raw[u], w);
@@ -81,74 +60,161 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
                         acc[b] = fmaf(w[4 * q + 1], x4.y, acc[b]);
                         acc[b] = fmaf(w[4 * q + 2], x4.z, acc[b]);
                         acc[b] = fmaf(w[4 * q + 3], x4.w, acc[b]);
+                        if (RMS) {
+                            ss[b] = fmaf(x4.x, x4.x, ss[b]);
+                            ss[b] = fmaf(x4.y, x4.y, ss[b]);
+                            ss[b] = fmaf(x4.z, x4.z, ss[b]);
+                            ss[b] = fmaf(x4.w, x4.w, ss[b]);
+                        }
                     }
                 }
             }
         }
     }
+    __shared__ float part[4][B], pss[4][B];
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-        const float s = wave_sum(acc[b]);
-        if (lane == 0) out[(size_t)b * rows + row] = s;
+        const float s = wave_sum_dpp(acc[b]);
+        const float q = RMS ? wave_sum_dpp(ss[b]) : 0.f;
+        if (lane == 0) {
+            part[wave][b] = s;
+            pss[wave][b] = q;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < B) {
+        const int b = threadIdx.x;
+        const float dot = ((part[0][b] + part[1][b]) + part[2][b]) + part[3][b];
+        const float sc = RMS ? rms_scale(((pss[0][b] + pss[1][b]) + pss[2][b]) + pss[3][b], cols) : 1.f;
+        out[(size_t)b * rows + row] = dot * sc;
     }
 }
 
 // ---- block selection --------------------------------------------------------------------
+// One workgroup.  Wave w selects for tokens w, w + waves, ...: the keys of a token sit in
+// registers (Q per lane); top-k finds the k-th largest key T by a bitwise search with wave
+// ballots (the largest T with at least k keys >= T) and takes every key > T plus the first
+// keys equal to T by index; the threshold test is key > key(tau) on non-NaN scores.  Members
+// are compacted by ballot prefix, then ranked among themselves (key descending, index
+// ascending) so the output is in priority order.  Union: the OR of the tokens' sets, ranked
+// by each block's largest key over all tokens.
+constexpr int kSelQ = kMaxBlocks / 64;
+
 __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ scores, int B,
                                                       int n, int mode, int k, float tau,
                                                       int union_batch, int cap,
                                                       int32_t* __restrict__ idx,
                                                       int32_t* __restrict__ count) {
-    __shared__ uint32_t key[kMaxBlocks];
-    __shared__ uint32_t ukey[kMaxBlocks];
-    __shared__ uint8_t member[kMaxBlocks];
-    __shared__ int cnt[kMaxBatch + 1];
+    __shared__ uint32_t key[kMaxBatch][kMaxBlocks];
+    __shared__ uint8_t memb[kMaxBatch][kMaxBlocks];
+    __shared__ int16_t mlist[kMaxBatch][kMaxBlocks];
+    __shared__ int16_t ulist[kMaxBlocks];
+    __shared__ int ucount;
     const int tid = threadIdx.x, nt = blockDim.x;
+    const int wave = tid >> 6, lane = tid & 63, nwaves = nt >> 6;
     const bool do_union = union_batch && B > 1;
-    for (int i = tid; i < n; i += nt) {
-        member[i] = 0;
-        ukey[i] = 0u;
-    }
-    if (tid <= kMaxBatch) cnt[tid] = 0;
-    for (int b = 0; b < B; ++b) {
-        __syncthreads();
-        for (int i = tid; i < n; i += nt) key[i] = order_key(scores[(size_t)b * n + i]);
-        __syncthreads();
-        for (int i = tid; i < n; i += nt) {
-            const uint32_t ki = key[i];
-            int rank = 0;
-            for (int j = 0; j < n; ++j) {
-                const uint32_t kj = key[j];
-                rank += (kj > ki) | ((kj == ki) & (j < i));
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int Qn = (n + 63) / 64;
+    for (int b = wave; b < B; b += nwaves) {
+        uint32_t ok[kSelQ];
+#pragma unroll
+        for (int q = 0; q < kSelQ; ++q) {
+            const int i = q * 64 + lane;
+            ok[q] = 0u;
+            if (q < Qn && i < n) {
+                ok[q] = order_key(scores[(size_t)b * n + i]);
+                key[b][i] = ok[q];
             }
-            const float si = scores[(size_t)b * n + i];
-            const bool sel = (mode == LS_SEL_TOPK) ? (rank < k) : (!isnan(si) && si > tau);
-            if (sel) {
-                member[i] = 1;
-                if (!do_union) idx[(size_t)b * cap + rank] = i;
-                atomicAdd(&cnt[b], 1);
+        }
+        // membership rule: key > T, or key == T among the first `rem` such by index
+        uint32_t T = 0u;
+        int rem = 0;
+        bool thr_mode = mode != LS_SEL_TOPK;
+        if (!thr_mode) {
+            for (int bit = 31; bit >= 0; --bit) {
+                const uint32_t c = T | (1u << bit);
+                int cnt = 0;
+#pragma unroll
+                for (int q = 0; q < kSelQ; ++q)
+                    if (q < Qn) cnt += __popcll(__ballot(ok[q] >= c));
+                if (cnt >= k) T = c;
             }
-            ukey[i] = ki > ukey[i] ? ki : ukey[i];
+            int gt = 0;
+#pragma unroll
+            for (int q = 0; q < kSelQ; ++q)
+                if (q < Qn) gt += __popcll(__ballot(ok[q] > T));
+            rem = k - gt;
+        }
+        const uint32_t ktau = isnan(tau) ? 0xffffffffu : order_key(tau);
+        int m = 0, eq_before = 0;
+#pragma unroll
+        for (int q = 0; q < kSelQ; ++q) {
+            if (q < Qn) {
+                const int i = q * 64 + lane;
+                const bool valid = i < n;
+                bool mem;
+                if (thr_mode) {
+                    mem = valid && ok[q] != 0u && ok[q] > ktau;
+                } else {
+                    const bool eq = valid && ok[q] == T;
+                    const uint64_t eqb = __ballot(eq);
+                    mem = valid && (ok[q] > T || (eq && eq_before + __popcll(eqb & below) < rem));
+                    eq_before += __popcll(eqb);
+                }
+                const uint64_t mb = __ballot(mem);
+                if (valid) memb[b][i] = mem ? 1 : 0;
+                if (mem) mlist[b][m + __popcll(mb & below)] = (int16_t)i;
+                m += __popcll(mb);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        if (!do_union) {
+            for (int p = lane; p < m; p += 64) {
+                const int ip = mlist[b][p];
+                const uint32_t kp = key[b][ip];
+                int rank = 0;
+                for (int j = 0; j < m; ++j) {
+                    const int ij = mlist[b][j];
+                    const uint32_t kj = key[b][ij];
+                    rank += (kj > kp) | ((kj == kp) & (ij < ip));
+                }
+                idx[(size_t)b * cap + rank] = ip;
+            }
+            if (lane == 0) count[b] = m;
         }
     }
+    if (!do_union) return;
     __syncthreads();
-    if (!do_union) {
-        if (tid < B) count[tid] = cnt[tid];
-        return;
+    // union members and their keys (largest over all tokens), compacted by wave 0
+    if (wave == 0) {
+        int u = 0;
+        for (int q = 0; q < Qn; ++q) {
+            const int i = q * 64 + lane;
+            bool in = false;
+            if (i < n)
+                for (int b = 0; b < B; ++b) in |= memb[b][i] != 0;
+            const uint64_t ub = __ballot(in);
+            if (in) ulist[u + __popcll(ub & below)] = (int16_t)i;
+            u += __popcll(ub);
+        }
+        if (lane == 0) ucount = u;
     }
-    for (int i = tid; i < n; i += nt) {
-        if (!member[i]) continue;
-        const uint32_t ki = ukey[i];
+    __syncthreads();
+    const int U = ucount;
+    for (int p = tid; p < U; p += nt) {
+        const int ip = ulist[p];
+        uint32_t kp = 0u;
+        for (int b = 0; b < B; ++b) kp = key[b][ip] > kp ? key[b][ip] : kp;
         int rank = 0;
-        for (int j = 0; j < n; ++j) {
-            const uint32_t kj = ukey[j];
-            rank += member[j] & ((kj > ki) | ((kj == ki) & (j < i)));
+        for (int j = 0; j < U; ++j) {
+            const int ij = ulist[j];
+            uint32_t kj = 0u;
+            for (int b = 0; b < B; ++b) kj = key[b][ij] > kj ? key[b][ij] : kj;
+            rank += (kj > kp) | ((kj == kp) & (ij < ip));
         }
-        idx[rank] = i;
-        atomicAdd(&cnt[kMaxBatch], 1);
+        idx[rank] = ip;
     }
-    __syncthreads();
-    if (tid == 0) count[0] = cnt[kMaxBatch];
+    if (tid == 0) count[0] = U;
 }
 
 // ---- gate/up gather + gating --------------------------------------------------------------
@@ -158,7 +224,7 @@ __device__ inline int list_end(const int32_t* count, int end, int n_blk) {
     return end < c ? end : c;
 }
 
-template <ls_dtype T, ls_act A, int B>
+template <ls_dtype T, ls_act A, int B, bool RMS>
 __global__ __launch_bounds__(256) void gateup_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
@@ -187,9 +253,9 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     const u32x4* grow = reinterpret_cast<const u32x4*>(base + (size_t)q * row_bytes);
     const u32x4* urow = reinterpret_cast<const u32x4*>(base + (size_t)(blk + q) * row_bytes);
     const int nchunk = d / V;
-    float ag[B], au[B];
+    float ag[B], au[B], ss[B];  // h here is the layer input x; ss its sum of squares
 #pragma unroll
-    for (int i = 0; i < B; ++i) ag[i] = au[i] = 0.f;
+    for (int i = 0; i < B; ++i) ag[i] = au[i] = ss[i] = 0.f;
     for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
         u32x4 rg[U], ru[U];
 #pragma unroll
@@ -220,6 +286,12 @@ __global__ __launch_bounds__(256) void gateup_kernel(
                         au[i] = fmaf(wu[4 * qq + 1], x4.y, au[i]);
                         au[i] = fmaf(wu[4 * qq + 2], x4.z, au[i]);
                         au[i] = fmaf(wu[4 * qq + 3], x4.w, au[i]);
+                        if (RMS) {
+                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
+                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
+                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
+                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
+                        }
                     }
                 }
             }
@@ -228,8 +300,9 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-        const float g = wave_sum(ag[i]) + bj;
-        const float u = wave_sum(au[i]);
+        const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
+        const float g = sc * wave_sum(ag[i]) + bj;
+        const float u = sc * wave_sum(au[i]);
         float a;
         if (A == LS_ACT_REGLU) {
             a = fmaxf(g, 0.f) * u;  // exactly zero for g <= 0
@@ -326,42 +399,37 @@ __global__ __launch_bounds__(256) void down_kernel(
     }
 }
 
-// ---- dispatch helpers -----------------------------------------------------------------------
-template <template <ls_dtype, int> class K, ls_dtype T>
-struct ByBatch;
-
 }  // namespace
 
-hipError_t launch_prenorm(const Shape& s, const float* x, int B, float* h, hipStream_t st) {
-    hipLaunchKernelGGL(prenorm_kernel, dim3(B), dim3(256), 0, st, x, s.d, s.prenorm, h);
-    return hipGetLastError();
-}
 
-template <ls_dtype T>
+template <ls_dtype T, bool RMS>
 static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, const float* v, int B,
                          float* out, hipStream_t st) {
-    const dim3 grid((rows + 3) / 4), blk(256);
+    const dim3 grid(rows), blk(256);
     const uint8_t* w = static_cast<const uint8_t*>(W);
     switch (B) {
-        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G, int rpw,
-                            const float* v, int B, float* out, hipStream_t st) {
+                            const float* v, int B, bool rms, float* out, hipStream_t st) {
     switch (t) {
-        case LS_F32: return gemv_t<LS_F32>(W, rows, cols, G, rpw, v, B, out, st);
-        case LS_F16: return gemv_t<LS_F16>(W, rows, cols, G, rpw, v, B, out, st);
-        case LS_BF16: return gemv_t<LS_BF16>(W, rows, cols, G, rpw, v, B, out, st);
+        case LS_F32: return rms ? gemv_t<LS_F32, true>(W, rows, cols, G, rpw, v, B, out, st)
+                                : gemv_t<LS_F32, false>(W, rows, cols, G, rpw, v, B, out, st);
+        case LS_F16: return rms ? gemv_t<LS_F16, true>(W, rows, cols, G, rpw, v, B, out, st)
+                                : gemv_t<LS_F16, false>(W, rows, cols, G, rpw, v, B, out, st);
+        case LS_BF16: return rms ? gemv_t<LS_BF16, true>(W, rows, cols, G, rpw, v, B, out, st)
+                                 : gemv_t<LS_BF16, false>(W, rows, cols, G, rpw, v, B, out, st);
     }
     return hipErrorInvalidValue;
 }
@@ -418,8 +486,11 @@ hipError_t launch_fold_predictor(ls_dtype t, const void* P1, const void* P2, int
 
 hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st) {
-    int threads = ((n_blk + 63) / 64) * 64;
-    threads = threads < 64 ? 64 : (threads > 1024 ? 1024 : threads);
+    // one wave per token; more waves share the union ranking
+    int waves = (n_blk + 63) / 64;
+    waves = waves < B ? B : waves;
+    waves = waves > 16 ? 16 : waves;
+    const int threads = 64 * waves;
     hipLaunchKernelGGL(select_kernel, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
                        union_batch, cap, idx, count);
     return hipGetLastError();
@@ -434,9 +505,16 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
     const dim3 grid((unsigned)((tasks + 3) / 4)), blk(256);
     const size_t bb = s.block_elems * elem_size(s.dtype);
 #define LS_GU(NB)                                                                                 \
-    hipLaunchKernelGGL((gateup_kernel<T, A, NB>), grid, blk, 0, st, L.blocks, bb, slot_table,     \
-                       L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, \
-                       a_buf)
+    do {                                                                                          \
+        if (s.prenorm)                                                                            \
+            hipLaunchKernelGGL((gateup_kernel<T, A, NB, true>), grid, blk, 0, st, L.blocks, bb,   \
+                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx,  \
+                               count, begin, end, a_buf);                                         \
+        else                                                                                      \
+            hipLaunchKernelGGL((gateup_kernel<T, A, NB, false>), grid, blk, 0, st, L.blocks, bb,  \
+                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx,  \
+                               count, begin, end, a_buf);                                         \
+    } while (0)
     switch (B) {
         case 1: LS_GU(1); break;
         case 2: LS_GU(2); break;

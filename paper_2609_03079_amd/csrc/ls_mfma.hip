@@ -86,7 +86,9 @@ constexpr int kUnroll = 4;  // K steps in flight per wave
 
 // One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry); the 4 waves split
 // the d / 32 K steps.  a_buf[tok * F + e * blk + q] as the VALU kernel writes it.
-template <ls_dtype T, ls_act A>
+// x is the layer input; with RMS each lane also sums the squares of the x values it loads
+// (every (token, k) exactly once per workgroup) and the dot products are scaled at the end.
+template <ls_dtype T, ls_act A, bool RMS>
 __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int B, int d, int blk,
@@ -117,6 +119,7 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     const float* hrow = h + (size_t)(tok_ok ? tok : 0) * d;
     const int ksteps = d / 32;
     f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
+    float ss = 0.f;
     for (int k0 = wave; k0 < ksteps; k0 += kWaves * kUnroll) {
         u32x4 rg[kUnroll], ru[kUnroll];
         f32x4 hx[kUnroll][2];
@@ -135,6 +138,10 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
         for (int u = 0; u < kUnroll; ++u) {
             const float xv[8] = {hx[u][0].x, hx[u][0].y, hx[u][0].z, hx[u][0].w,
                                  hx[u][1].x, hx[u][1].y, hx[u][1].z, hx[u][1].w};
+            if (RMS) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) ss = fmaf(xv[i], xv[i], ss);
+            }
             typename S::vec hi, lo;
             S::run(xv, hi, lo);
             const typename S::vec wg = S::from_raw(rg[u]), wu = S::from_raw(ru[u]);
@@ -145,18 +152,24 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
         }
     }
     // lane l holds rows 4 (l / 16) + i, token l % 16 of this wave's partial sums
-    __shared__ float pg[kWaves][16][16], pu[kWaves][16][16];
+    __shared__ float pg[kWaves][16][16], pu[kWaves][16][16], pss[kWaves][16];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         pg[wave][4 * (lane >> 4) + i][lane & 15] = cg[i];
         pu[wave][4 * (lane >> 4) + i][lane & 15] = cu[i];
     }
+    if (RMS) {  // lanes l, l+16, l+32, l+48 hold the same token
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        if (lane < 16) pss[wave][lane] = ss;
+    }
     __syncthreads();
     if (threadIdx.x < 16 * B) {
         const int t = threadIdx.x / 16, r = threadIdx.x % 16;
-        const float g = ((pg[0][r][t] + pg[1][r][t]) + pg[2][r][t]) + pg[3][r][t] +
+        const float sc = RMS ? rms_scale(((pss[0][t] + pss[1][t]) + pss[2][t]) + pss[3][t], d) : 1.f;
+        const float g = sc * (((pg[0][r][t] + pg[1][r][t]) + pg[2][r][t]) + pg[3][r][t]) +
                         (bias ? Wt<T>::scalar(bias, (size_t)b * blk + r0 + r) : 0.f);
-        const float u = ((pu[0][r][t] + pu[1][r][t]) + pu[2][r][t]) + pu[3][r][t];
+        const float u = sc * (((pu[0][r][t] + pu[1][r][t]) + pu[2][r][t]) + pu[3][r][t]);
         float a;
         if (A == LS_ACT_REGLU) {
             a = fmaxf(g, 0.f) * u;
@@ -237,17 +250,24 @@ bool mfma_path(const Shape& s, int B) {
 }
 
 hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
-                              const float* h, int B, const int32_t* idx, const int32_t* count,
+                              const float* x, int B, const int32_t* idx, const int32_t* count,
                               int begin, int end, float* a_buf, hipStream_t st) {
     const long groups = (long)(end - begin) * (s.blk / 16);
     if (groups <= 0) return hipSuccess;
     const size_t bb = s.block_elems * elem_size(s.dtype);
     const dim3 grid((unsigned)groups), blk(256);
     const bool relu = s.act == LS_ACT_REGLU;
-#define LS_GUM(TT, AA)                                                                           \
-    hipLaunchKernelGGL((gateup_mfma_kernel<TT, AA>), grid, blk, 0, st, L.blocks, bb, slot_table, \
-                       L.bias, L.threshold, h, B, s.d, s.blk, s.n_blk, s.F, idx, count, begin,  \
-                       end, a_buf)
+#define LS_GUM(TT, AA)                                                                            \
+    do {                                                                                          \
+        if (s.prenorm)                                                                            \
+            hipLaunchKernelGGL((gateup_mfma_kernel<TT, AA, true>), grid, blk, 0, st, L.blocks, bb, \
+                               slot_table, L.bias, L.threshold, x, B, s.d, s.blk, s.n_blk, s.F,   \
+                               idx, count, begin, end, a_buf);                                    \
+        else                                                                                      \
+            hipLaunchKernelGGL((gateup_mfma_kernel<TT, AA, false>), grid, blk, 0, st, L.blocks,   \
+                               bb, slot_table, L.bias, L.threshold, x, B, s.d, s.blk, s.n_blk,    \
+                               s.F, idx, count, begin, end, a_buf);                               \
+    } while (0)
     if (s.dtype == LS_F16) {
         if (relu) LS_GUM(LS_F16, LS_ACT_REGLU);
         else LS_GUM(LS_F16, LS_ACT_SWIGLU_THRESH);

@@ -334,12 +334,22 @@ def test_full_size_layers_sampled(cfg_name):
         x_in, x_out = x_out, x_in
 
 
-@pytest.mark.parametrize("name", ["f16_b64", "bf16_swiglu"])
+# ReGLU shapes: with thresholded SiLU, two fp32-accurate paths may decide neurons within
+# rounding of the threshold differently (the oracle tests cover that with a guard band).
+MFMA_CMP = {
+    "f16_b64": SMALL["f16_b64"],
+    "bf16_reglu": C["mistral_7b_ffn"].with_(n_layers=1, d_model=512, d_ff=2048, block=128, rank=128,
+                                            keep_pct=50, act=lsgen.ACT_REGLU),
+}
+
+
+@pytest.mark.parametrize("name", list(MFMA_CMP))
 @pytest.mark.parametrize("B", [4, 8])
 def test_batch_matrix_core_path_matches_vector_path(name, B):
     """The matrix-core kernels (B >= 4) against the vector-ALU kernels on the same union list:
-    both accumulate in fp32, the activations enter the matrix cores as hi + lo 16-bit parts."""
-    cfg = SMALL[name]
+    both accumulate in fp32, the activations enter the matrix cores as hi + lo 16-bit parts
+    (about 22 significant bits for fp16 operands, 16 for bf16)."""
+    cfg = MFMA_CMP[name]
     f, ws = make_ffn(cfg, max_batch=B)
     xs = lsgen.tokens(cfg, 11, 1, B)[0]
     x_in = dev_f32(xs)
@@ -354,7 +364,7 @@ def test_batch_matrix_core_path_matches_vector_path(name, B):
         x_out = empty_f32(B, cfg.d_model)
         f.ls_sparse_ffn_step(0, x_in, B, idx, cnt, 0, cap, x_out)
         ys.append(host(x_out).astype(np.float64) - xs.astype(np.float64))
-    tol = 1e-5 if cfg.act == lsgen.ACT_REGLU else Y_TOL[cfg.dtype]
+    tol = 1e-5 if cfg.dtype == lsgen.DT_F16 else 1e-4
     for b in range(B):
         assert rel_l2(ys[0][b], ys[1][b]) <= tol, (name, B, b, rel_l2(ys[0][b], ys[1][b]))
     with pytest.raises(lsffn.LsError):
