@@ -98,8 +98,8 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
 // are compacted by ballot prefix, then ranked among themselves (key descending, index
 // ascending) so the output is in priority order.  Union: the OR of the tokens' sets, ranked
 // by each block's largest key over all tokens.
-constexpr int kSelQ = kMaxBlocks / 64;
-
+// Q: keys per lane (n <= 64 Q); small lists get a small unrolled body.
+template <int Q>
 __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ scores, int B,
                                                       int n, int mode, int k, float tau,
                                                       int union_batch, int cap,
@@ -109,6 +109,7 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
     __shared__ uint8_t memb[kMaxBatch][kMaxBlocks];
     __shared__ int16_t mlist[kMaxBatch][kMaxBlocks];
     __shared__ int16_t ulist[kMaxBlocks];
+    __shared__ uint32_t ukey[kMaxBlocks];  // union member p: largest key over all tokens
     __shared__ int ucount;
     const int tid = threadIdx.x, nt = blockDim.x;
     const int wave = tid >> 6, lane = tid & 63, nwaves = nt >> 6;
@@ -116,9 +117,9 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
     const uint64_t below = (1ull << lane) - 1ull;
     const int Qn = (n + 63) / 64;
     for (int b = wave; b < B; b += nwaves) {
-        uint32_t ok[kSelQ];
+        uint32_t ok[Q];
 #pragma unroll
-        for (int q = 0; q < kSelQ; ++q) {
+        for (int q = 0; q < Q; ++q) {
             const int i = q * 64 + lane;
             ok[q] = 0u;
             if (q < Qn && i < n) {
@@ -135,20 +136,20 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
                 const uint32_t c = T | (1u << bit);
                 int cnt = 0;
 #pragma unroll
-                for (int q = 0; q < kSelQ; ++q)
+                for (int q = 0; q < Q; ++q)
                     if (q < Qn) cnt += __popcll(__ballot(ok[q] >= c));
                 if (cnt >= k) T = c;
             }
             int gt = 0;
 #pragma unroll
-            for (int q = 0; q < kSelQ; ++q)
+            for (int q = 0; q < Q; ++q)
                 if (q < Qn) gt += __popcll(__ballot(ok[q] > T));
             rem = k - gt;
         }
         const uint32_t ktau = isnan(tau) ? 0xffffffffu : order_key(tau);
         int m = 0, eq_before = 0;
 #pragma unroll
-        for (int q = 0; q < kSelQ; ++q) {
+        for (int q = 0; q < Q; ++q) {
             if (q < Qn) {
                 const int i = q * 64 + lane;
                 const bool valid = i < n;
@@ -205,12 +206,16 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
         const int ip = ulist[p];
         uint32_t kp = 0u;
         for (int b = 0; b < B; ++b) kp = key[b][ip] > kp ? key[b][ip] : kp;
+        ukey[p] = kp;
+    }
+    __syncthreads();
+    for (int p = tid; p < U; p += nt) {
+        const int ip = ulist[p];
+        const uint32_t kp = ukey[p];
         int rank = 0;
         for (int j = 0; j < U; ++j) {
-            const int ij = ulist[j];
-            uint32_t kj = 0u;
-            for (int b = 0; b < B; ++b) kj = key[b][ij] > kj ? key[b][ij] : kj;
-            rank += (kj > kp) | ((kj == kp) & (ij < ip));
+            const uint32_t kj = ukey[j];
+            rank += (kj > kp) | ((kj == kp) & ((int)ulist[j] < ip));
         }
         idx[rank] = ip;
     }
@@ -491,7 +496,8 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
     waves = waves < B ? B : waves;
     waves = waves > 16 ? 16 : waves;
     const int threads = 64 * waves;
-    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
+    auto fn = n_blk <= 256 ? select_kernel<4> : n_blk <= 512 ? select_kernel<8> : select_kernel<kMaxBlocks / 64>;
+    hipLaunchKernelGGL(fn, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
                        union_batch, cap, idx, count);
     return hipGetLastError();
 }

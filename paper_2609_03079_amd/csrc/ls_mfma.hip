@@ -82,7 +82,7 @@ __device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
 }
 
 constexpr int kWaves = 4;
-constexpr int kUnroll = 4;  // K steps in flight per wave
+constexpr int kUnroll = 8;  // K steps in flight per wave
 
 // One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry); the 4 waves split
 // the d / 32 K steps.  a_buf[tok * F + e * blk + q] as the VALU kernel writes it.
@@ -199,35 +199,46 @@ __global__ __launch_bounds__(256) void down_mfma_kernel(
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
     f32x4v c = {0.f, 0.f, 0.f, 0.f};
-    for (int e = begin + wave; e < n_end; e += kWaves) {
-        const int b = idx[e];
-        const int slot = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
-        if (slot < 0) continue;  // contributes nothing
-        const u32x4* piece = reinterpret_cast<const u32x4*>(blocks + (size_t)slot * block_bytes + down_off);
-        const float* arow = a_buf + (size_t)(tok_ok ? tok : 0) * F + (size_t)e * blk;
-        for (int s0 = 0; s0 < ksteps; s0 += kUnroll) {
-            u32x4 w[kUnroll];
-            f32x4 av[kUnroll][2];
+    // work items (entry, K step) of the list range, dealt to the waves round-robin; kUnroll
+    // items per wave are in flight together
+    const long items = (long)(n_end - begin) * ksteps;
+    for (long i0 = wave; i0 < items; i0 += (long)kWaves * kUnroll) {
+        const u32x4* src[kUnroll];
+        const float* arow[kUnroll];
+        bool live[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int s = s0 + u;
-                const bool ok = s < ksteps;
-                w[u] = ok ? ld_stream(piece + 64 * s + lane) : u32x4{0u, 0u, 0u, 0u};
-                const int n0 = 32 * s + 8 * (lane >> 4);
-                const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-                av[u][0] = ok && tok_ok ? reinterpret_cast<const f32x4*>(arow + n0)[0] : z;
-                av[u][1] = ok && tok_ok ? reinterpret_cast<const f32x4*>(arow + n0)[1] : z;
+        for (int u = 0; u < kUnroll; ++u) {
+            const long it = i0 + (long)kWaves * u;
+            const int e = begin + (int)(it / ksteps), s = (int)(it % ksteps);
+            live[u] = it < items;
+            int slot = -1;
+            if (live[u]) {
+                const int b = idx[e];
+                slot = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
             }
+            live[u] = live[u] && slot >= 0;  // an invalid or absent block contributes nothing
+            src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
+                                                    down_off) + 64 * s + lane;
+            arow[u] = a_buf + (size_t)(tok_ok ? tok : 0) * F + (size_t)e * blk + 32 * s + 8 * (lane >> 4);
+        }
+        u32x4 w[kUnroll];
+        f32x4 av[kUnroll][2];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const float xv[8] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w,
-                                     av[u][1].x, av[u][1].y, av[u][1].z, av[u][1].w};
-                typename S::vec hi, lo;
-                S::run(xv, hi, lo);
-                const typename S::vec wv = S::from_raw(w[u]);
-                c = S::mfma(wv, hi, c);
-                c = S::mfma(wv, lo, c);
-            }
+        for (int u = 0; u < kUnroll; ++u) {
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+            w[u] = live[u] ? ld_stream(src[u]) : u32x4{0u, 0u, 0u, 0u};
+            av[u][0] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[0] : z;
+            av[u][1] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[1] : z;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const float xv[8] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w,
+                                 av[u][1].x, av[u][1].y, av[u][1].z, av[u][1].w};
+            typename S::vec hi, lo;
+            S::run(xv, hi, lo);
+            const typename S::vec wv = S::from_raw(w[u]);
+            c = S::mfma(wv, hi, c);
+            c = S::mfma(wv, lo, c);
         }
     }
     // lane l holds columns 4 (l / 16) + i of the tile for token l % 16
