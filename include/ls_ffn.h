@@ -216,11 +216,13 @@ ls_status ls_debug_decode_trace(ls_ffn* ctx, int32_t layer, float* x_in, float* 
 
 /* Debug: phase timestamps of the traced workgroup from the last fused
  * ls_decode_step, host int64 [n_layers][16] in wall-clock ticks (100 MHz):
- * 0 layer start, 1 input ready, 2 scores published, 3 all scores,
- * 4 keys barrier passed, 5 control wave ranked, 6 slot map,
- * 7 activations published, 8 all activations, 9 output published,
- * 10 miss gate/up done (worker), 11 down done (worker), 12 worker ranked,
- * 13 speculative gate/up done (worker), 14-15 unused (0).  Synchronises the stream.  *n receives n_layers * 16. */
+ * control wave: 0 layer start, 1 input gathered, 2 scores published,
+ * 3 all scores gathered, 4 list activations gathered, 5 exact top-k ready,
+ * 6 slot map, 7 misses done, 8 all down partials ready, 9 output published;
+ * first worker wave: 10 next layer's prefetch issued, 11 down partials done,
+ * 13 speculative gate/up done, 14 start after the input barrier; ranking wave:
+ * 12 next layer's list ranked; 15 unused (0).  Synchronises the stream.
+ * *n receives n_layers * 16. */
 ls_status ls_debug_phase_trace(ls_ffn* ctx, int64_t* host_out, int64_t cap, int64_t* n);
 
 /* Wait for all work enqueued on the context's stream and report a device-side

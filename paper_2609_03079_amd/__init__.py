@@ -31,9 +31,10 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
 LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA = range(5)
-PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "keys_barrier",
-          "ctrl_ranked", "slot_map", "acts_published", "all_acts", "output_published", "gateup_done",
-          "down_done", "worker_ranked", "early_gateup_done", "spare14", "spare15")
+PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_gathered",
+          "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",
+          "prefetch_issued", "partials_done", "next_list_ranked", "early_gateup_done",
+          "worker_start", "spare15")
 LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE = range(7)
 
 

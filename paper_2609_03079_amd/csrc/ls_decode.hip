@@ -30,8 +30,15 @@
 //   X   h_l = prenorm(x_l)                     (x_l from the previous layer)
 //   S   s_l = Pf_l h_l, s~_{l+1} = Pf_{l+1} h_l (block scores of this workgroup's rows)
 //   SEL E_l = topk(s_l, k); P_{l+1} = topk(s~_{l+1}, kp)  (every workgroup)
-//   GU  a_j for the neurons of E_l held in this workgroup's slots
-//   D   y over E_l for this workgroup's 16-column tile; x_{l+1} = x_l + y
+//   GU  activations of every neuron of the speculative list P_l held in this workgroup's
+//       slots (rows prefetched during layer l-1), published at their list positions
+//       while SEL runs; an E_l block missing from P_l borrows the slots of a list
+//       position outside E_l and is loaded and computed on demand
+//   D   this workgroup's 16-column tile of the down partial of every list position (and
+//       of every miss), from pieces staged in LDS; y = sum of the partials of E_l in E_l
+//       order; x_{l+1} = x_l + y
+// The weights of P_{l+1} (gate/up rows into registers, down pieces later into LDS) are
+// requested as soon as P_{l+1} is ranked.
 #include "ls_decode.h"
 #include "ls_device.h"
 
@@ -45,7 +52,7 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kWorkers = kWaves - 1;    // worker waves 1..3
 constexpr int kWL = kWorkers * 64;      // worker lanes
 constexpr int kSlots = 3;               // neuron slots per worker wave
-constexpr int kDnPos = 8;               // speculative list positions per worker wave
+constexpr int kDnPos = 9;               // down positions per worker wave
 constexpr int kDnPer = 2;               // 16-byte down chunks per lane per position
 constexpr int kMaxDn = kDnPos * kDnPer;
 constexpr int kMaxDnTot = kDnPos * kWorkers;  // down positions held per workgroup
@@ -130,7 +137,50 @@ __device__ __forceinline__ void wait_gather(Addr addr, int used, uint32_t tag, i
     }
 }
 
+// Same, for words base[off(u)] with a wave-uniform base and 32-bit offsets.
+template <int W, typename Off>
+__device__ __forceinline__ void wait_gather_off(const uint64_t* base, Off off, int used, uint32_t tag,
+                                                int lane, int* err, uint64_t (&v)[W]) {
+    uint32_t o[W];
+#pragma unroll
+    for (int u = 0; u < W; ++u) o[u] = off(u);
+    for (unsigned spins = 0;; ++spins) {
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            if (u < used) v[u] = mb_load(base + o[u]);
+        bool done = true;
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            if (u < used) done &= (uint32_t)(v[u] >> 32) == tag;
+        if (__all(done)) break;
+        if (spins > kSpinLimit) {
+            if (lane == 0) atomicOr(err, 1);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
 __device__ __forceinline__ float word_value(uint64_t w) { return __uint_as_float((uint32_t)w); }
+
+// Flags between the waves of one workgroup, in LDS: the writer's earlier LDS stores are
+// visible to a reader that saw the flag reach v.  Waits are bounded like the mailbox waits.
+__device__ __forceinline__ void flag_set(int* f, int v, int lane) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    if (lane == 0) __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void flag_wait(const int* f, int v, int lane, int* err) {
+    for (unsigned spins = 0; __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < v;
+         ++spins) {
+        if (spins > kSpinLimit) {
+            if (lane == 0) atomicOr(err, 2);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Keep a prefetched register in its storage type until this point: without it the compiler
 // may widen 16-bit weights to fp32 right after their load and hold twice the registers.
@@ -163,20 +213,26 @@ struct Smem {
     LayerPtrs lt[kMaxLayers];  // the layer table (LDS reads keep weight loads off the wait path)
     float hs[kMaxD];
     float xt[kColTile];
-    float sp[kWorkers][2 * kMaxSRows];  // per-wave partial scores (exact rows, then speculative)
     uint32_t key[2][kMaxNb];   // order keys of the exact and the speculative scores
     int E[kMaxKp];
     int Plist[2][kMaxKp];
     int hole_miss[kMaxKp];   // speculative position -> miss it recomputes, or -1
     int missE[kMaxKp];       // miss m -> E entry
-    int act_at[kMaxKp];      // E entry -> first activation word in the layer's mailbox row
-    int dn_entry[kMaxDnTot]; // down position -> E entry it serves, or -1
-    int dn_load[kMaxDnTot];  // 1: the down position's registers must be loaded for its entry
-    int needE[kMaxKp];
+    int row_of_e[kMaxKp];    // E entry -> list position whose partial row holds its partial
+    int hole_pos[kMaxKp];    // miss m -> the list position (hole) that computes it
+    int n_miss;
     int posE[kMaxNb];   // block -> position in E, or -1
     int posP[kMaxNb];   // block -> position in the current speculative list, or -1
-    float aall[kMaxA];  // activations of E in entry order
-    float dpart[kWL];
+    float aall[kMaxA];  // activations of the speculative list, in list order
+    // down partials for this tile: row p < kMaxDnTot of list position p, row kMaxDnTot + m of
+    // miss m
+    float dparts[kMaxDnTot + kMaxKp][kColTile];
+    // down pieces (this tile) of the list positions, staged from registers at the layer start
+    u32x4 dnl[kMaxDnTot][64 * kDnPer];
+    float amiss[kMaxKp][64];  // activations of the misses
+    // LDS flags (value = layer + 1 once set for that layer)
+    int f_keys, f_acts, f_E, f_pn;
+    int f_done[kWaves];
 };
 
 // Static shape of one launch, shared by both roles.
@@ -185,7 +241,6 @@ struct Geo {
     int SPW;  // folded predictor rows of this workgroup: rows w, w + G, ... below n_blk
     int CH;   // 16-byte chunks of one folded row (d / 4)
     int NPC;  // 16-byte chunks of one block's down piece for one column tile
-    int DN;   // down positions in use: min(kp, kMaxDnTot)
     int AW;   // activation words per layer: list positions, then misses
     int miss_base;
     bool has_tile;
@@ -234,24 +289,116 @@ __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int*
     }
 }
 
-// Exact top-k of layer l into E (wave 0) and, unless last, the speculative top-kp of layer
-// l+1 into Pn (wave 1).
-__device__ __forceinline__ void rank_all(Smem& sm, const Geo g, bool last, int* Pn, int wave,
-                                         int lane) {
-    if (wave == 0) top_set(sm.key[0], g.nb, g.k, sm.E, lane);
-    else if (wave == 1 && !last) top_set(sm.key[1], g.nb, g.kp, Pn, lane);
+// Control wave, misses: activations of up to two neurons (block b[u] >= 0, neuron q[u]) from
+// rows streamed straight from HBM (the control wave has no other weight loads in flight).
+template <ls_dtype T, ls_act A, int NC>
+__device__ __forceinline__ void ctl_gate_up(const Smem& sm, const Geo& g, int layer, size_t bb,
+                                            const int (&b)[2], const int (&q)[2], float (&a)[2],
+                                            int lane) {
+    constexpr int V = Wt<T>::V;
+    constexpr int KB = Wt<T>::kBytes;
+    const size_t row_bytes = (size_t)NC * V * 64 * KB;
+    u32x4 gw[2][NC], uw[2][NC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        if (b[u] >= 0) {
+            const uint8_t* base = sm.lt[layer].blocks + (size_t)b[u] * bb;
+            const uint8_t* gr = base + (size_t)q[u] * row_bytes;
+            const uint8_t* ur = base + (size_t)(g.blk + q[u]) * row_bytes;
+#pragma unroll
+            for (int j = 0; j < NC; ++j) {
+                gw[u][j] = gload_u(gr, (uint32_t)(lane + 64 * j) * 16u);
+                uw[u][j] = gload_u(ur, (uint32_t)(lane + 64 * j) * 16u);
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        a[u] = 0.f;
+        if (b[u] >= 0) {
+            float gs = 0.f, us = 0.f;
+#pragma unroll
+            for (int j = 0; j < NC; ++j) {
+                const float* hx = sm.hs + (lane + 64 * j) * V;
+                gs += dot_chunk<T>(gw[u][j], hx);
+                us += dot_chunk<T>(uw[u][j], hx);
+            }
+            const void* bias = sm.lt[layer].bias;
+            const float g0 = wave_sum_dpp(gs) + (bias ? Wt<T>::scalar(bias, (size_t)b[u] * g.blk + q[u]) : 0.f);
+            const float u0 = wave_sum_dpp(us);
+            if (A == LS_ACT_REGLU) {
+                a[u] = fmaxf(g0, 0.f) * u0;
+            } else {
+                const float sg = g0 / (1.f + expf(-g0));
+                a[u] = fabsf(sg) > sm.lt[layer].threshold ? sg * u0 : 0.f;
+            }
+        }
+    }
+}
+
+// Control wave, misses: this tile's down partial of misses 0..M-1 (rows kMaxDnTot + m of
+// dparts), eight at a time: their down pieces are requested first, then their activations
+// are gathered from every workgroup.
+template <ls_dtype T>
+__device__ __forceinline__ void ctl_miss_down(const FusedArgs& P, Smem& sm, const Geo& g, int l,
+                                              int M, int lane) {
+    constexpr int V = Wt<T>::V;
+    constexpr int KB = Wt<T>::kBytes;
+    const size_t down_off = 2 * (size_t)g.blk * P.d * KB + (size_t)g.w * g.blk * kColTile * KB;
+    for (int m0 = 0; m0 < M; m0 += 8) {
+        const int cnt = min(M - m0, 8);
+        u32x4 pc[8][kDnPer];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (u < cnt) {
+                const uint8_t* base = sm.lt[l].blocks + (size_t)sm.E[sm.missE[m0 + u]] * P.block_bytes + down_off;
+#pragma unroll
+                for (int i = 0; i < kDnPer; ++i)
+                    pc[u][i] = gload_u(base, (uint32_t)min(lane + 64 * i, g.NPC - 1) * 16u);
+            }
+        }
+        const int n = cnt * g.blk;
+        uint64_t v[8];
+        wait_words<8>(P.amb + (size_t)l * g.AW + g.miss_base + m0 * g.blk, n, g.tag, lane, P.err, v);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int f = u * 64 + lane;
+            if (f < n) sm.amiss[m0 + f / g.blk][f % g.blk] = word_value(v[u]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (u < cnt) {
+                float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i = 0; i < kDnPer; ++i) {
+                    const int cc = lane + 64 * i;
+                    if (cc < g.NPC) {
+                        float wv[V];
+                        Wt<T>::widen(pc[u][i], wv);
+                        const float* ap = sm.amiss[m0 + u] + (cc / kColTile) * V;
+#pragma unroll
+                        for (int e = 0; e < V; ++e) acc[e & 3] = fmaf(ap[e], wv[e], acc[e & 3]);
+                    }
+                }
+                float t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+                t += __shfl_xor(t, 16, 64);
+                t += __shfl_xor(t, 32, 64);
+                if (lane < kColTile) sm.dparts[kMaxDnTot + m0 + u][lane] = t;
+            }
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------------------
 // Control wave: waits, publications, the slot map.
-template <ls_dtype T, int NC>
+template <ls_dtype T, ls_act A, int NC>
 __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const Geo g, int lane) {
     constexpr int V = Wt<T>::V;
     constexpr int D = NC * V * 64;
     for (int l = 0; l < g.L; ++l) {
         const bool last = l == g.L - 1;
-        int* Pc = sm.Plist[l & 1];
-        int* Pn = sm.Plist[(l + 1) & 1];
+        const int* Pc = sm.Plist[l & 1];
         LS_STAMP(P, g, l, 0, lane == 0);
         // X: the layer input (layer 0's was tagged into the mailbox before the launch), the
         // RMS scale from the values in registers, h into LDS, this tile's raw x into xt.
@@ -273,18 +420,37 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         }
         LS_STAMP(P, g, l, 1, lane == 0);
         lds_barrier();  // 1: h ready (and the folded rows of layers l, l+1 staged)
-        lds_barrier();  // 2: partial scores ready
-        if (lane < 2 * g.SPW) {
-            const int set = lane / g.SPW, m = lane % g.SPW;
-            if (set == 0 || !last) {
-                float sc = 0.f;
+        // S: this workgroup's scores, exact (layer l) and speculative (layer l+1), as dot
+        // products of the staged folded rows with h (lane-strided chunks, then DPP)
+        {
+            const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.hs);
 #pragma unroll
-                for (int v = 0; v < kWorkers; ++v) sc += sm.sp[v][set * kMaxSRows + m];
-                mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, sc);
+            for (int set = 0; set < 2; ++set) {
+#pragma unroll
+                for (int m = 0; m < kMaxSRows; ++m) {
+                    if (m < g.SPW && (set == 0 || !last)) {
+                        const f32x4* row = sm.pfs[(l + set) & 1][m];
+                        float a[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int i = 0; i < kMaxD / 4 / 64; ++i) {
+                            const int c = lane + 64 * i;
+                            if (c < g.CH) {
+                                const f32x4 pv = row[c], hv = h4[c];
+                                a[i & 3] = fmaf(pv.x, hv.x, a[i & 3]);
+                                a[i & 3] = fmaf(pv.y, hv.y, a[i & 3]);
+                                a[i & 3] = fmaf(pv.z, hv.z, a[i & 3]);
+                                a[i & 3] = fmaf(pv.w, hv.w, a[i & 3]);
+                            }
+                        }
+                        const float sc = wave_sum_dpp((a[0] + a[1]) + (a[2] + a[3]));
+                        if (lane == 0)
+                            mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, sc);
+                    }
+                }
             }
         }
         LS_STAMP(P, g, l, 2, lane == 0);
-        // SEL: order keys of every block's score (exact, then speculative)
+        // order keys of every block's score (exact, then speculative); waves 2 and 3 rank them
         {
             const int n = last ? g.nb : 2 * g.nb;
             uint64_t v[2 * kMaxNb / 64];
@@ -298,18 +464,34 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                 }
             }
         }
+        flag_set(&sm.f_keys, l + 1, lane);
         LS_STAMP(P, g, l, 3, lane == 0);
-        lds_barrier();  // 3: keys ready
+        // the list's activations (published by every workgroup's early gate/up), gathered
+        // before the workers start streaming the next layer's weights
+        if (l > 0 && g.has_tile) {
+            const int n = g.kp * g.blk;
+            const uint64_t* row = P.amb + (size_t)l * g.AW;
+            for (int base = 0; base < n; base += 16 * 64) {
+                uint64_t v[16];
+                wait_words<16>(row + base, min(n - base, 16 * 64), g.tag, lane, P.err, v);
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int i = base + u * 64 + lane;
+                    if (i < n) sm.aall[i] = word_value(v[u]);
+                }
+            }
+        }
+        flag_set(&sm.f_acts, l + 1, lane);
         LS_STAMP(P, g, l, 4, lane == 0);
-        rank_all(sm, g, last, Pn, 0, lane);
+        flag_wait(&sm.f_E, l + 1, lane, P.err);  // E = exact top-k (wave 2)
         LS_STAMP(P, g, l, 5, lane == 0);
-        lds_barrier();  // 4: E and the speculative list ready
-        // Slot maps.  Activations: an E block found in the speculative list Pc was computed
-        // at its list position (early, before the selection); the others ("misses") are
-        // recomputed by the slots of holes (list positions whose block is not in E) and
-        // published after the list, at word miss_base + m * blk.  Down pieces: positions
-        // [0, DN) hold the prefetched pieces of Pc[0, DN); E blocks not among them are
-        // loaded into the holes of that range.
+        // Maps.  An E block at list position p has its activations and its down partial
+        // computed at p from the speculatively prefetched rows.  An E block missing from the
+        // list is miss m: hole m (the m-th list position whose block is not in E) lends its
+        // neuron slots, whose control waves recompute the activations and publish them after
+        // the list (word miss_base + m * blk); every workgroup's control wave computes its
+        // tile's down partial of the miss.  row_of_e: the partial row of E entry e.
+        int M = 0;
         {
             const bool spec = l > 0;
             for (int b = lane; b < g.nb; b += 64) {
@@ -324,69 +506,61 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             const int pp = lane < g.k ? sm.posP[sm.E[lane]] : -1;  // -1 when !spec
             const bool miss = lane < g.k && pp < 0;
             const uint64_t mm = __ballot(miss);
-            const int M = __popcll(mm), mr = __popcll(mm & below);
+            M = __popcll(mm);
+            const int mr = __popcll(mm & below);
             if (miss) sm.missE[mr] = lane;
-            if (lane < g.k) sm.act_at[lane] = miss ? g.miss_base + mr * g.blk : pp * g.blk;
+            if (lane < g.k) sm.row_of_e[lane] = miss ? kMaxDnTot + mr : pp;
             const int pe = spec && lane < g.kp ? sm.posE[Pc[lane]] : -1;
             const bool hole = lane < g.kp && pe < 0;
             const uint64_t hm = __ballot(hole);
             const int hr = __popcll(hm & below);
             sm.hole_miss[lane] = hole && hr < M ? hr : -1;
-            // down positions
-            const bool need = lane < g.k && (miss || pp >= g.DN);
-            const uint64_t nm = __ballot(need);
-            if (need) sm.needE[__popcll(nm & below)] = lane;
-            const bool dhole = lane < g.DN && pe < 0;
-            const uint64_t dm = __ballot(dhole);
-            const int dr = __popcll(dm & below);
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
-            if (lane < kMaxDnTot) {
-                int de = -1, dl = 0;
-                if (lane < g.DN) {
-                    if (!dhole) de = pe;
-                    else if (dr < __popcll(nm)) {
-                        de = sm.needE[dr];
-                        dl = 1;
-                    }
-                }
-                sm.dn_entry[lane] = de;
-                sm.dn_load[lane] = dl;
-            }
         }
         LS_STAMP(P, g, l, 6, lane == 0);
-        lds_barrier();  // 5: slot maps ready
-        // activations of E, gathered from the words of every workgroup
-        {
-            const int n = g.k * g.blk;
-            const uint64_t* row = P.amb + (size_t)l * g.AW;
-            for (int base = 0; base < n; base += 16 * 64) {
-                uint64_t v[16];
-                const int* at = sm.act_at;
-                const int blk = g.blk;
-                wait_gather<16>(
-                    [&](int u) {
-                        const int f = min(base + u * 64 + lane, n - 1);
-                        return row + at[f / blk] + f % blk;
-                    },
-                    (n - base + 63) / 64, g.tag, lane, P.err, v);
+        if (M > 0) {
+            // activations of the misses' neurons held by this workgroup's hole slots
+            for (int i0 = 0; i0 < kWorkers * kSlots; i0 += 2) {
+                int bb2[2], qq2[2], mm2[2];
 #pragma unroll
-                for (int u = 0; u < 16; ++u) {
-                    const int i = base + u * 64 + lane;
-                    if (i < n) sm.aall[i] = word_value(v[u]);
+                for (int u = 0; u < 2; ++u) {
+                    const int t = g.w + g.G * (i0 + u);
+                    const int m = (i0 + u < kWorkers * kSlots && t < g.kp * g.blk) ? sm.hole_miss[t / g.blk] : -1;
+                    mm2[u] = m;
+                    bb2[u] = m >= 0 ? sm.E[sm.missE[m]] : -1;
+                    qq2[u] = t % g.blk;
                 }
+                float a2[2];
+                ctl_gate_up<T, A, NC>(sm, g, l, P.block_bytes, bb2, qq2, a2, lane);
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    if (mm2[u] >= 0 && lane == 0)
+                        mb_store(P.amb + (size_t)l * g.AW + g.miss_base + mm2[u] * g.blk + qq2[u], g.tag, a2[u]);
+            }
+            // this tile's down partial of every miss
+            if (g.has_tile) ctl_miss_down<T>(P, sm, g, l, M, lane);
+        }
+        LS_STAMP(P, g, l, 7, lane == 0);
+        // every worker's down partials of the list positions
+#pragma unroll
+        for (int v = 1; v < kWaves; ++v) flag_wait(&sm.f_done[v], l + 1, lane, P.err);
+        LS_STAMP(P, g, l, 8, lane == 0);
+        if (g.has_tile) {
+            // y = sum over E of the entries' partial rows: lane = column + 16 * quarter; each
+            // quarter sums its entries in E order, then the quarters in a fixed order
+            const int col = lane & (kColTile - 1), qtr = lane >> 4;
+            float y = 0.f;
+#pragma unroll 4
+            for (int e = qtr; e < g.k; e += 4) y += sm.dparts[sm.row_of_e[e]][col];
+            y += __shfl_xor(y, 16, 64);
+            y += __shfl_xor(y, 32, 64);
+            const float xn = sm.xt[col] + y;
+            if (lane < kColTile) {
+                if (last) P.x[g.w * kColTile + lane] = xn;
+                else mb_store(P.xmb + (size_t)(l + 1) * D + g.w * kColTile + lane, g.tag, xn);
             }
         }
-        LS_STAMP(P, g, l, 8, lane == 0);
-        lds_barrier();  // 6: activations of every workgroup ready
-        lds_barrier();  // 7: down partials ready
         LS_STAMP(P, g, l, 9, lane == 0);
-        if (g.has_tile && lane < kColTile) {
-            float y = 0.f;
-            for (int i = 0; i < kWL / kColTile; ++i) y += sm.dpart[lane + kColTile * i];
-            const float xn = sm.xt[lane] + y;
-            if (last) P.x[g.w * kColTile + lane] = xn;
-            else mb_store(P.xmb + (size_t)(l + 1) * D + g.w * kColTile + lane, g.tag, xn);
-        }
     }
 }
 
@@ -415,17 +589,15 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
 #pragma unroll
     for (int j = 0; j < kMaxDn; ++j) dn[j] = zero4;
 
+    // every load is issued (clamped to valid addresses) so that later waits count exactly
     auto load_pf = [&](int layer) {
 #pragma unroll
         for (int m = 0; m < kMaxSRows; ++m) {
-            if (m < g.SPW) {
-                const float* row = sm.lt[layer].pf + (size_t)(g.w + g.G * m) * D;
+            const int r = m < g.SPW ? g.w + g.G * m : 0;
+            const float* row = sm.lt[layer].pf + (size_t)r * D;
 #pragma unroll
-                for (int j = 0; j < kPfPer; ++j) {
-                    const int c = wl + kWL * j;
-                    if (c < g.CH) pfr[m * kPfPer + j] = gload_u(row, (uint32_t)c * 16u);
-                }
-            }
+            for (int j = 0; j < kPfPer; ++j)
+                pfr[m * kPfPer + j] = gload_u(row, (uint32_t)min(wl + kWL * j, g.CH - 1) * 16u);
         }
     };
     auto stash_pf = [&](int layer) {  // pfr -> LDS buffer of `layer`
@@ -464,7 +636,7 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         const uint8_t* base = sm.lt[layer].blocks + (size_t)b * bb + down_off;
 #pragma unroll
         for (int i = 0; i < kDnPer; ++i)
-            if (lane + 64 * i < g.NPC) dn[jp * kDnPer + i] = gload_u(base, (uint32_t)(lane + 64 * i) * 16u);
+            dn[jp * kDnPer + i] = gload_u(base, (uint32_t)min(lane + 64 * i, g.NPC - 1) * 16u);
     };
 
     // activations of the slots in `use` (wave-uniform bit mask) from their rows in gg/uu:
@@ -526,6 +698,28 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         }
     };
 
+    // this tile's down partial of the block whose piece sits in register position jp, with
+    // its activations at act[0..blk): lanes l, l+16, l+32, l+48 share a column; the column
+    // sums end in lanes 0..15
+    auto down_partial = [&](int p, const float* act) -> float {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < kDnPer; ++i) {
+            const int cc = lane + 64 * i;
+            if (cc < g.NPC) {
+                float wv[V];
+                Wt<T>::widen(sm.dnl[p][cc], wv);
+                const float* ap = act + (cc / kColTile) * V;
+#pragma unroll
+                for (int v = 0; v < V; ++v) acc[v & 3] = fmaf(ap[v], wv[v], acc[v & 3]);
+            }
+        }
+        float t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+        t += __shfl_xor(t, 16, 64);
+        t += __shfl_xor(t, 32, 64);
+        return t;
+    };
+
     int slot_t[kSlots];  // global slot index of each of this wave's slots
 #pragma unroll
     for (int sl = 0; sl < kSlots; ++sl) slot_t[sl] = g.w + g.G * ((wave - 1) + kWorkers * sl);
@@ -546,42 +740,18 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         } else if (!last) {
             stash_pf(l + 1);
         }
-        lds_barrier();  // 1: h ready
-        // S partials: exact rows (layer l) and speculative rows (layer l+1) against h
-        {
-            float acc[2 * kMaxSRows];
+        // this layer's down pieces (prefetched during the previous layer) into LDS
+        if (l > 0 && g.has_tile) {
 #pragma unroll
-            for (int m2 = 0; m2 < 2 * kMaxSRows; ++m2) acc[m2] = 0.f;
-            const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.hs);
+            for (int jp = 0; jp < kDnPos; ++jp) {
+                const int p = (wave - 1) + kWorkers * jp;
+                if (p < g.kp) {
 #pragma unroll
-            for (int j = 0; j < kPfPer; ++j) {
-                const int c = wl + kWL * j;
-                if (c < g.CH) {
-                    const f32x4 hv = h4[c];
-#pragma unroll
-                    for (int set = 0; set < 2; ++set) {
-#pragma unroll
-                        for (int m = 0; m < kMaxSRows; ++m) {
-                            if (m < g.SPW && (set == 0 || !last)) {
-                                const f32x4 pv = sm.pfs[(l + set) & 1][m][c];
-                                float a = acc[set * kMaxSRows + m];
-                                a = fmaf(pv.x, hv.x, a);
-                                a = fmaf(pv.y, hv.y, a);
-                                a = fmaf(pv.z, hv.z, a);
-                                a = fmaf(pv.w, hv.w, a);
-                                acc[set * kMaxSRows + m] = a;
-                            }
-                        }
-                    }
+                    for (int i = 0; i < kDnPer; ++i) sm.dnl[p][lane + 64 * i] = pin(dn[jp * kDnPer + i]);
                 }
             }
-#pragma unroll
-            for (int m2 = 0; m2 < 2 * kMaxSRows; ++m2) {
-                const float t = wave_sum_dpp(acc[m2]);
-                if (lane == 0) sm.sp[wave - 1][m2] = t;
-            }
         }
-        lds_barrier();  // 2: partial scores ready
+        lds_barrier();  // 1: h ready
         // early GU: every speculative position held in this wave's slots (prefetched during
         // the previous layer), published at its list position while the selection runs
         if (l > 0) {
@@ -602,90 +772,52 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
                 if ((use & (1u << sl)) && lane == 0) mb_store(P.amb + (size_t)l * g.AW + slot_t[sl], g.tag, as[sl]);
         }
         LS_STAMP(P, g, l, 13, wave == 1 && lane == 0);
-        // folded rows of layer l+2 (after the early GU: its waits must not cover these loads)
-        if (l + 2 < g.L) load_pf(l + 2);
-        lds_barrier();  // 3: keys ready
-        rank_all(sm, g, last, const_cast<int*>(Pn), wave, lane);
-        LS_STAMP(P, g, l, 12, wave == 1 && lane == 0);
-        lds_barrier();  // 4
-        lds_barrier();  // 5: slot maps ready
-        // down pieces of E blocks that are not among the prefetched positions
-        if (g.has_tile) {
+        // the selection: wave 2 the exact top-k of this layer, wave 3 the next layer's list
+        if (wave == 2) {
+            flag_wait(&sm.f_keys, l + 1, lane, P.err);
+            top_set(sm.key[0], g.nb, g.k, sm.E, lane);
+            flag_set(&sm.f_E, l + 1, lane);
+        } else if (wave == 3) {
+            flag_wait(&sm.f_keys, l + 1, lane, P.err);
+            if (!last) top_set(sm.key[1], g.nb, g.kp, const_cast<int*>(Pn), lane);
+            flag_set(&sm.f_pn, l + 1, lane);
+            LS_STAMP(P, g, l, 12, lane == 0);
+        }
+        // gate/up rows of the next layer's speculative list (issued by every slot; the last
+        // layer re-reads rows of its own so that the count stays fixed)
+        flag_wait(&sm.f_pn, l + 1, lane, P.err);
+        {
+            const int nl = last ? l : l + 1;
+#pragma unroll
+            for (int sl = 0; sl < kSlots; ++sl) {
+                const int t = slot_t[sl];
+                const bool used = !last && t < g.kp * g.blk;
+                load_gu(sl, nl, used ? Pn[t / g.blk] : 0, used ? t % g.blk : 0);
+            }
+            // and their down pieces for this workgroup's tile
 #pragma unroll
             for (int jp = 0; jp < kDnPos; ++jp) {
                 const int p = (wave - 1) + kWorkers * jp;
-                if (p < g.DN && sm.dn_load[p]) load_down_pos(l, sm.E[sm.dn_entry[p]], jp);
-            }
-        }
-        LS_STAMP(P, g, l, 15, wave == 1 && lane == 0);
-        // misses: the slots of a hole recompute one E block that the list missed
-        {
-            unsigned use = 0;
-            int bs[kSlots], qs[kSlots], ms[kSlots];
-            float as[kSlots];
-#pragma unroll
-            for (int sl = 0; sl < kSlots; ++sl) {
-                const int t = slot_t[sl];
-                ms[sl] = t < g.kp * g.blk ? sm.hole_miss[t / g.blk] : -1;
-                bs[sl] = ms[sl] >= 0 ? sm.E[sm.missE[ms[sl]]] : 0;
-                qs[sl] = t % g.blk;
-                if (ms[sl] >= 0) {
-                    use |= 1u << sl;
-                    load_gu(sl, l, bs[sl], qs[sl]);
-                }
-            }
-            if (use) {
-                gate_up(l, use, bs, qs, as);
-#pragma unroll
-                for (int sl = 0; sl < kSlots; ++sl)
-                    if ((use & (1u << sl)) && lane == 0)
-                        mb_store(P.amb + (size_t)l * g.AW + g.miss_base + ms[sl] * g.blk + qs[sl], g.tag, as[sl]);
-            }
-        }
-        // gate/up rows of the next layer's speculative list (known since the selection)
-        if (!last) {
-#pragma unroll
-            for (int sl = 0; sl < kSlots; ++sl) {
-                const int t = slot_t[sl];
-                if (t < g.kp * g.blk) load_gu(sl, l + 1, Pn[t / g.blk], t % g.blk);
+                load_down_pos(nl, (!last && p < g.kp) ? Pn[p] : 0, jp);
             }
         }
         LS_STAMP(P, g, l, 10, wave == 1 && lane == 0);
-        lds_barrier();  // 6: activations of every workgroup ready
-        if (g.has_tile) {
-            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        // down partials of every list position, from the pieces prefetched one layer ago
+        flag_wait(&sm.f_acts, l + 1, lane, P.err);
+        if (l > 0 && g.has_tile) {
 #pragma unroll
             for (int jp = 0; jp < kDnPos; ++jp) {
                 const int p = (wave - 1) + kWorkers * jp;
-                const int e = p < g.DN ? sm.dn_entry[p] : -1;
-                if (e >= 0) {
-#pragma unroll
-                    for (int i = 0; i < kDnPer; ++i) {
-                        const int cc = lane + 64 * i;
-                        if (cc < g.NPC) {
-                            float wv[V];
-                            Wt<T>::widen(pin(dn[jp * kDnPer + i]), wv);
-                            const float* ap = sm.aall + e * g.blk + (cc / kColTile) * V;
-#pragma unroll
-                            for (int v = 0; v < V; ++v) acc[v & 3] = fmaf(ap[v], wv[v], acc[v & 3]);
-                        }
-                    }
+                if (p < g.kp) {
+                    const float part = down_partial(p, sm.aall + p * g.blk);
+                    if (lane < kColTile) sm.dparts[p][lane] = part;
                 }
             }
-            sm.dpart[wl] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
         }
+        flag_set(&sm.f_done[wave], l + 1, lane);
         LS_STAMP(P, g, l, 11, wave == 1 && lane == 0);
-        lds_barrier();  // 7
-        // down pieces of the next layer's speculative list
-        if (!last) {
-            if (g.has_tile) {
-#pragma unroll
-                for (int jp = 0; jp < kDnPos; ++jp) {
-                    const int p = (wave - 1) + kWorkers * jp;
-                    if (p < g.DN) load_down_pos(l + 1, Pn[p], jp);
-                }
-            }
-        }
+        // folded rows of layer l+2
+        load_pf(min(l + 2, g.L - 1));
     }
 }
 
@@ -707,7 +839,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
     g.F = P.F;
     g.SPW = g.w < g.nb ? (g.nb - 1 - g.w) / g.G + 1 : 0;
     g.CH = D / 4;
-    g.DN = min(g.kp, kMaxDnTot);
     g.miss_base = g.kp * g.blk;
     g.AW = (g.kp + g.k) * g.blk;
     g.NPC = g.blk * KB;
@@ -718,9 +849,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
         uint32_t* dst = reinterpret_cast<uint32_t*>(sm.lt);
         const int words = P.L * (int)(sizeof(LayerPtrs) / 4);
         for (int i = threadIdx.x; i < words; i += kThreads) dst[i] = src[i];
+        if (threadIdx.x == 0) {
+            sm.f_keys = sm.f_acts = sm.f_E = sm.f_pn = 0;
+            for (int v = 0; v < kWaves; ++v) sm.f_done[v] = 0;
+        }
         __syncthreads();
     }
-    if (wave == 0) control_loop<T, NC>(P, sm, g, lane);
+    if (wave == 0) control_loop<T, A, NC>(P, sm, g, lane);
     else worker_loop<T, A, NC>(P, sm, g, wave, lane);
 }
 
@@ -771,14 +906,14 @@ FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int
     if (s.n_blk > kMaxNb) return {false, "n_blk"};
     if (k < 1 || kp < k || kp > kMaxKp || kp > s.n_blk) return {false, "k / speculative width"};
     if ((long)kp * s.blk > (long)kWorkers * kSlots * n_wg) return {false, "neuron slots"};
-    if (s.blk * KB > 64 * kDnPer || k > kMaxDnTot) return {false, "down chunks"};
+    if (s.blk * KB > 64 * kDnPer || kp > kMaxDnTot) return {false, "down chunks"};
     if ((long)k * s.blk > kMaxA) return {false, "k * block"};
     return {true, ""};
 }
 
 int fused_max_spec(const Shape& s, int n_wg) {
     const long by_slots = (long)kWorkers * kSlots * n_wg / s.blk;
-    const long m = std::min<long>(by_slots, kMaxKp);
+    const long m = std::min<long>(std::min<long>(by_slots, kMaxKp), kMaxDnTot);
     return (int)std::min<long>(m, s.n_blk);
 }
 
