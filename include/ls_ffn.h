@@ -219,9 +219,10 @@ ls_status ls_debug_decode_trace(ls_ffn* ctx, int32_t layer, float* x_in, float* 
  * control wave: 0 layer start, 1 input gathered, 2 scores published,
  * 3 all scores gathered, 4 list activations gathered, 5 exact top-k ready,
  * 6 slot map, 7 misses done, 8 all down partials ready, 9 output published;
- * first worker wave: 10 next layer's prefetch issued, 11 down partials done,
- * 13 speculative gate/up done, 14 start after the input barrier; ranking wave:
- * 12 next layer's list ranked; 15 unused (0).  Synchronises the stream.
+ * last worker wave (it also ranks the next layer's list): 14 past the input
+ * barrier, 13 speculative gate/up done, 12 next layer's list ranked, 15 list
+ * activations seen, 11 down partials done, 10 next layer's loads issued.
+ * Synchronises the stream.
  * *n receives n_layers * 16. */
 ls_status ls_debug_phase_trace(ls_ffn* ctx, int64_t* host_out, int64_t cap, int64_t* n);
 

@@ -34,7 +34,7 @@ LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_
 PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_gathered",
           "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",
           "prefetch_issued", "partials_done", "next_list_ranked", "early_gateup_done",
-          "worker_start", "spare15")
+          "worker_start", "worker_acts_seen")
 LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE = range(7)
 
 

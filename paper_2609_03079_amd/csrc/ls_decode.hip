@@ -43,6 +43,7 @@
 #include "ls_device.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace ls {
 namespace {
@@ -59,7 +60,7 @@ constexpr int kMaxDnTot = kDnPos * kWorkers;  // down positions held per workgro
 constexpr int kMaxD = 4096;
 constexpr int kMaxNb = 256;
 constexpr int kMaxKp = 64;
-constexpr int kMaxA = 4096;             // k * block
+constexpr int kMaxA = 4096;             // speculative width * block
 constexpr int kMaxSRows = 1;            // folded predictor rows (block scores) per workgroup
 constexpr int kPfPer = (kMaxD / 4 + kWL - 1) / kWL;  // 16-byte chunks of one row per worker lane
 constexpr int kMaxLayers = 128;
@@ -211,7 +212,8 @@ __device__ __forceinline__ float dot_chunk(const u32x4& raw_in, const float* x) 
 struct Smem {
     f32x4 pfs[2][kMaxSRows][kMaxD / 4];  // this workgroup's folded predictor rows, two layers
     LayerPtrs lt[kMaxLayers];  // the layer table (LDS reads keep weight loads off the wait path)
-    float hs[kMaxD];
+    float xin[kMaxD];         // the layer input as gathered (the RMS scale is applied later)
+    float ssp[2][kWaves];     // per-wave sums of squares of xin (by layer parity)
     float xt[kColTile];
     uint32_t key[2][kMaxNb];   // order keys of the exact and the speculative scores
     int E[kMaxKp];
@@ -223,13 +225,13 @@ struct Smem {
     int n_miss;
     int posE[kMaxNb];   // block -> position in E, or -1
     int posP[kMaxNb];   // block -> position in the current speculative list, or -1
-    float aall[kMaxA];  // activations of the speculative list, in list order
+    alignas(16) float aall[kMaxA];  // activations of the speculative list, in list order
     // down partials for this tile: row p < kMaxDnTot of list position p, row kMaxDnTot + m of
     // miss m
-    float dparts[kMaxDnTot + kMaxKp][kColTile];
+    alignas(16) float dparts[kMaxDnTot + kMaxKp][kColTile];
     // down pieces (this tile) of the list positions, staged from registers at the layer start
     u32x4 dnl[kMaxDnTot][64 * kDnPer];
-    float amiss[kMaxKp][64];  // activations of the misses
+    alignas(16) float amiss[kMaxKp][64];  // activations of the misses
     // LDS flags (value = layer + 1 once set for that layer)
     int f_keys, f_acts, f_E, f_pn;
     int f_done[kWaves];
@@ -289,10 +291,39 @@ __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int*
     }
 }
 
+// X, one quarter per wave: words [wave*D/4, (wave+1)*D/4) of the layer input into xin (and
+// this workgroup's tile into xt), and the quarter's sum of squares into ssp.
+template <int D>
+__device__ __forceinline__ void gather_input(const FusedArgs& P, Smem& sm, const Geo& g, int l, int wave,
+                                             int lane) {
+    constexpr int Q = D / kWaves;
+    constexpr int W = Q / 64;
+    uint64_t v[W];
+    wait_words<W>(P.xmb + (size_t)l * D + wave * Q, Q, g.tag, lane, P.err, v);
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < W; ++u) {
+        const int i = wave * Q + u * 64 + lane;
+        const float x = word_value(v[u]);
+        ss = fmaf(x, x, ss);
+        sm.xin[i] = x;
+        if (g.has_tile && (i >> 4) == g.w) sm.xt[i & (kColTile - 1)] = x;
+    }
+    ss = wave_sum_dpp(ss);
+    if (lane == 0) sm.ssp[l & 1][wave] = ss;
+}
+
+// RMS scale of the gathered input (every wave, after the input barrier; fixed order)
+template <int D>
+__device__ __forceinline__ float input_scale(const FusedArgs& P, const Smem& sm, int l) {
+    const float* q = sm.ssp[l & 1];
+    return P.prenorm ? rms_scale((q[0] + q[1]) + (q[2] + q[3]), D) : 1.f;
+}
+
 // Control wave, misses: activations of up to two neurons (block b[u] >= 0, neuron q[u]) from
 // rows streamed straight from HBM (the control wave has no other weight loads in flight).
 template <ls_dtype T, ls_act A, int NC>
-__device__ __forceinline__ void ctl_gate_up(const Smem& sm, const Geo& g, int layer, size_t bb,
+__device__ __forceinline__ void ctl_gate_up(const Smem& sm, const Geo& g, int layer, size_t bb, float sc,
                                             const int (&b)[2], const int (&q)[2], float (&a)[2],
                                             int lane) {
     constexpr int V = Wt<T>::V;
@@ -319,13 +350,13 @@ __device__ __forceinline__ void ctl_gate_up(const Smem& sm, const Geo& g, int la
             float gs = 0.f, us = 0.f;
 #pragma unroll
             for (int j = 0; j < NC; ++j) {
-                const float* hx = sm.hs + (lane + 64 * j) * V;
+                const float* hx = sm.xin + (lane + 64 * j) * V;
                 gs += dot_chunk<T>(gw[u][j], hx);
                 us += dot_chunk<T>(uw[u][j], hx);
             }
             const void* bias = sm.lt[layer].bias;
-            const float g0 = wave_sum_dpp(gs) + (bias ? Wt<T>::scalar(bias, (size_t)b[u] * g.blk + q[u]) : 0.f);
-            const float u0 = wave_sum_dpp(us);
+            const float g0 = sc * wave_sum_dpp(gs) + (bias ? Wt<T>::scalar(bias, (size_t)b[u] * g.blk + q[u]) : 0.f);
+            const float u0 = sc * wave_sum_dpp(us);
             if (A == LS_ACT_REGLU) {
                 a[u] = fmaxf(g0, 0.f) * u0;
             } else {
@@ -400,30 +431,17 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         const bool last = l == g.L - 1;
         const int* Pc = sm.Plist[l & 1];
         LS_STAMP(P, g, l, 0, lane == 0);
-        // X: the layer input (layer 0's was tagged into the mailbox before the launch), the
-        // RMS scale from the values in registers, h into LDS, this tile's raw x into xt.
-        {
-            uint64_t v[D / 64];
-            wait_words<D / 64>(P.xmb + (size_t)l * D, D, g.tag, lane, P.err, v);
-            float ss = 0.f;
-#pragma unroll
-            for (int u = 0; u < D / 64; ++u) ss = fmaf(word_value(v[u]), word_value(v[u]), ss);
-            ss = wave_sum_dpp(ss);
-            const float sc = P.prenorm ? 1.f / sqrtf(ss / (float)D + 1e-6f) : 1.f;
-#pragma unroll
-            for (int u = 0; u < D / 64; ++u) {
-                const int i = u * 64 + lane;
-                const float x = word_value(v[u]);
-                if (g.has_tile && (i >> 4) == g.w) sm.xt[i & (kColTile - 1)] = x;
-                sm.hs[i] = x * sc;
-            }
-        }
+        // X: this wave's quarter of the layer input (layer 0's was tagged into the mailbox
+        // before the launch); the worker waves gather the other three
+        gather_input<D>(P, sm, g, l, 0, lane);
         LS_STAMP(P, g, l, 1, lane == 0);
-        lds_barrier();  // 1: h ready (and the folded rows of layers l, l+1 staged)
+        lds_barrier();  // 1: input gathered (and the folded rows of layers l, l+1 staged)
+        const float sc = input_scale<D>(P, sm, l);
         // S: this workgroup's scores, exact (layer l) and speculative (layer l+1), as dot
-        // products of the staged folded rows with h (lane-strided chunks, then DPP)
+        // products of the staged folded rows with the input (lane-strided chunks, then DPP),
+        // times the RMS scale
         {
-            const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.hs);
+            const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.xin);
 #pragma unroll
             for (int set = 0; set < 2; ++set) {
 #pragma unroll
@@ -442,9 +460,9 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                                 a[i & 3] = fmaf(pv.w, hv.w, a[i & 3]);
                             }
                         }
-                        const float sc = wave_sum_dpp((a[0] + a[1]) + (a[2] + a[3]));
+                        const float s_b = sc * wave_sum_dpp((a[0] + a[1]) + (a[2] + a[3]));
                         if (lane == 0)
-                            mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, sc);
+                            mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, s_b);
                     }
                 }
             }
@@ -531,7 +549,7 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                     qq2[u] = t % g.blk;
                 }
                 float a2[2];
-                ctl_gate_up<T, A, NC>(sm, g, l, P.block_bytes, bb2, qq2, a2, lane);
+                ctl_gate_up<T, A, NC>(sm, g, l, P.block_bytes, sc, bb2, qq2, a2, lane);
 #pragma unroll
                 for (int u = 0; u < 2; ++u)
                     if (mm2[u] >= 0 && lane == 0)
@@ -580,6 +598,9 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
     // pfr: folded predictor rows in flight (one layer), moved to LDS one layer after they
     // were requested; chunk c = wl + kWL*j of row m sits in pfr[m * kPfPer + j]
     u32x4 pfr[kMaxSRows * kPfPer], gg[kSlots][NC], uu[kSlots][NC], dn[kMaxDn];
+    uint32_t bw[kSlots];  // the word holding each slot's gate bias (when the layer has one)
+#pragma unroll
+    for (int sl = 0; sl < kSlots; ++sl) bw[sl] = 0u;
 #pragma unroll
     for (int j = 0; j < kMaxSRows * kPfPer; ++j) pfr[j] = zero4;
 #pragma unroll
@@ -623,6 +644,12 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         b = __builtin_amdgcn_readfirstlane(b);
         q = __builtin_amdgcn_readfirstlane(q);
         const uint8_t* base = sm.lt[layer].blocks + (size_t)b * bb;
+        {
+            // the gate bias word (from the block base when the layer has no bias)
+            const void* bias = sm.lt[layer].bias;
+            const uint32_t e = (uint32_t)min(b * g.blk + q, g.F - 1);
+            bw[sl] = gload_word(bias ? bias : (const void*)base, bias ? (e * KB) & ~3u : 0u);
+        }
         const uint8_t* gr = base + (size_t)q * row_bytes;
         const uint8_t* ur = base + (size_t)(g.blk + q) * row_bytes;
 #pragma unroll
@@ -642,16 +669,20 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
     // activations of the slots in `use` (wave-uniform bit mask) from their rows in gg/uu:
     // slot sl holds neuron q[sl] of block b[sl]; every lane gets the results.  One
     // slot at a time, with several partial sums per row for instruction-level parallelism.
-    auto gate_up = [&](int layer, unsigned use, const int (&b)[kSlots], const int (&q)[kSlots],
+    auto gate_up = [&](int layer, float sc, unsigned use, const int (&b)[kSlots], const int (&q)[kSlots],
                        float (&a)[kSlots]) {
         constexpr int NA = 4;  // partial sums per row
-        // this lane's part of h: all LDS reads in flight together, reused by every slot
+        // this lane's part of the input: all LDS reads in flight together, reused by every
+        // slot.  Read only by a wave with a slot in use: its published activations are what
+        // orders these reads before the next layer's input overwrites xin.
         f32x4 hr[NC][V / 4];
+        if (use) {
 #pragma unroll
-        for (int j = 0; j < NC; ++j)
+            for (int j = 0; j < NC; ++j)
 #pragma unroll
-            for (int i = 0; i < V / 4; ++i)
-                hr[j][i] = reinterpret_cast<const f32x4*>(sm.hs + (lane + 64 * j) * V)[i];
+                for (int i = 0; i < V / 4; ++i)
+                    hr[j][i] = reinterpret_cast<const f32x4*>(sm.xin + (lane + 64 * j) * V)[i];
+        }
         float gs[kSlots], us[kSlots];
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
@@ -685,9 +716,9 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
             if (use & (1u << sl)) {
-                const float g0 = wave_sum_dpp(gs[sl]) +
-                                 (bias ? Wt<T>::scalar(bias, (size_t)b[sl] * g.blk + q[sl]) : 0.f);
-                const float u0 = wave_sum_dpp(us[sl]);
+                const float g0 = sc * wave_sum_dpp(gs[sl]) +
+                                 (bias ? Wt<T>::from_word(bw[sl], (size_t)min(b[sl] * g.blk + q[sl], g.F - 1)) : 0.f);
+                const float u0 = sc * wave_sum_dpp(us[sl]);
                 if (A == LS_ACT_REGLU) {
                     a[sl] = fmaxf(g0, 0.f) * u0;
                 } else {
@@ -698,26 +729,44 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         }
     };
 
-    // this tile's down partial of the block whose piece sits in register position jp, with
-    // its activations at act[0..blk): lanes l, l+16, l+32, l+48 share a column; the column
-    // sums end in lanes 0..15
-    auto down_partial = [&](int p, const float* act) -> float {
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    // this tile's down partials of the wave's list positions (p = wave-1 + kWorkers*jp), from
+    // the pieces staged in LDS and the gathered activations.  Lane = column c + 16*gq; round r
+    // takes position jp = 4r + gq, and each lane sums its column over the block's NG*V neurons
+    // (chunk n*16 + c of a piece holds neurons n*V..n*V+V-1 of column c): no cross-lane
+    // reduction, and every LDS read of a round is issued before its products.
+    constexpr int kDnRounds = (kDnPos + 3) / 4;
+    auto down_round = [&](auto ng_const, int r) {
+        constexpr int NG = decltype(ng_const)::value;
+        const int c = lane & (kColTile - 1), gq = lane >> 4;
+        {
+            const int jp = 4 * r + gq;
+            const int p0 = (wave - 1) + kWorkers * jp;
+            const bool ok = jp < kDnPos && p0 < g.kp;
+            const int p = ok ? p0 : 0;  // a lane group without a position reads position 0
+            u32x4 wr[NG];
+            f32x4 av[NG][V / 4];
 #pragma unroll
-        for (int i = 0; i < kDnPer; ++i) {
-            const int cc = lane + 64 * i;
-            if (cc < g.NPC) {
-                float wv[V];
-                Wt<T>::widen(sm.dnl[p][cc], wv);
-                const float* ap = act + (cc / kColTile) * V;
+            for (int n = 0; n < NG; ++n) {
+                wr[n] = sm.dnl[p][n * kColTile + c];
 #pragma unroll
-                for (int v = 0; v < V; ++v) acc[v & 3] = fmaf(ap[v], wv[v], acc[v & 3]);
+                for (int i = 0; i < V / 4; ++i)
+                    av[n][i] = reinterpret_cast<const f32x4*>(sm.aall + p * g.blk + n * V)[i];
             }
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int n = 0; n < NG; ++n) {
+                float wv[V];
+                Wt<T>::widen(wr[n], wv);
+#pragma unroll
+                for (int i = 0; i < V / 4; ++i) {
+                    acc[0] = fmaf(av[n][i].x, wv[4 * i + 0], acc[0]);
+                    acc[1] = fmaf(av[n][i].y, wv[4 * i + 1], acc[1]);
+                    acc[2] = fmaf(av[n][i].z, wv[4 * i + 2], acc[2]);
+                    acc[3] = fmaf(av[n][i].w, wv[4 * i + 3], acc[3]);
+                }
+            }
+            if (ok) sm.dparts[p][c] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
         }
-        float t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-        t += __shfl_xor(t, 16, 64);
-        t += __shfl_xor(t, 32, 64);
-        return t;
     };
 
     int slot_t[kSlots];  // global slot index of each of this wave's slots
@@ -751,7 +800,10 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
                 }
             }
         }
-        lds_barrier();  // 1: h ready
+        // this wave's quarter of the layer input (no weight loads are in flight now)
+        gather_input<D>(P, sm, g, l, wave, lane);
+        lds_barrier();  // 1: input gathered
+        const float sc = input_scale<D>(P, sm, l);
         // early GU: every speculative position held in this wave's slots (prefetched during
         // the previous layer), published at its list position while the selection runs
         if (l > 0) {
@@ -765,13 +817,13 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
                 qs[sl] = t % g.blk;
                 if (t < g.kp * g.blk) use |= 1u << sl;
             }
-            LS_STAMP(P, g, l, 14, wave == 1 && lane == 0);
-            gate_up(l, use, bs, qs, as);
+            LS_STAMP(P, g, l, 14, wave == 3 && lane == 0);
+            gate_up(l, sc, use, bs, qs, as);
 #pragma unroll
             for (int sl = 0; sl < kSlots; ++sl)
                 if ((use & (1u << sl)) && lane == 0) mb_store(P.amb + (size_t)l * g.AW + slot_t[sl], g.tag, as[sl]);
         }
-        LS_STAMP(P, g, l, 13, wave == 1 && lane == 0);
+        LS_STAMP(P, g, l, 13, wave == 3 && lane == 0);
         // the selection: wave 2 the exact top-k of this layer, wave 3 the next layer's list
         if (wave == 2) {
             flag_wait(&sm.f_keys, l + 1, lane, P.err);
@@ -783,39 +835,37 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
             flag_set(&sm.f_pn, l + 1, lane);
             LS_STAMP(P, g, l, 12, lane == 0);
         }
-        // gate/up rows of the next layer's speculative list (issued by every slot; the last
-        // layer re-reads rows of its own so that the count stays fixed)
+        // the next layer's speculative list: its gate/up rows (and bias words), one slot at a
+        // time (issued by every slot; the last layer re-reads rows of its own so that the count
+        // stays fixed), each followed by a round of this layer's down partials: a compute unit
+        // holds only about one slot's loads per wave in flight before issue stalls, so the
+        // rounds run while the loads stream in
+        const int nl = last ? l : l + 1;
         flag_wait(&sm.f_pn, l + 1, lane, P.err);
-        {
-            const int nl = last ? l : l + 1;
-#pragma unroll
-            for (int sl = 0; sl < kSlots; ++sl) {
-                const int t = slot_t[sl];
-                const bool used = !last && t < g.kp * g.blk;
-                load_gu(sl, nl, used ? Pn[t / g.blk] : 0, used ? t % g.blk : 0);
-            }
-            // and their down pieces for this workgroup's tile
-#pragma unroll
-            for (int jp = 0; jp < kDnPos; ++jp) {
-                const int p = (wave - 1) + kWorkers * jp;
-                load_down_pos(nl, (!last && p < g.kp) ? Pn[p] : 0, jp);
-            }
-        }
-        LS_STAMP(P, g, l, 10, wave == 1 && lane == 0);
-        // down partials of every list position, from the pieces prefetched one layer ago
         flag_wait(&sm.f_acts, l + 1, lane, P.err);
-        if (l > 0 && g.has_tile) {
+        LS_STAMP(P, g, l, 15, wave == 3 && lane == 0);
+        const int ng = g.NPC / kColTile;
+        static_assert(kDnRounds == kSlots, "one down round per slot");
 #pragma unroll
-            for (int jp = 0; jp < kDnPos; ++jp) {
-                const int p = (wave - 1) + kWorkers * jp;
-                if (p < g.kp) {
-                    const float part = down_partial(p, sm.aall + p * g.blk);
-                    if (lane < kColTile) sm.dparts[p][lane] = part;
-                }
+        for (int sl = 0; sl < kSlots; ++sl) {
+            const int t = slot_t[sl];
+            const bool used = !last && t < g.kp * g.blk;
+            load_gu(sl, nl, used ? Pn[t / g.blk] : 0, used ? t % g.blk : 0);
+            if (l > 0 && g.has_tile) {
+                if (ng == 8) down_round(std::integral_constant<int, 8>{}, sl);
+                else if (ng == 4) down_round(std::integral_constant<int, 4>{}, sl);
+                else down_round(std::integral_constant<int, 2>{}, sl);
             }
         }
         flag_set(&sm.f_done[wave], l + 1, lane);
-        LS_STAMP(P, g, l, 11, wave == 1 && lane == 0);
+        LS_STAMP(P, g, l, 11, wave == 3 && lane == 0);
+        // then the next layer's down pieces for this workgroup's tile
+#pragma unroll
+        for (int jp = 0; jp < kDnPos; ++jp) {
+            const int p = (wave - 1) + kWorkers * jp;
+            load_down_pos(nl, (!last && p < g.kp) ? Pn[p] : 0, jp);
+        }
+        LS_STAMP(P, g, l, 10, wave == 3 && lane == 0);
         // folded rows of layer l+2
         load_pf(min(l + 2, g.L - 1));
     }
@@ -907,7 +957,11 @@ FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int
     if (k < 1 || kp < k || kp > kMaxKp || kp > s.n_blk) return {false, "k / speculative width"};
     if ((long)kp * s.blk > (long)kWorkers * kSlots * n_wg) return {false, "neuron slots"};
     if (s.blk * KB > 64 * kDnPer || kp > kMaxDnTot) return {false, "down chunks"};
-    if ((long)k * s.blk > kMaxA) return {false, "k * block"};
+    {
+        const int ng = s.blk * KB / 16;  // 16-byte chunks of one column of a down piece
+        if (s.blk * KB % 16 || (ng != 2 && ng != 4 && ng != 8)) return {false, "block size"};
+    }
+    if ((long)kp * s.blk > kMaxA) return {false, "speculative width * block"};
     return {true, ""};
 }
 

@@ -29,6 +29,8 @@ struct Wt<LS_F32> {
     __device__ static inline float scalar(const void* p, size_t i) {
         return static_cast<const float*>(p)[i];
     }
+    // element i of the array from the aligned 32-bit word holding it
+    __device__ static inline float from_word(uint32_t w, size_t) { return __uint_as_float(w); }
 };
 
 __device__ inline float half_bits_to_float(unsigned int bits16) {
@@ -53,6 +55,9 @@ struct Wt<LS_F16> {
     __device__ static inline float scalar(const void* p, size_t i) {
         return half_bits_to_float(static_cast<const unsigned short*>(p)[i]);
     }
+    __device__ static inline float from_word(uint32_t w, size_t i) {
+        return half_bits_to_float((i & 1) ? w >> 16 : w & 0xffffu);
+    }
 };
 
 template <>
@@ -72,6 +77,9 @@ struct Wt<LS_BF16> {
     }
     __device__ static inline float scalar(const void* p, size_t i) {
         return __uint_as_float(static_cast<unsigned int>(static_cast<const unsigned short*>(p)[i]) << 16);
+    }
+    __device__ static inline float from_word(uint32_t w, size_t i) {
+        return __uint_as_float((i & 1) ? w & 0xffff0000u : w << 16);
     }
 };
 
@@ -119,6 +127,16 @@ __device__ inline u32x4 gload_u(const void* uniform_base, uint32_t byte_off) {
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
     const char* base = (const char*)(((uint64_t)hi << 32) | lo);
     return __builtin_nontemporal_load((gvec_ptr)(base + byte_off));
+}
+
+// One aligned 32-bit word at a wave-uniform base plus a per-lane byte offset.
+typedef const __attribute__((address_space(1))) uint32_t* gword_ptr;
+__device__ inline uint32_t gload_word(const void* uniform_base, uint32_t byte_off) {
+    const uint64_t b = (uint64_t)uniform_base;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const char* base = (const char*)(((uint64_t)hi << 32) | lo);
+    return *(gword_ptr)(base + byte_off);
 }
 
 // Order-preserving map of a binary32 score to uint32: NaN -> 0 (below every number),
