@@ -254,17 +254,19 @@ struct Geo {
 // bit finds T, the m-th largest order key (the largest T with at least m keys >= T); the
 // set is every key > T plus the elements equal to T with the smallest indices.  Members
 // are written to out[] in index order (the set is what matters to the fused step; its
-// summation order is fixed by the slot map).  Needs 1 <= m <= n.
+// summation order is fixed by the slot map).  Only the top BITS bits of each key take part
+// (BITS = 32: the exact order).  Needs 1 <= m <= n.
+template <int BITS>
 __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int* out, int lane) {
     constexpr int Q = kMaxNb / 64;
     uint32_t ok[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int i = q * 64 + lane;
-        ok[q] = i < n ? keys[i] : 0u;  // padding compares below every c >= 1
+        ok[q] = i < n ? keys[i] >> (32 - BITS) : 0u;  // padding compares below every c >= 1
     }
     uint32_t T = 0u;
-    for (int bit = 31; bit >= 0; --bit) {
+    for (int bit = BITS - 1; bit >= 0; --bit) {
         const uint32_t c = T | (1u << bit);
         int cnt = 0;
 #pragma unroll
@@ -438,33 +440,34 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         lds_barrier();  // 1: input gathered (and the folded rows of layers l, l+1 staged)
         const float sc = input_scale<D>(P, sm, l);
         // S: this workgroup's scores, exact (layer l) and speculative (layer l+1), as dot
-        // products of the staged folded rows with the input (lane-strided chunks, then DPP),
-        // times the RMS scale
-        {
+        // products of the staged folded rows with the input (lane-strided chunks, both rows
+        // at once, then DPP), times the RMS scale.  The last layer's second row is stale and
+        // its score is not published.
+        static_assert(kMaxSRows == 1, "one folded row per workgroup and layer");
+        if (g.SPW > 0) {
+            constexpr int C = D / 4 / 64;  // 16-byte chunks per lane
             const f32x4* h4 = reinterpret_cast<const f32x4*>(sm.xin);
+            const f32x4* r0 = sm.pfs[l & 1][0];
+            const f32x4* r1 = sm.pfs[(l + 1) & 1][0];
+            float a0[4] = {0.f, 0.f, 0.f, 0.f}, a1[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int set = 0; set < 2; ++set) {
-#pragma unroll
-                for (int m = 0; m < kMaxSRows; ++m) {
-                    if (m < g.SPW && (set == 0 || !last)) {
-                        const f32x4* row = sm.pfs[(l + set) & 1][m];
-                        float a[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                        for (int i = 0; i < kMaxD / 4 / 64; ++i) {
-                            const int c = lane + 64 * i;
-                            if (c < g.CH) {
-                                const f32x4 pv = row[c], hv = h4[c];
-                                a[i & 3] = fmaf(pv.x, hv.x, a[i & 3]);
-                                a[i & 3] = fmaf(pv.y, hv.y, a[i & 3]);
-                                a[i & 3] = fmaf(pv.z, hv.z, a[i & 3]);
-                                a[i & 3] = fmaf(pv.w, hv.w, a[i & 3]);
-                            }
-                        }
-                        const float s_b = sc * wave_sum_dpp((a[0] + a[1]) + (a[2] + a[3]));
-                        if (lane == 0)
-                            mb_store(P.smb + (size_t)l * 2 * g.nb + set * g.nb + (g.w + g.G * m), g.tag, s_b);
-                    }
-                }
+            for (int i = 0; i < C; ++i) {
+                const int c = lane + 64 * i;
+                const f32x4 hv = h4[c], p0 = r0[c], p1 = r1[c];
+                a0[i & 3] = fmaf(p0.x, hv.x, a0[i & 3]);
+                a1[i & 3] = fmaf(p1.x, hv.x, a1[i & 3]);
+                a0[i & 3] = fmaf(p0.y, hv.y, a0[i & 3]);
+                a1[i & 3] = fmaf(p1.y, hv.y, a1[i & 3]);
+                a0[i & 3] = fmaf(p0.z, hv.z, a0[i & 3]);
+                a1[i & 3] = fmaf(p1.z, hv.z, a1[i & 3]);
+                a0[i & 3] = fmaf(p0.w, hv.w, a0[i & 3]);
+                a1[i & 3] = fmaf(p1.w, hv.w, a1[i & 3]);
+            }
+            const float s0 = sc * wave_sum_dpp((a0[0] + a0[1]) + (a0[2] + a0[3]));
+            const float s1 = sc * wave_sum_dpp((a1[0] + a1[1]) + (a1[2] + a1[3]));
+            if (lane == 0) {
+                mb_store(P.smb + (size_t)l * 2 * g.nb + g.w, g.tag, s0);
+                if (!last) mb_store(P.smb + (size_t)l * 2 * g.nb + g.nb + g.w, g.tag, s1);
             }
         }
         LS_STAMP(P, g, l, 2, lane == 0);
@@ -827,11 +830,13 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         // the selection: wave 2 the exact top-k of this layer, wave 3 the next layer's list
         if (wave == 2) {
             flag_wait(&sm.f_keys, l + 1, lane, P.err);
-            top_set(sm.key[0], g.nb, g.k, sm.E, lane);
+            top_set<32>(sm.key[0], g.nb, g.k, sm.E, lane);
             flag_set(&sm.f_E, l + 1, lane);
         } else if (wave == 3) {
             flag_wait(&sm.f_keys, l + 1, lane, P.err);
-            if (!last) top_set(sm.key[1], g.nb, g.kp, const_cast<int*>(Pn), lane);
+            // the speculative list only decides what is prefetched: its keys are cut to 16 bits
+            // (ties to the smaller index), which halves the search
+            if (!last) top_set<16>(sm.key[1], g.nb, g.kp, const_cast<int*>(Pn), lane);
             flag_set(&sm.f_pn, l + 1, lane);
             LS_STAMP(P, g, l, 12, lane == 0);
         }
