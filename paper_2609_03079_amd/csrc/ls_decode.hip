@@ -660,7 +660,7 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
 #pragma unroll
         for (int j = 0; j < NC; ++j) uu[sl][j] = gload_u(ur, (uint32_t)(lane + 64 * j) * 16u);
     };
-    // down pieces: position p = (wave-1) + 7*jp of the list, chunks lane + 64*i of the piece
+    // down pieces: position p = (wave-1) + kWorkers*jp of the list, chunks lane + 64*i of the piece
     auto load_down_pos = [&](int layer, int b, int jp) {
         b = __builtin_amdgcn_readfirstlane(b);
         const uint8_t* base = sm.lt[layer].blocks + (size_t)b * bb + down_off;
@@ -841,21 +841,21 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
             LS_STAMP(P, g, l, 12, lane == 0);
         }
         // the next layer's speculative list: its gate/up rows (and bias words), one slot at a
-        // time (issued by every slot; the last layer re-reads rows of its own so that the count
-        // stays fixed), each followed by a round of this layer's down partials: a compute unit
-        // holds only about one slot's loads per wave in flight before issue stalls, so the
-        // rounds run while the loads stream in
-        const int nl = last ? l : l + 1;
+        // time, each followed by a round of this layer's down partials: a compute unit holds
+        // only about one slot's loads per wave in flight before issue stalls, so the rounds run
+        // while the loads stream in.  Slots beyond the list (and the last layer) load nothing:
+        // the next uses of these registers come after the layer-start wait for every load.
         flag_wait(&sm.f_pn, l + 1, lane, P.err);
-        flag_wait(&sm.f_acts, l + 1, lane, P.err);
-        LS_STAMP(P, g, l, 15, wave == 3 && lane == 0);
         const int ng = g.NPC / kColTile;
         static_assert(kDnRounds == kSlots, "one down round per slot");
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
             const int t = slot_t[sl];
-            const bool used = !last && t < g.kp * g.blk;
-            load_gu(sl, nl, used ? Pn[t / g.blk] : 0, used ? t % g.blk : 0);
+            if (!last && t < g.kp * g.blk) load_gu(sl, l + 1, Pn[t / g.blk], t % g.blk);
+            if (sl == 0) {
+                flag_wait(&sm.f_acts, l + 1, lane, P.err);
+                LS_STAMP(P, g, l, 15, wave == 3 && lane == 0);
+            }
             if (l > 0 && g.has_tile) {
                 if (ng == 8) down_round(std::integral_constant<int, 8>{}, sl);
                 else if (ng == 4) down_round(std::integral_constant<int, 4>{}, sl);
@@ -865,14 +865,16 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         flag_set(&sm.f_done[wave], l + 1, lane);
         LS_STAMP(P, g, l, 11, wave == 3 && lane == 0);
         // then the next layer's down pieces for this workgroup's tile
+        if (!last) {
 #pragma unroll
-        for (int jp = 0; jp < kDnPos; ++jp) {
-            const int p = (wave - 1) + kWorkers * jp;
-            load_down_pos(nl, (!last && p < g.kp) ? Pn[p] : 0, jp);
+            for (int jp = 0; jp < kDnPos; ++jp) {
+                const int p = (wave - 1) + kWorkers * jp;
+                if (p < g.kp) load_down_pos(l + 1, Pn[p], jp);
+            }
         }
         LS_STAMP(P, g, l, 10, wave == 3 && lane == 0);
-        // folded rows of layer l+2
-        load_pf(min(l + 2, g.L - 1));
+        // folded rows of layer l+2 (staged at the next layer's start)
+        if (l + 2 < g.L) load_pf(l + 2);
     }
 }
 
