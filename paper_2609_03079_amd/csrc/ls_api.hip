@@ -377,7 +377,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
         return bail(LS_E_NOMEM, "workspace allocation failed");
     }
     {
-        c->mailbox_words = ls::fused_mailbox_words(s, L);
+        c->mailbox_words = ls::fused_mailbox_words(s, L, c->n_wg);
         c->layer_tab_host.assign(L, ls::LayerPtrs{});
         if (dmalloc(&c->mailbox, c->mailbox_words) != hipSuccess || dmalloc(&c->layer_tab, (size_t)L) != hipSuccess ||
             dmalloc(&c->dev_err, 1) != hipSuccess) {
@@ -690,7 +690,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             const size_t L = (size_t)c->desc.n_layers;
             a.xmb = c->mailbox;
             a.smb = a.xmb + L * s.d;
-            a.amb = a.smb + L * 2 * s.n_blk;
+            a.amb = a.smb + L * ls::fused_score_words(s);
             a.tag = ++c->epoch;
             a.err = c->dev_err;
             a.trace = c->trace_wg >= 0 ? c->trace : nullptr;
@@ -772,9 +772,10 @@ ls_status ls_debug_decode_trace(ls_ffn* c, int32_t layer, float* x_in, float* sc
     const uint64_t* smb = xmb + L * s.d;
     if (x_in) {
         if (layer == 0) return fail(c, LS_E_INVAL, "layer 0 input is the caller's own x");
-        LS_HIP(c, ls::launch_untag(xmb + (size_t)layer * s.d, s.d, x_in, c->stream));
+        LS_HIP(c, ls::launch_untag(xmb + (size_t)layer * s.d, s.d, 1, x_in, c->stream));
     }
-    if (scores) LS_HIP(c, ls::launch_untag(smb + (size_t)layer * 2 * s.n_blk, s.n_blk, scores, c->stream));
+    if (scores)
+        LS_HIP(c, ls::launch_untag(smb + (size_t)layer * ls::fused_score_words(s), s.n_blk, ls::kScoreStride, scores, c->stream));
     return LS_OK;
 }
 

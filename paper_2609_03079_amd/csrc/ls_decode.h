@@ -40,11 +40,20 @@ FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int
 // Largest speculative width (blocks prefetched for the next layer) the fused kernel holds.
 int fused_max_spec(const Shape& s, int n_wg);
 
-// Number of 64-bit mailbox words the fused kernel needs for L layers.
-size_t fused_mailbox_words(const Shape& s, int L);
+// Mailbox layout of the fused kernel: per layer, the input x (d words; workgroup w writes its
+// 16-column tile, one 128-byte line), then the scores (kScoreStride words per workgroup, a
+// 64-byte line of its own: exact at +0, speculative at +1; when many workgroups write into
+// one line the exchange takes about twice as long), then the activations in list order
+// (kp*blk words, then k*blk for the misses; at most F + F).
+constexpr int kScoreStride = 8;
+__host__ __device__ inline size_t fused_score_words_n(int n_blk) { return (size_t)n_blk * kScoreStride; }
+inline size_t fused_score_words(const Shape& s) { return fused_score_words_n(s.n_blk); }
+inline size_t fused_mailbox_words(const Shape& s, int L, int /*n_wg*/) {
+    return (size_t)L * ((size_t)s.d + fused_score_words(s) + 2 * (size_t)s.F);
+}
 
-// dst[i] = value bits of the tagged words src[0..n)
-hipError_t launch_untag(const uint64_t* src, int n, float* dst, hipStream_t st);
+// dst[i] = value bits of the tagged words src[i * stride], i < n
+hipError_t launch_untag(const uint64_t* src, int n, int stride, float* dst, hipStream_t st);
 
 // cooperative: hipLaunchCooperativeKernel (guaranteed co-residency), else a plain launch
 hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, bool cooperative,

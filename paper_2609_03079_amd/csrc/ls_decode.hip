@@ -243,6 +243,7 @@ struct Geo {
     int SPW;  // folded predictor rows of this workgroup: rows w, w + G, ... below n_blk
     int CH;   // 16-byte chunks of one folded row (d / 4)
     int NPC;  // 16-byte chunks of one block's down piece for one column tile
+    int SW;   // score words per layer
     int AW;   // activation words per layer: list positions, then misses
     int miss_base;
     bool has_tile;
@@ -466,23 +467,28 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             const float s0 = sc * wave_sum_dpp((a0[0] + a0[1]) + (a0[2] + a0[3]));
             const float s1 = sc * wave_sum_dpp((a1[0] + a1[1]) + (a1[2] + a1[3]));
             if (lane == 0) {
-                mb_store(P.smb + (size_t)l * 2 * g.nb + g.w, g.tag, s0);
-                if (!last) mb_store(P.smb + (size_t)l * 2 * g.nb + g.nb + g.w, g.tag, s1);
+                mb_store(P.smb + (size_t)l * g.SW + g.w * kScoreStride, g.tag, s0);
+                if (!last) mb_store(P.smb + (size_t)l * g.SW + g.w * kScoreStride + 1, g.tag, s1);
             }
         }
         LS_STAMP(P, g, l, 2, lane == 0);
         // order keys of every block's score (exact, then speculative); waves 2 and 3 rank them
         {
-            const int n = last ? g.nb : 2 * g.nb;
-            uint64_t v[2 * kMaxNb / 64];
-            wait_words<2 * kMaxNb / 64>(P.smb + (size_t)l * 2 * g.nb, n, g.tag, lane, P.err, v);
+            // load u: block (u >> 1) * 64 + lane, list u & 1 (the last layer has no second list)
+            constexpr int W = 2 * kMaxNb / 64;
+            uint64_t v[W];
+            const uint32_t row = (uint32_t)(l * g.SW);
+            wait_gather_off<W>(
+                P.smb,
+                [&](int u) {
+                    const int b = min((u >> 1) * 64 + lane, g.nb - 1);
+                    return row + (uint32_t)(b * kScoreStride + (last ? 0 : (u & 1)));
+                },
+                2 * ((g.nb + 63) / 64), g.tag, lane, P.err, v);
 #pragma unroll
-            for (int u = 0; u < 2 * kMaxNb / 64; ++u) {
-                const int i = u * 64 + lane;
-                if (i < n) {
-                    const int list = i >= g.nb;
-                    sm.key[list][i - list * g.nb] = order_key(word_value(v[u]));
-                }
+            for (int u = 0; u < W; ++u) {
+                const int b = (u >> 1) * 64 + lane;
+                if (b < g.nb && !(last && (u & 1))) sm.key[u & 1][b] = order_key(word_value(v[u]));
             }
         }
         flag_set(&sm.f_keys, l + 1, lane);
@@ -896,6 +902,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
     g.F = P.F;
     g.SPW = g.w < g.nb ? (g.nb - 1 - g.w) / g.G + 1 : 0;
     g.CH = D / 4;
+    g.SW = (int)fused_score_words_n(g.nb);
     g.miss_base = g.kp * g.blk;
     g.AW = (g.kp + g.k) * g.blk;
     g.NPC = g.blk * KB;
@@ -939,16 +946,16 @@ hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hip
     return hipLaunchKernel(fn, dim3(n_wg), dim3(kThreads), args, 0, st);
 }
 
-__global__ void untag_kernel(const uint64_t* __restrict__ src, int n, float* __restrict__ dst) {
+__global__ void untag_kernel(const uint64_t* __restrict__ src, int n, int stride, float* __restrict__ dst) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) dst[i] = __uint_as_float((uint32_t)src[i]);
+    if (i < n) dst[i] = __uint_as_float((uint32_t)src[(size_t)i * stride]);
 }
 
 }  // namespace
 
-hipError_t launch_untag(const uint64_t* src, int n, float* dst, hipStream_t st) {
+hipError_t launch_untag(const uint64_t* src, int n, int stride, float* dst, hipStream_t st) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(untag_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, n, dst);
+    hipLaunchKernelGGL(untag_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, n, stride, dst);
     return hipGetLastError();
 }
 
@@ -978,10 +985,6 @@ int fused_max_spec(const Shape& s, int n_wg) {
     return (int)std::min<long>(m, s.n_blk);
 }
 
-size_t fused_mailbox_words(const Shape& s, int L) {
-    // per layer: x, scores (exact | speculative), activations (list positions | misses)
-    return (size_t)L * ((size_t)s.d + 2 * (size_t)s.n_blk + 2 * (size_t)s.F);
-}
 
 hipError_t launch_decode_fused(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hipStream_t st) {
     const bool relu = s.act == LS_ACT_REGLU;
