@@ -233,7 +233,7 @@ struct Smem {
     u32x4 dnl[kMaxDnTot][64 * kDnPer];
     alignas(16) float amiss[kMaxKp][64];  // activations of the misses
     // LDS flags (value = layer + 1 once set for that layer)
-    int f_keys, f_acts, f_E, f_pn;
+    int f_keys, f_acts, f_E, f_pn, f_out;
     int f_done[kWaves];
 };
 
@@ -587,6 +587,7 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                 else mb_store(P.xmb + (size_t)(l + 1) * D + g.w * kColTile + lane, g.tag, xn);
             }
         }
+        flag_set(&sm.f_out, l + 1, lane);  // the output store is issued: the workers may queue loads
         LS_STAMP(P, g, l, 9, lane == 0);
     }
 }
@@ -870,7 +871,9 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         }
         flag_set(&sm.f_done[wave], l + 1, lane);
         LS_STAMP(P, g, l, 11, wave == 3 && lane == 0);
-        // then the next layer's down pieces for this workgroup's tile
+        // then the next layer's down pieces for this workgroup's tile, once the control wave
+        // has issued this layer's output (loads queued before it would delay the exchange)
+        flag_wait(&sm.f_out, l + 1, lane, P.err);
         if (!last) {
 #pragma unroll
             for (int jp = 0; jp < kDnPos; ++jp) {
@@ -914,7 +917,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
         const int words = P.L * (int)(sizeof(LayerPtrs) / 4);
         for (int i = threadIdx.x; i < words; i += kThreads) dst[i] = src[i];
         if (threadIdx.x == 0) {
-            sm.f_keys = sm.f_acts = sm.f_E = sm.f_pn = 0;
+            sm.f_keys = sm.f_acts = sm.f_E = sm.f_pn = sm.f_out = 0;
             for (int v = 0; v < kWaves; ++v) sm.f_done[v] = 0;
         }
         __syncthreads();
