@@ -155,6 +155,40 @@ ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int3
 ls_status ls_stream_weights(ls_ffn* ctx, int32_t layer, const int32_t* idx_host, int32_t n,
                             int32_t n_stages, ls_stream_stats* stats);
 
+/* Cross-layer prefetch policy of ls_decode_step_streamed. */
+typedef enum {
+    LS_PREFETCH_NONE = 0,    /* a layer's blocks are requested once its own list is known */
+    LS_PREFETCH_ONESHOT = 1, /* while layer n runs, layer n+1 is scored once on x_n (the
+                                input of layer n) and its list is prefetched */
+    LS_PREFETCH_REFINE = 2   /* after every stage j of layer n, layer n+1 is re-scored on the
+                                refined feature x~_n^(j) (Sec. 2.1, Eq. 2) and the blocks of
+                                its new list that are not yet resident are prefetched */
+} ls_prefetch_mode;
+
+typedef struct {
+    int64_t final_bytes;   /* block bytes of every layer's final list (k blocks per layer) */
+    int64_t copied_bytes;  /* all bytes copied host -> HBM by the step */
+    int64_t late_bytes;    /* copied after the layer's own list was known: its compute waits */
+    int64_t spec_bytes;    /* copied ahead of time for the next layer */
+    int64_t wasted_bytes;  /* of spec_bytes: blocks the next layer's final list did not hold */
+} ls_stream_report;
+
+/* One decode step (B = 1) over every layer with host-resident weights, staged
+ * (Sec. 2.1, Eq. 1-2).  Layer n's final list is topk(predict(n, x_n), k), from
+ * its complete input exactly as in ls_decode_step; its blocks are requested
+ * (misses copied in priority order in n_stages stages) and the layer runs as
+ * n_stages sparse steps over equal parts of the list, each waiting only for its
+ * own copies.  mode adds prefetch of layer n+1 during layer n (k_spec blocks per
+ * prediction), with layer n's blocks protected from eviction meanwhile.  The
+ * result depends only on the final lists, so every mode gives the same x
+ * bitwise; the modes differ in when and how many bytes cross the host link.
+ * x: dev fp32 [d], updated in place.  report may be NULL.
+ * LS_E_UNSUPPORTED with HBM-resident weights; LS_E_INVAL on bad arguments;
+ * LS_E_CAPACITY if the cache cannot hold a layer's list (plus, while
+ * prefetching, the next layer's) with the running layer's blocks protected. */
+ls_status ls_decode_step_streamed(ls_ffn* ctx, float* x, int32_t k, int32_t n_stages, int32_t mode,
+                                  int32_t k_spec, ls_stream_report* report);
+
 /* One decode step over every layer: for l in 0..L-1:
  *   scores = predict(l, x); idx = topk(scores, k) (union over the B tokens if B > 1);
  *   x = x + sparse_ffn(l, x, idx[0..count)).

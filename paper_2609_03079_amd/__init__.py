@@ -24,9 +24,10 @@ LS_F32, LS_F16, LS_BF16 = 0, 1, 2
 LS_ACT_REGLU, LS_ACT_SWIGLU_THRESH = 0, 1
 LS_WEIGHTS_HBM, LS_WEIGHTS_HOST = 0, 1
 LS_SEL_TOPK, LS_SEL_THRESHOLD = 0, 1
+LS_PREFETCH_NONE, LS_PREFETCH_ONESHOT, LS_PREFETCH_REFINE = 0, 1, 2
 
 EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", "ls_select_blocks",
-           "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step",
+           "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step_streamed", "ls_decode_step",
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
@@ -58,6 +59,12 @@ class LsStreamStats(ctypes.Structure):
                 ("evictions", ctypes.c_int64)]
 
 
+class LsStreamReport(ctypes.Structure):
+    _fields_ = [("final_bytes", ctypes.c_int64), ("copied_bytes", ctypes.c_int64),
+                ("late_bytes", ctypes.c_int64), ("spec_bytes", ctypes.c_int64),
+                ("wasted_bytes", ctypes.c_int64)]
+
+
 class LsError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
@@ -84,6 +91,7 @@ def load():
     lib.ls_sparse_ffn_step.argtypes = [P, I32, P, I32, P, P, I32, I32, P]
     lib.ls_stream_weights.argtypes = [P, I32, P, I32, I32, ctypes.POINTER(LsStreamStats)]
     lib.ls_decode_step.argtypes = [P, P, I32, I32]
+    lib.ls_decode_step_streamed.argtypes = [P, P, I32, I32, I32, I32, ctypes.POINTER(LsStreamReport)]
     lib.ls_debug_last_activations.argtypes = [P, P, I64, ctypes.POINTER(I64)]
     lib.ls_set_kernel_timing.argtypes = [P, I32]
     lib.ls_kernel_timing.argtypes = [P, I32, I32, ctypes.POINTER(ctypes.c_double),
@@ -177,6 +185,13 @@ class Ffn:
                                                               int(a.size), n_stages,
                                                               ctypes.byref(stats)))
         return stats
+
+    def ls_decode_step_streamed(self, x, k: int, n_stages: int, mode: int, k_spec: int = 0
+                                ) -> LsStreamReport:
+        rep = LsStreamReport()
+        _check(self.lib, self.ctx, self.lib.ls_decode_step_streamed(self.ctx, _ptr(x), k, n_stages,
+                                                                    mode, k_spec, ctypes.byref(rep)))
+        return rep
 
     def ls_decode_step(self, x, B: int, k: int) -> None:
         _check(self.lib, self.ctx, self.lib.ls_decode_step(self.ctx, _ptr(x), B, k))

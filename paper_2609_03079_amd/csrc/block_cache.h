@@ -19,9 +19,10 @@ namespace ls {
 class BlockCache {
 public:
     struct Fill {
-        int pos;    // position of the block in the request
-        int block;  // block id
-        int slot;   // destination slot
+        int pos;            // position of the block in the request
+        int block;          // block id
+        int slot;           // destination slot
+        int evicted_layer;  // layer of the block the slot held before, or -1
     };
     struct Result {
         bool ok = false;
@@ -43,14 +44,22 @@ public:
 
     int64_t slots() const { return slots_; }
 
-    // Place blocks[0..n) of `layer`; fills receives the misses in priority order.
-    Result request(int layer, const int32_t* blocks, int n, std::vector<Fill>* fills) {
+    // Place blocks[0..n) of `layer`; fills receives the misses in priority order.  Blocks of
+    // `protect_layer` (>= 0: a layer whose compute may still be queued) are not evicted either;
+    // the request fails when the remaining slots cannot hold its misses.
+    Result request(int layer, const int32_t* blocks, int n, std::vector<Fill>* fills, int protect_layer = -1) {
         Result r;
         if (fills) fills->clear();
         if (layer < 0 || layer >= n_layers_ || n < 0 || n > slots_) return r;
         ++epoch_;
         for (int i = 0; i < n; ++i)
             if (blocks[i] < 0 || blocks[i] >= n_blk_) return r;
+        if (protect_layer >= 0 && protect_layer < n_layers_ && protect_layer != layer) {
+            for (int b = 0; b < n_blk_; ++b) {
+                const int64_t s = table_[key(protect_layer, b)];
+                if (s >= 0) mark_[s] = epoch_;
+            }
+        }
         // pass 1: hits become most recent and are marked as part of this request
         std::vector<char> hit(n, 0);
         for (int i = 0; i < n; ++i) {
@@ -62,6 +71,19 @@ public:
                 ++r.hits;
             }
         }
+        // capacity check before any slot changes hands: the distinct misses must fit in the
+        // slots this request may take (not its hits, not the protected layer's)
+        {
+            int64_t marked = 0, need = 0;
+            for (int64_t s = 0; s < slots_; ++s) marked += mark_[s] == epoch_;
+            std::vector<char> seen((size_t)n_blk_, 0);
+            for (int i = 0; i < n; ++i)
+                if (!hit[i] && !seen[(size_t)blocks[i]]) {
+                    seen[(size_t)blocks[i]] = 1;
+                    ++need;
+                }
+            if (need > slots_ - marked) return Result{};
+        }
         // pass 2: misses take the least recent slot not marked by this request; a repeat of a
         // block placed earlier in this pass counts as a hit, so hits + misses == n.
         for (int i = 0; i < n; ++i) {
@@ -70,9 +92,12 @@ public:
                 ++r.hits;
                 continue;
             }
-            const int64_t s = tail_;
-            if (s < 0 || mark_[s] == epoch_) return Result{};  // cannot happen for n <= slots
+            int64_t s = tail_;
+            while (s >= 0 && mark_[s] == epoch_) s = prev_[s];  // least recent unprotected slot
+            if (s < 0) return Result{};
+            int evicted = -1;
             if (owner_[s] >= 0) {
+                evicted = (int)(owner_[s] / n_blk_);
                 table_[owner_[s]] = -1;
                 ++r.evictions;
             }
@@ -81,7 +106,7 @@ public:
             mark_[s] = epoch_;
             touch(s);
             ++r.misses;
-            if (fills) fills->push_back(Fill{i, blocks[i], (int)s});
+            if (fills) fills->push_back(Fill{i, blocks[i], (int)s, evicted});
         }
         r.ok = true;
         return r;

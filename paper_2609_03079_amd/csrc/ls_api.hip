@@ -49,10 +49,17 @@ struct ls_ffn {
     int32_t* slot_tables = nullptr;  // device, [L][n_blk]
     int32_t* slot_tables_host = nullptr;  // pinned mirror
     ls::BlockCache* bcache = nullptr;
-    std::vector<hipEvent_t> stage_events;
-    std::vector<std::pair<int, int>> stage_ranges;  // [begin,end) of each pending stage
-    int pending_layer = -1;
-    hipEvent_t compute_done = nullptr;
+    // per layer: the copy stages of its latest request ([begin,end) of the list and the event
+    // after the stage's copies), whether it was ever requested, and an event after its latest
+    // compute (a copy into a slot waits only for the compute of the layer that held the slot)
+    std::vector<std::vector<hipEvent_t>> stage_events;
+    std::vector<std::vector<std::pair<int, int>>> stage_ranges;
+    std::vector<uint8_t> streamed;
+    std::vector<hipEvent_t> layer_done;
+    std::vector<uint8_t> layer_done_recorded;
+    int32_t* idx_pinned = nullptr;  // pinned [3][n_blk]: lists read back by the streamed decode step
+    int32_t* spec_idx = nullptr;    // device [2][n_blk] + counts [2]: its speculative selections
+    hipEvent_t spec_read[2] = {nullptr, nullptr};  // after the read-back of each speculative list
 
     std::vector<hipEvent_t> table_uploaded;  // per layer: last slot-table upload
 
@@ -241,14 +248,17 @@ void free_all(ls_ffn* c) {
     c->arena.clear();
     for (void* p : {(void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
                     (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
-                    (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err,
+                    (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err, (void*)c->spec_idx,
                     (void*)c->trace})
         if (p) (void)hipFree(p);
     if (c->staging) (void)hipHostFree(c->staging);
     if (c->host_blocks) (void)hipHostFree(c->host_blocks);
     if (c->slot_tables_host) (void)hipHostFree(c->slot_tables_host);
-    for (auto e : c->stage_events) (void)hipEventDestroy(e);
-    if (c->compute_done) (void)hipEventDestroy(c->compute_done);
+    for (auto& v : c->stage_events)
+        for (auto e : v) (void)hipEventDestroy(e);
+    for (auto e : c->layer_done) if (e) (void)hipEventDestroy(e);
+    for (auto e : c->spec_read) if (e) (void)hipEventDestroy(e);
+    if (c->idx_pinned) (void)hipHostFree(c->idx_pinned);
     if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
     for (auto e : c->table_uploaded) if (e) (void)hipEventDestroy(e);
     for (auto& p : c->pending) {
@@ -361,12 +371,25 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             return bail(LS_E_DEVICE, "slot table upload failed");
         c->bcache = new (std::nothrow) ls::BlockCache(slots, L, s.n_blk);
         if (!c->bcache) return bail(LS_E_NOMEM, "host allocation failed");
-        if (hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking) != hipSuccess ||
-            hipEventCreateWithFlags(&c->compute_done, hipEventDisableTiming) != hipSuccess)
-            return bail(LS_E_DEVICE, "stream/event creation failed");
+        if (hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking) != hipSuccess)
+            return bail(LS_E_DEVICE, "stream creation failed");
         c->table_uploaded.assign(L, nullptr);
+        c->layer_done.assign(L, nullptr);
+        c->layer_done_recorded.assign(L, 0);
+        c->streamed.assign(L, 0);
+        c->stage_events.assign(L, {});
+        c->stage_ranges.assign(L, {});
         for (int l = 0; l < L; ++l)
-            if (hipEventCreateWithFlags(&c->table_uploaded[l], hipEventDisableTiming) != hipSuccess)
+            if (hipEventCreateWithFlags(&c->table_uploaded[l], hipEventDisableTiming) != hipSuccess ||
+                hipEventCreateWithFlags(&c->layer_done[l], hipEventDisableTiming) != hipSuccess)
+                return bail(LS_E_DEVICE, "event creation failed");
+        if (hipHostMalloc((void**)&c->idx_pinned, 3 * (size_t)s.n_blk * sizeof(int32_t)) != hipSuccess ||
+            dmalloc(&c->spec_idx, 2 * (size_t)s.n_blk + 2) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(LS_E_NOMEM, "streamed-step buffers allocation failed");
+        }
+        for (auto& e : c->spec_read)
+            if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess)
                 return bail(LS_E_DEVICE, "event creation failed");
     }
     if (dmalloc(&c->z, (size_t)B * (s.fold ? 1 : s.r)) != hipSuccess ||
@@ -537,12 +560,11 @@ ls_status ls_select_blocks(ls_ffn* c, const float* scores, int32_t B, ls_sel_mod
 
 // Waits of the compute stream for the copy stages of a streamed layer that overlap [begin,end).
 static ls_status wait_stages(ls_ffn* c, int32_t layer, int32_t begin, int32_t end) {
-    if (c->desc.residency != LS_WEIGHTS_HOST || c->pending_layer != layer) return LS_OK;
-    for (size_t s = 0; s < c->stage_ranges.size(); ++s) {
-        const auto r = c->stage_ranges[s];
-        if (r.first < end && begin < r.second)
-            LS_HIP(c, hipStreamWaitEvent(c->stream, c->stage_events[s], 0));
-    }
+    if (c->desc.residency != LS_WEIGHTS_HOST) return LS_OK;
+    const auto& ranges = c->stage_ranges[layer];
+    for (size_t s = 0; s < ranges.size(); ++s)
+        if (ranges[s].first < end && begin < ranges[s].second)
+            LS_HIP(c, hipStreamWaitEvent(c->stream, c->stage_events[layer][s], 0));
     return LS_OK;
 }
 
@@ -563,7 +585,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
     ls::LayerDev L = c->dev[layer];
     const int32_t* slot_table = nullptr;
     if (c->desc.residency == LS_WEIGHTS_HOST) {
-        if (c->pending_layer != layer)
+        if (!c->streamed[layer])
             return fail(c, LS_E_STATE, "blocks of this layer were not streamed (ls_stream_weights)");
         L.blocks = c->cache;
         slot_table = c->slot_tables + (size_t)layer * s.n_blk;
@@ -572,7 +594,10 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
     }
     LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, x_in, B, idx, count, begin, end, c->a, c->stream); }));
     LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream); }));
-    if (c->desc.residency == LS_WEIGHTS_HOST) LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
+    if (c->desc.residency == LS_WEIGHTS_HOST) {
+        LS_HIP(c, hipEventRecord(c->layer_done[layer], c->stream));
+        c->layer_done_recorded[layer] = 1;
+    }
     c->last_act_n = (int64_t)end * s.blk;
     c->last_act_B = B;
     return LS_OK;
@@ -591,6 +616,69 @@ ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t*
     return LS_OK;
 }
 
+// Host-resident request (validated by the caller): place idx_host[0..n) of `layer` in the block
+// cache and queue the misses' copies in n_stages stages.  The copy stream first waits for the
+// latest compute of every layer that held a reassigned slot and of `layer` itself (whose slot
+// table it rewrites); compute of other layers keeps running under the copies.  The stages of
+// the latest request of a layer are what its sparse steps wait for (earlier requests' copies
+// precede them on the copy stream).  copied (may be null) receives the blocks copied.
+static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_host, int32_t n, int32_t n_stages,
+                                ls_stream_stats* stats, std::vector<int32_t>* copied, int protect_layer = -1) {
+    const Shape& s = c->shape;
+    if (n > c->bcache->slots()) return fail(c, LS_E_CAPACITY, "request exceeds the HBM cache slots");
+    std::vector<ls::BlockCache::Fill> fills;
+    ls::BlockCache::Result res = c->bcache->request(layer, idx_host, n, &fills, protect_layer);
+    if (!res.ok) return fail(c, LS_E_CAPACITY, "cache could not place the request");
+    {
+        std::vector<uint8_t> wait((size_t)c->desc.n_layers, 0);
+        wait[(size_t)layer] = 1;
+        for (const auto& f : fills)
+            if (f.evicted_layer >= 0) wait[(size_t)f.evicted_layer] = 1;
+        for (int l = 0; l < c->desc.n_layers; ++l)
+            if (wait[(size_t)l] && c->layer_done_recorded[(size_t)l])
+                LS_HIP(c, hipStreamWaitEvent(c->copy_stream, c->layer_done[(size_t)l], 0));
+    }
+    int32_t* tab = c->slot_tables_host + (size_t)layer * s.n_blk;
+    // the pinned table of this layer may still feed its previous upload
+    LS_HIP(c, hipEventSynchronize(c->table_uploaded[layer]));
+    c->bcache->slot_table(layer, tab);
+    // table upload first: it only changes entries of blocks filled below, which no earlier
+    // compute of this layer reads any more (the copy stream waited for it).
+    LS_HIP(c, hipMemcpyAsync(c->slot_tables + (size_t)layer * s.n_blk, tab, (size_t)s.n_blk * sizeof(int32_t),
+                             hipMemcpyHostToDevice, c->copy_stream));
+    LS_HIP(c, hipEventRecord(c->table_uploaded[layer], c->copy_stream));
+    auto& events = c->stage_events[layer];
+    auto& ranges = c->stage_ranges[layer];
+    while ((int)events.size() < n_stages) {
+        hipEvent_t e;
+        LS_HIP(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        events.push_back(e);
+    }
+    ranges.clear();
+    size_t fi = 0;
+    const uint8_t* layer_host = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+    for (int sidx = 0; sidx < n_stages; ++sidx) {
+        const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);
+        for (; fi < fills.size() && fills[fi].pos < hi; ++fi) {
+            const auto& f = fills[fi];
+            LS_HIP(c, hipMemcpyAsync(c->cache + (size_t)f.slot * c->block_bytes,
+                                     layer_host + (size_t)f.block * c->block_bytes, c->block_bytes,
+                                     hipMemcpyHostToDevice, c->copy_stream));
+            if (copied) copied->push_back(f.block);
+        }
+        LS_HIP(c, hipEventRecord(events[sidx], c->copy_stream));
+        ranges.emplace_back(lo, hi);
+    }
+    c->streamed[layer] = 1;
+    if (stats) {
+        stats->hits = res.hits;
+        stats->misses = res.misses;
+        stats->bytes = (int64_t)res.misses * (int64_t)c->block_bytes;
+        stats->evictions = res.evictions;
+    }
+    return LS_OK;
+}
+
 ls_status ls_stream_weights(ls_ffn* c, int32_t layer, const int32_t* idx_host, int32_t n,
                             int32_t n_stages, ls_stream_stats* stats) {
     ls_status st = check_ctx(c);
@@ -602,54 +690,104 @@ ls_status ls_stream_weights(ls_ffn* c, int32_t layer, const int32_t* idx_host, i
     for (int i = 0; i < n; ++i)
         if (idx_host[i] < 0 || idx_host[i] >= s.n_blk) return fail(c, LS_E_INVAL, "block id out of range");
     if (!c->is_set[layer]) return fail(c, LS_E_STATE, "layer weights not set");
-    ls_stream_stats local{};
     if (c->desc.residency == LS_WEIGHTS_HBM) {
-        local.hits = n;
-        if (stats) *stats = local;
+        if (stats) *stats = ls_stream_stats{n, 0, 0, 0};
         return LS_OK;
     }
-    if (n > c->bcache->slots()) return fail(c, LS_E_CAPACITY, "request exceeds the HBM cache slots");
-    // Slots reassigned by this call may still be read by compute enqueued earlier: the copy
-    // stream first waits for all compute enqueued so far.
-    LS_HIP(c, hipEventRecord(c->compute_done, c->stream));
-    LS_HIP(c, hipStreamWaitEvent(c->copy_stream, c->compute_done, 0));
-    std::vector<ls::BlockCache::Fill> fills;
-    ls::BlockCache::Result res = c->bcache->request(layer, idx_host, n, &fills);
-    if (!res.ok) return fail(c, LS_E_CAPACITY, "cache could not place the request");
-    int32_t* tab = c->slot_tables_host + (size_t)layer * s.n_blk;
-    // the pinned table of this layer may still feed its previous upload
-    LS_HIP(c, hipEventSynchronize(c->table_uploaded[layer]));
-    c->bcache->slot_table(layer, tab);
-    // table upload first: it only changes entries of blocks filled below, which no earlier
-    // compute of this layer reads any more (the copy stream waited for it).
-    LS_HIP(c, hipMemcpyAsync(c->slot_tables + (size_t)layer * s.n_blk, tab, (size_t)s.n_blk * sizeof(int32_t),
-                             hipMemcpyHostToDevice, c->copy_stream));
-    LS_HIP(c, hipEventRecord(c->table_uploaded[layer], c->copy_stream));
-    while ((int)c->stage_events.size() < n_stages) {
-        hipEvent_t e;
-        LS_HIP(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
-        c->stage_events.push_back(e);
-    }
-    c->stage_ranges.clear();
-    size_t fi = 0;
-    const uint8_t* layer_host = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
-    for (int sidx = 0; sidx < n_stages; ++sidx) {
-        const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);
-        for (; fi < fills.size() && fills[fi].pos < hi; ++fi) {
-            const auto& f = fills[fi];
-            LS_HIP(c, hipMemcpyAsync(c->cache + (size_t)f.slot * c->block_bytes,
-                                     layer_host + (size_t)f.block * c->block_bytes, c->block_bytes,
-                                     hipMemcpyHostToDevice, c->copy_stream));
+    return stream_request(c, layer, idx_host, n, n_stages, stats, nullptr);
+}
+
+// Device list -> host: copies n ids after the work queued on the compute stream and waits.
+static ls_status read_list(ls_ffn* c, const int32_t* dev, int32_t n, int32_t* host) {
+    LS_HIP(c, hipMemcpyAsync(host, dev, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+    LS_HIP(c, hipStreamSynchronize(c->stream));
+    return LS_OK;
+}
+
+ls_status ls_decode_step_streamed(ls_ffn* c, float* x, int32_t k, int32_t n_stages, int32_t mode,
+                                  int32_t k_spec, ls_stream_report* report) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    const int L = c->desc.n_layers, nb = s.n_blk;
+    if (!x) return fail(c, LS_E_INVAL, "null pointer");
+    if (c->desc.residency != LS_WEIGHTS_HOST) return fail(c, LS_E_UNSUPPORTED, "needs host-resident weights");
+    if (k < 1 || k > nb) return fail(c, LS_E_INVAL, "k must be in 1..n_blk");
+    if (n_stages < 1) return fail(c, LS_E_INVAL, "n_stages must be >= 1");
+    if (mode < LS_PREFETCH_NONE || mode > LS_PREFETCH_REFINE) return fail(c, LS_E_INVAL, "unknown prefetch mode");
+    if (mode != LS_PREFETCH_NONE && (k_spec < 1 || k_spec > nb)) return fail(c, LS_E_INVAL, "k_spec must be in 1..n_blk");
+    for (int l = 0; l < L; ++l)
+        if (!c->is_set[l]) return fail(c, LS_E_STATE, "layer weights not set");
+    ls_stream_report rep{};
+    const int64_t bb = (int64_t)c->block_bytes;
+    int32_t* fin_h = c->idx_pinned;                      // the current layer's final list
+    int32_t* spec_h[2] = {c->idx_pinned + nb, c->idx_pinned + 2 * (size_t)nb};
+    int32_t* spec_d[2] = {c->spec_idx, c->spec_idx + nb};
+    int32_t* spec_cnt = c->spec_idx + 2 * (size_t)nb;
+    float* cur = x;
+    float* nxt = c->xbuf;
+    std::vector<int32_t> fin((size_t)k), spec_copied;
+    // final list of layer 0
+    if ((st = ls_predict(c, 0, cur, 1, c->scores)) != LS_OK) return st;
+    if ((st = ls_select_blocks(c, c->scores, 1, LS_SEL_TOPK, k, 0.f, 0, k, c->idx, c->count)) != LS_OK) return st;
+    if ((st = read_list(c, c->idx, k, fin_h)) != LS_OK) return st;
+    for (int l = 0; l < L; ++l) {
+        const bool next = l + 1 < L;
+        std::copy(fin_h, fin_h + k, fin.begin());
+        ls_stream_stats ss{};
+        if ((st = stream_request(c, l, fin.data(), k, n_stages, &ss, nullptr)) != LS_OK) return st;
+        rep.final_bytes += (int64_t)k * bb;
+        rep.late_bytes += ss.bytes;
+        spec_copied.clear();
+        // one speculative list of layer l+1 from the device list in spec_d[b]: read back and
+        // request the blocks not yet resident, protecting layer l's blocks (its stages may
+        // still be queued)
+        auto prefetch = [&](int b) -> ls_status {
+            LS_HIP(c, hipEventSynchronize(c->spec_read[b]));
+            ls_stream_stats sp{};
+            ls_status r = stream_request(c, l + 1, spec_h[b], k_spec, 1, &sp, &spec_copied, l);
+            if (r == LS_OK) rep.spec_bytes += sp.bytes;
+            return r;
+        };
+        auto speculate = [&](const float* feat, int b) -> ls_status {
+            ls_status r = ls_predict(c, l + 1, feat, 1, c->scores);
+            if (r == LS_OK) r = ls_select_blocks(c, c->scores, 1, LS_SEL_TOPK, k_spec, 0.f, 0, k_spec, spec_d[b], spec_cnt + b);
+            if (r == LS_OK && (hipMemcpyAsync(spec_h[b], spec_d[b], (size_t)k_spec * sizeof(int32_t),
+                                              hipMemcpyDeviceToHost, c->stream) != hipSuccess ||
+                               hipEventRecord(c->spec_read[b], c->stream) != hipSuccess))
+                r = fail(c, LS_E_DEVICE, "list read-back failed");
+            return r;
+        };
+        if (next && mode == LS_PREFETCH_ONESHOT) {
+            if ((st = speculate(cur, 0)) != LS_OK || (st = prefetch(0)) != LS_OK) return st;
         }
-        LS_HIP(c, hipEventRecord(c->stage_events[sidx], c->copy_stream));
-        c->stage_ranges.emplace_back(lo, hi);
+        int pending = -1;  // a refined list read back but not yet requested
+        for (int j = 0; j < n_stages; ++j) {
+            const int lo = (int)((int64_t)j * k / n_stages), hi = (int)((int64_t)(j + 1) * k / n_stages);
+            if (hi > lo || j == 0)
+                if ((st = ls_sparse_ffn_step(c, l, cur, 1, c->idx, c->count, lo, hi, nxt)) != LS_OK) return st;
+            if (next && mode == LS_PREFETCH_REFINE) {
+                // x~^(j+1) is in nxt: score layer l+1 on it; the list of the previous stage is
+                // requested meanwhile (the host waits for it while this stage runs)
+                if ((st = speculate(nxt, j & 1)) != LS_OK) return st;
+                if (pending >= 0 && (st = prefetch(pending)) != LS_OK) return st;
+                pending = j & 1;
+            }
+        }
+        if (pending >= 0 && (st = prefetch(pending)) != LS_OK) return st;
+        if (next) {
+            // layer l+1's final list from its complete input
+            if ((st = ls_predict(c, l + 1, nxt, 1, c->scores)) != LS_OK) return st;
+            if ((st = ls_select_blocks(c, c->scores, 1, LS_SEL_TOPK, k, 0.f, 0, k, c->idx, c->count)) != LS_OK) return st;
+            if ((st = read_list(c, c->idx, k, fin_h)) != LS_OK) return st;
+            for (int32_t b : spec_copied)
+                if (std::find(fin_h, fin_h + k, b) == fin_h + k) rep.wasted_bytes += bb;
+        }
+        std::swap(cur, nxt);
     }
-    c->pending_layer = layer;
-    local.hits = res.hits;
-    local.misses = res.misses;
-    local.bytes = (int64_t)res.misses * (int64_t)c->block_bytes;
-    local.evictions = res.evictions;
-    if (stats) *stats = local;
+    if (cur != x) LS_HIP(c, hipMemcpyAsync(x, cur, (size_t)s.d * sizeof(float), hipMemcpyDeviceToDevice, c->stream));
+    rep.copied_bytes = rep.late_bytes + rep.spec_bytes;
+    if (report) *report = rep;
     return LS_OK;
 }
 

@@ -109,3 +109,77 @@ def test_entries_not_resident_contribute_nothing():
     y_r = _staged(fr, 0, x, idx4, cnt4, 4, 1)
     assert np.array_equal(host(y_h), host(y_r))
     fh.ls_ffn_sync()
+
+
+# ---- the streamed decode step: one token through every layer with cross-layer prefetch ----
+
+def _replay_resident(fr, x0, k, K):
+    """The same staged computation through the per-layer calls on HBM-resident weights."""
+    L = len(fr_layers(fr))
+    cur = dev_f32(x0)
+    scores = empty_f32(1, CFG.n_blk)
+    idx, cnt = empty_i32(k), empty_i32(1)
+    for l in range(L):
+        fr.ls_predict(l, cur, 1, scores)
+        fr.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, k, 0.0, 0, k, idx, cnt)
+        nxt = _staged(fr, l, cur, idx, cnt, k, K)
+        cur = nxt
+    return host(cur)
+
+
+def fr_layers(f):
+    return range(f.n_layers)
+
+
+@pytest.mark.parametrize("K", [1, 4])
+def test_streamed_step_modes_are_bitwise_equal_to_the_staged_resident_replay(K):
+    fr, fh, ws = _pair()
+    k = CFG.k
+    ref = None
+    for t in range(2):
+        x0 = lsgen.tokens(CFG, 20 + t, 1, 1)[0]
+        ref = _replay_resident(fr, x0, k, K)
+        for mode in (lsffn.LS_PREFETCH_NONE, lsffn.LS_PREFETCH_ONESHOT, lsffn.LS_PREFETCH_REFINE):
+            x = dev_f32(x0)
+            rep = fh.ls_decode_step_streamed(x, k, K, mode, k)
+            assert np.array_equal(host(x), ref), (t, mode)
+            bb = BLOCK_BYTES
+            assert rep.final_bytes == CFG.n_layers * k * bb
+            assert rep.copied_bytes == rep.late_bytes + rep.spec_bytes
+            assert rep.late_bytes % bb == 0 and rep.spec_bytes % bb == 0
+            assert 0 <= rep.wasted_bytes <= rep.spec_bytes
+            if mode == lsffn.LS_PREFETCH_NONE:
+                assert rep.spec_bytes == 0 and rep.wasted_bytes == 0
+    fh.ls_ffn_sync()
+
+
+def test_streamed_step_refined_prefetch_of_the_exact_list_has_no_late_copies():
+    # one stage: the refined feature after the only stage is the layer output itself, so the
+    # prefetched list of layer n+1 is exactly its final list and nothing is copied late after
+    # layer 0 (whose list cannot be known earlier)
+    fr, fh, ws = _pair()
+    k = CFG.k
+    x0 = lsgen.tokens(CFG, 30, 1, 1)[0]
+    x = dev_f32(x0)
+    rep = fh.ls_decode_step_streamed(x, k, 1, lsffn.LS_PREFETCH_REFINE, k)
+    assert rep.wasted_bytes == 0
+    assert rep.late_bytes <= k * BLOCK_BYTES  # layer 0's misses only
+    fh.ls_ffn_sync()
+
+
+def test_streamed_step_errors():
+    fr, fh, ws = _pair()
+    x = dev_f32(lsgen.tokens(CFG, 0, 1, 1)[0])
+    with pytest.raises(lsffn.LsError) as e:
+        fr.ls_decode_step_streamed(x, CFG.k, 2, lsffn.LS_PREFETCH_NONE)  # HBM-resident weights
+    assert e.value.status == lsffn.LS_E_UNSUPPORTED
+    for bad in [dict(k=0, n_stages=1, mode=0), dict(k=CFG.k, n_stages=0, mode=0),
+                dict(k=CFG.k, n_stages=1, mode=3), dict(k=CFG.k, n_stages=1, mode=2, k_spec=0)]:
+        with pytest.raises(lsffn.LsError) as e:
+            fh.ls_decode_step_streamed(x, **bad)
+        assert e.value.status == lsffn.LS_E_INVAL
+    # prefetching next to a protected layer needs room for both lists
+    with pytest.raises(lsffn.LsError) as e:
+        fh.ls_decode_step_streamed(x, CFG.k, 1, lsffn.LS_PREFETCH_ONESHOT, SLOTS - CFG.k + 1)
+    assert e.value.status == lsffn.LS_E_CAPACITY
+    fh.ls_ffn_sync()

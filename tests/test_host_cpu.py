@@ -63,7 +63,7 @@ def bc(tmp_path_factory):
     lib.bc_create.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int]
     lib.bc_destroy.argtypes = [ctypes.c_void_p]
     lib.bc_request.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
-                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
     lib.bc_slot_table.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
     lib.bc_invalidate_layer.argtypes = [ctypes.c_void_p, ctypes.c_int]
     return lib
@@ -74,14 +74,14 @@ class Cache:
         self.lib, self.L, self.n_blk = lib, L, n_blk
         self.h = lib.bc_create(slots, L, n_blk)
 
-    def request(self, layer, blocks):
+    def request(self, layer, blocks, protect=-1):
         b = np.ascontiguousarray(blocks, np.int32)
         counts = np.zeros(3, np.int64)
-        fills = np.zeros(3 * max(1, len(b)), np.int32)
+        fills = np.zeros(4 * max(1, len(b)), np.int32)
         nf = np.zeros(1, np.int32)
         ok = self.lib.bc_request(self.h, layer, b.ctypes.data, len(b), counts.ctypes.data,
-                                 fills.ctypes.data, nf.ctypes.data)
-        return ok, counts.tolist(), fills[:3 * nf[0]].reshape(-1, 3).tolist()
+                                 fills.ctypes.data, nf.ctypes.data, protect)
+        return ok, counts.tolist(), fills[:4 * nf[0]].reshape(-1, 4).tolist()
 
     def table(self, layer):
         t = np.zeros(self.n_blk, np.int32)
@@ -93,12 +93,14 @@ def test_block_cache_accounting_and_lru(bc):
     c = Cache(bc, 4, 2, 10)
     ok, cnt, fills = c.request(0, [3, 1, 4])
     assert ok and cnt == [0, 3, 0]
+    assert all(f[3] == -1 for f in fills)  # empty slots: nothing evicted
     assert [f[:2] for f in fills] == [[0, 3], [1, 1], [2, 4]]  # misses in priority order
     ok, cnt, _ = c.request(0, [1, 5])
     assert ok and cnt == [1, 1, 0]
     # cache full: {3,1,4,5}; LRU order oldest -> newest: 3, 4, 1, 5
     ok, cnt, fills = c.request(1, [7])
     assert ok and cnt == [0, 1, 1]
+    assert fills[0][3] == 0  # the slot it took held a block of layer 0
     t0 = c.table(0)
     assert t0[3] == -1 and t0[1] >= 0 and t0[4] >= 0 and t0[5] >= 0
     # a request never evicts its own blocks, even when they are the least recent
@@ -126,10 +128,27 @@ def test_block_cache_properties_random(bc):
         t = c.table(layer)
         assert all(t[b] >= 0 for b in req)
         assert [f[0] for f in fills] == sorted(f[0] for f in fills)
+        # a fill that evicted reports the layer whose block the slot held
+        assert sum(1 for f in fills if f[3] >= 0) == ev and all(-1 <= f[3] < L for f in fills)
         occupied = [s for l in range(L) for s in c.table(l) if s >= 0]
         assert len(occupied) == len(set(occupied)) <= S
     ok, _, _ = c.request(0, list(range(S + 1)))
     assert not ok  # larger than the cache
+
+
+def test_block_cache_protected_layer_and_failed_request(bc):
+    c = Cache(bc, 5, 3, 10)
+    assert c.request(0, [0, 1, 2])[0]
+    assert c.request(1, [5, 6])[0]          # cache full; layer 0's blocks are the least recent
+    ok, cnt, fills = c.request(2, [7, 8], protect=0)
+    assert ok and cnt == [0, 2, 2] and all(f[3] == 1 for f in fills)  # only layer 1 gave way
+    assert all(c.table(0)[[0, 1, 2]] >= 0)
+    before = [c.table(l).copy() for l in range(3)]
+    ok, _, _ = c.request(1, [3, 4, 9], protect=0)  # 3 misses, 2 takeable slots: refused
+    assert not ok
+    assert all(np.array_equal(c.table(l), before[l]) for l in range(3))  # nothing changed hands
+    ok, cnt, fills = c.request(1, [3, 4, 9])      # without protection it fits
+    assert ok and cnt == [0, 3, 3] and [f[3] for f in fills] == [0, 0, 0]  # the least recent: layer 0
 
 
 def test_block_cache_invalidate(bc):
