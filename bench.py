@@ -161,9 +161,11 @@ def overlap_from_trace(d: str) -> dict:
 
 
 def bench_streaming(args, cfg) -> int:
-    """Host-resident stack: per layer predict -> select -> ls_stream_weights (misses copied from
-    pinned host memory in priority order, in stages) -> staged sparse steps that wait per stage.
-    The HBM cache holds the same fraction of all blocks as the full workload's budget."""
+    """Host-resident stack through ls_decode_step_streamed: per layer predict -> select -> misses
+    copied from pinned host memory in priority order, in stages -> staged sparse steps that wait
+    per stage, with the next layer's blocks prefetched during the current layer (--prefetch:
+    none, one-shot from the layer input, or refined after every stage on the partial result,
+    Eq. 2).  The HBM cache holds the same fraction of all blocks as the full workload's budget."""
     import numpy as np
     import torch
 
@@ -175,7 +177,8 @@ def bench_streaming(args, cfg) -> int:
     cfg = cfg.with_(n_layers=L)
     block_bytes = 3 * cfg.block * cfg.d_model * cfg.elem_bytes
     cache_frac = cfg.hbm_cache_bytes / (full_blocks * block_bytes)
-    slots = max(cfg.k, int(cache_frac * L * cfg.n_blk))
+    # a layer's list and the next layer's prefetched list must fit together
+    slots = max(cfg.k + (args.k_spec or cfg.k), int(cache_frac * L * cfg.n_blk))
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
@@ -191,11 +194,6 @@ def bench_streaming(args, cfg) -> int:
         print(f"set-up: {l + 1}/{L} layers", file=sys.stderr, flush=True)
     W, K, S = args.warmup, args.steps, args.stages
     xs = torch.from_numpy(lsgen.tokens(cfg, 0, W + K, 1)).to(dev)
-    scores = torch.empty(1, cfg.n_blk, dtype=torch.float32, device=dev)
-    idx = torch.empty(cfg.k, dtype=torch.int32, device=dev)
-    cnt = torch.empty(1, dtype=torch.int32, device=dev)
-    xa = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
-    xb = torch.empty_like(xa)
     # pinned host -> HBM peak of one large copy, the ceiling of this path
     src = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
     dst = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -211,37 +209,42 @@ def bench_streaming(args, cfg) -> int:
     del src, dst
     setup_s = time.perf_counter() - t_setup
 
-    totals = {"hits": 0, "misses": 0, "bytes": 0}
+    modes = {"none": lsffn.LS_PREFETCH_NONE, "oneshot": lsffn.LS_PREFETCH_ONESHOT,
+             "refine": lsffn.LS_PREFETCH_REFINE}
+    k_spec = args.k_spec or cfg.k
+    x = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
 
-    def step(x0, count):
-        xa.copy_(x0)
-        cur, nxt = xa, xb
-        for l in range(L):
-            f.ls_predict(l, cur, 1, scores)
-            f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 0, cfg.k, idx, cnt)
-            idx_h = idx.cpu().numpy()  # the host resolves hits and orders the copies
-            st = f.ls_stream_weights(l, idx_h, n_stages=S)
-            if count:
-                totals["hits"] += st.hits
-                totals["misses"] += st.misses
-                totals["bytes"] += st.bytes
-            for s_ in range(S):
-                lo, hi = s_ * cfg.k // S, (s_ + 1) * cfg.k // S
-                if hi > lo or s_ == 0:
-                    f.ls_sparse_ffn_step(l, cur, 1, idx, cnt, lo, hi, nxt)
-            cur, nxt = nxt, cur
-        return cur
+    def run(mode_name):
+        totals = {"final": 0, "late": 0, "spec": 0, "wasted": 0}
+        mode = modes[mode_name]
+        for i in range(W):
+            x.copy_(xs[i])
+            f.ls_decode_step_streamed(x, cfg.k, S, mode, k_spec)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            x.copy_(xs[W + i])
+            r = f.ls_decode_step_streamed(x, cfg.k, S, mode, k_spec)
+            totals["final"] += r.final_bytes
+            totals["late"] += r.late_bytes
+            totals["spec"] += r.spec_bytes
+            totals["wasted"] += r.wasted_bytes
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        totals["bytes"] = totals["late"] + totals["spec"]
+        return wall, totals
 
-    for i in range(W):
-        step(xs[i], False)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        step(xs[W + i], True)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    compare = {}
+    if args.prefetch_compare:
+        for name in modes:
+            w_, t_ = run(name)
+            compare[name] = {"tokens_per_s": round(K / w_, 3),
+                             "copied_GB_per_token": round(t_["bytes"] / K / 1e9, 4),
+                             "late_GB_per_token": round(t_["late"] / K / 1e9, 4),
+                             "relative_loading_redundancy": round(t_["wasted"] / t_["final"], 4)}
+            print(f"prefetch {name}: {compare[name]}", file=sys.stderr, flush=True)
+    wall, totals = run(args.prefetch)
     copy_gbs = totals["bytes"] / wall / 1e9
-    n_req = totals["hits"] + totals["misses"]
     cpu = None
     if args.cpu_tokens > 0:
         cpu = cpu_baseline(cfg, weights, lsgen.tokens(cfg, 0, W + K, 1), min(args.cpu_tokens, W + K))
@@ -253,11 +256,14 @@ def bench_streaming(args, cfg) -> int:
         "config": {"workload": f"{cfg.name}: {L} of 80 layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, "
                                f"block {cfg.block} (k={cfg.k} of {cfg.n_blk}), rank {cfg.rank}, batch 1, "
                                f"host-resident blocks, HBM cache {slots} slots ({100 * cache_frac:.1f}% of "
-                               f"the blocks), {S} copy stages per layer",
+                               f"the blocks), {S} copy stages per layer, prefetch {args.prefetch} "
+                               f"({k_spec} blocks per prediction)",
                    "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)", "decode_path": "kernels"},
-        "streaming": {"hit_rate": round(totals["hits"] / n_req, 4) if n_req else None,
-                      "copied_GB_per_token": round(totals["bytes"] / K / 1e9, 4),
-                      "copy_GBs": round(copy_gbs, 2), "h2d_peak_GBs": round(h2d_gbs, 2)},
+        "streaming": {"copied_GB_per_token": round(totals["bytes"] / K / 1e9, 4),
+                      "late_GB_per_token": round(totals["late"] / K / 1e9, 4),
+                      "relative_loading_redundancy": round(totals["wasted"] / totals["final"], 4),
+                      "copy_GBs": round(copy_gbs, 2), "h2d_peak_GBs": round(h2d_gbs, 2),
+                      "prefetch_modes": compare or None},
         "roofline": {"bound": "host_link", "kernel": "hipMemcpyAsync (pinned host -> HBM)",
                      "achieved": round(copy_gbs, 2), "peak": round(h2d_gbs, 2), "unit": "GB/s",
                      "frac": round(copy_gbs / h2d_gbs, 4), "traffic": None},
@@ -285,6 +291,12 @@ def main() -> int:
                          "device (default; the launch rocprofv3 can trace) or hipLaunchCooperativeKernel")
     ap.add_argument("--stages", type=int, default=8,
                     help="host-resident workloads: copy stages per layer (events the compute waits on)")
+    ap.add_argument("--prefetch", choices=("none", "oneshot", "refine"), default="refine",
+                    help="host-resident workloads: cross-layer prefetch policy of the streamed step")
+    ap.add_argument("--k-spec", type=int, default=0,
+                    help="host-resident workloads: blocks per next-layer prediction (0: k)")
+    ap.add_argument("--prefetch-compare", action="store_true",
+                    help="host-resident workloads: also time every prefetch policy")
     ap.add_argument("--overlap-from-trace", default="", metavar="DIR",
                     help="instead of the benchmark: copy/compute overlap from a rocprofv3 kernel + "
                          "memory-copy trace (csv) in DIR")
