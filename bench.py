@@ -275,6 +275,108 @@ def bench_streaming(args, cfg) -> int:
     return 0
 
 
+def bench_refinement(args, cfg) -> int:
+    """Quality of the next layer's prediction after each of K stages of a layer (Eq. 2), on a
+    workload with a planted predictor: importance ratio and top-10% recall of the predicted
+    next-layer set against that layer's block importance on its complete input (sum over a
+    block's neurons of |a_j| * ||Wd[:, j]||).  The stages run over the priority list and, for
+    comparison, over the same blocks in reverse priority order.  Staged steps, predictions,
+    selections and the all-block activations run in the library; the two ratios are computed
+    on the host from its outputs."""
+    import numpy as np
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    L = args.layers or 4
+    cfg = cfg.with_(n_layers=L)
+    K, k, nb = args.stages, cfg.k, cfg.n_blk
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(0)
+    f = lsffn.Ffn(n_layers=L, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank,
+                  max_batch=1, dtype=cfg.dtype, act=cfg.act, prenorm_rms=int(cfg.prenorm))
+    col = []
+    for l in range(L):
+        w = lsgen.layer_weights(cfg, l)
+        f.ls_ffn_set_layer(l, w)
+        wd = lsgen.decode_bits(w.down, cfg.dtype)
+        col.append(np.sqrt((wd * wd).sum(axis=0)))
+        print(f"set-up: {l + 1}/{L} layers", file=sys.stderr, flush=True)
+    scores = torch.empty(1, nb, dtype=torch.float32, device=dev)
+    idx = torch.empty(k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    sel = torch.empty(k, dtype=torch.int32, device=dev)
+    scnt = torch.empty(1, dtype=torch.int32, device=dev)
+    acc = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
+    full = torch.empty_like(acc)
+    all_blk = torch.arange(nb, dtype=torch.int32, device=dev)
+    all_cnt = torch.tensor([nb], dtype=torch.int32, device=dev)
+    act = torch.empty(cfg.d_ff, dtype=torch.float32, device=dev)
+
+    def next_set(l, feat):
+        f.ls_predict(l, feat, 1, scores)
+        f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, k, 0.0, 0, k, sel, scnt)
+        return sel.cpu().numpy().copy()
+
+    def ratios(imp, P):
+        best = np.sort(imp)[::-1][:len(P)].sum()
+        m = max(1, -(-nb // 10))
+        top = np.lexsort((np.arange(nb), -imp))[:m]
+        return imp[P].sum() / best, np.isin(top, P).sum() / m
+
+    curves = {"priority": np.zeros((K + 1, 2)), "reverse": np.zeros((K + 1, 2))}
+    n_obs = 0
+    xs = torch.from_numpy(lsgen.tokens(cfg, 0, args.steps, 1)).to(dev)
+    t0 = time.perf_counter()
+    for t in range(args.steps):
+        x = xs[t].clone()
+        for n in range(L - 1):
+            f.ls_predict(n, x, 1, scores)
+            f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, k, 0.0, 0, k, idx, cnt)
+            sets = {}
+            for name, lst in (("priority", idx), ("reverse", torch.flip(idx, [0]).contiguous())):
+                sets[name] = [next_set(n + 1, x)]
+                for j in range(K):
+                    f.ls_sparse_ffn_step(n, x, 1, lst, cnt, j * k // K, (j + 1) * k // K, acc)
+                    sets[name].append(next_set(n + 1, acc))
+                if name == "priority":
+                    nxt = acc.clone()
+            # the next layer's block importance on its complete input
+            f.ls_sparse_ffn_step(n + 1, nxt, 1, all_blk, all_cnt, 0, nb, full)
+            f.ls_debug_last_activations(act)
+            a = act.cpu().numpy().astype(np.float64)
+            imp = (np.abs(a) * col[n + 1]).reshape(nb, cfg.block).sum(axis=1)
+            for name in curves:
+                for j, P in enumerate(sets[name]):
+                    curves[name][j] += ratios(imp, P)
+            n_obs += 1
+            x = nxt
+        print(f"token {t + 1}/{args.steps}", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for name in curves:
+        curves[name] /= n_obs
+    out = {
+        "metric": "next-layer importance ratio after refinement stages (Eq. 2), planted predictor",
+        "value": round(float(curves["priority"][K // 2, 0]), 4), "unit": f"ratio after {K // 2}/{K} stages",
+        "n_gpus": 1, "steps": args.steps, "warmup": 0, "ms_per_step": round(1e3 * wall / args.steps, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": lsgen.DTYPE_NAMES[cfg.dtype], "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {L} layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, block "
+                               f"{cfg.block} (k={k} of {nb}), rank {cfg.rank}, {K} stages, "
+                               f"{n_obs} (token, layer) pairs",
+                   "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)"},
+        "refinement": {name: {"importance_ratio": [round(float(v), 4) for v in c[:, 0]],
+                              "top10_recall": [round(float(v), 4) for v in c[:, 1]]}
+                       for name, c in curves.items()},
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -295,6 +397,9 @@ def main() -> int:
                     help="host-resident workloads: cross-layer prefetch policy of the streamed step")
     ap.add_argument("--k-spec", type=int, default=0,
                     help="host-resident workloads: blocks per next-layer prediction (0: k)")
+    ap.add_argument("--refinement-quality", action="store_true",
+                    help="instead of the benchmark: next-layer prediction quality per refinement "
+                         "stage (use with --config llama2_7b_planted)")
     ap.add_argument("--prefetch-compare", action="store_true",
                     help="host-resident workloads: also time every prefetch policy")
     ap.add_argument("--overlap-from-trace", default="", metavar="DIR",
@@ -312,6 +417,9 @@ def main() -> int:
     if args.overlap_from_trace:
         print(json.dumps(overlap_from_trace(args.overlap_from_trace)))
         return 0
+    if args.refinement_quality:
+        import lsgen
+        return bench_refinement(args, lsgen.CONFIGS[args.config])
 
     import numpy as np
     import torch

@@ -30,7 +30,7 @@ DT_F32, DT_F16, DT_BF16 = 0, 1, 2
 DTYPE_NAMES = {DT_F32: "f32", DT_F16: "f16", DT_BF16: "bf16"}
 ACT_REGLU, ACT_SWIGLU_THRESH = 0, 1
 
-TID_GATE, TID_UP, TID_DOWN, TID_P1, TID_P2, TID_TOKEN, TID_CALIB = 1, 2, 3, 5, 6, 7, 8
+TID_GATE, TID_UP, TID_DOWN, TID_P1, TID_P2, TID_TOKEN, TID_CALIB, TID_SPREAD = 1, 2, 3, 5, 6, 7, 8, 9
 
 
 def build(force: bool = True) -> str:
@@ -98,6 +98,17 @@ def const(shape, value: float, dtype: int) -> np.ndarray:
     return out
 
 
+def to_storage(a: np.ndarray, dtype: int) -> np.ndarray:
+    """fp32 values rounded to nearest-even in a storage type (finite inputs)."""
+    a = np.ascontiguousarray(a, np.float32)
+    if dtype == DT_F32:
+        return a
+    if dtype == DT_F16:
+        return a.astype(np.float16)
+    bits = a.view(np.uint32).astype(np.uint64)
+    return ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16).astype(np.uint16)
+
+
 def splitmix64(seed: int, n: int) -> int:
     return int(_load().lsgen_splitmix64(seed, n))
 
@@ -136,6 +147,12 @@ class Config:
     hbm_cache_bytes: int = 0
     seed: int = BASE_SEED
     note: str = ""
+    # "random": predictor factors independent of the FFN weights.  "planted": the gate rows of
+    # block b share a direction C_b (rows (C_b + spread_i) B / sqrt(r) + noise), and the
+    # predictor is P1 = B, P2 = C / sqrt(r): its block score is the shared part of the block's
+    # gate pre-activations, so it ranks blocks by expected activity (a trained predictor's role).
+    predictor: str = "random"
+    down_gain: float = 1.0   # down-projection std = down_gain / sqrt(d_model)
 
     @property
     def n_blk(self) -> int:
@@ -174,11 +191,21 @@ CONFIGS = {
     # Llama-2-13B-shaped FFN stack, fp16, ~10% active, batched decode with a block union.
     "llama2_13b_ffn": Config("llama2_13b_ffn", 40, 5120, 13824, DT_F16, ACT_REGLU, 64, 1280, 12,
                              -_probit(0.90), True, 256, batches=(1, 2, 4, 8)),
+    # Llama-2-7B-shaped FFN stack with a planted predictor (gate rows of a block share a
+    # direction the predictor knows), for the quality of refined next-layer predictions.
+    "llama2_7b_planted": Config("llama2_7b_planted", 32, 4096, 11008, DT_F16, ACT_REGLU, 64, 1024, 12,
+                                -_probit(0.90), True, 64, predictor="planted"),
     # Llama-2-70B-shaped FFN stack, weights in pinned host memory, 16 GiB HBM block cache.
     "llama2_70b_stream": Config("llama2_70b_stream", 80, 8192, 28672, DT_F16, ACT_REGLU, 128, 2048,
                                 10, -_probit(0.92), True, 64, host_resident=True,
                                 hbm_cache_bytes=16 << 30),
 }
+
+
+# planted predictor: per-neuron spread of the shared block direction, and the gate noise (both
+# relative to the unit shared part)
+PLANT_SPREAD = 0.5
+PLANT_NOISE = 0.5
 
 
 @dataclass
@@ -203,12 +230,24 @@ def layer_weights(cfg: Config, layer: int, threshold: float | None = None) -> La
     P2 ~ N(0, 1/rank); constant gate bias when the config has one."""
     d, F, r, nb, dt, s = cfg.d_model, cfg.d_ff, cfg.rank, cfg.n_blk, cfg.dtype, cfg.seed
     sd = 1.0 / math.sqrt(d)
-    gate = normal((F, d), seed=s, tensor_id=TID_GATE, layer=layer, std=sd, dtype=dt)
     up = normal((F, d), seed=s, tensor_id=TID_UP, layer=layer, std=sd, dtype=dt)
-    down = normal((d, F), seed=s, tensor_id=TID_DOWN, layer=layer, std=sd, dtype=dt)
+    down = normal((d, F), seed=s, tensor_id=TID_DOWN, layer=layer, std=cfg.down_gain * sd, dtype=dt)
     bias = const((F,), cfg.gate_bias, dt) if cfg.gate_bias is not None else None
-    p1 = normal((r, d), seed=s, tensor_id=TID_P1, layer=layer, std=sd, dtype=dt)
-    p2 = normal((nb, r), seed=s, tensor_id=TID_P2, layer=layer, std=1.0 / math.sqrt(r), dtype=dt)
+    if cfg.predictor == "planted":
+        B = normal((r, d), seed=s, tensor_id=TID_P1, layer=layer, std=sd, dtype=DT_F32)
+        C = normal((nb, r), seed=s, tensor_id=TID_P2, layer=layer, std=1.0, dtype=DT_F32)
+        A = normal((F, r), seed=s, tensor_id=TID_SPREAD, layer=layer, std=PLANT_SPREAD, dtype=DT_F32)
+        A += np.repeat(C, cfg.block, axis=0)
+        A *= np.float32(1.0 / math.sqrt(r))
+        G = normal((F, d), seed=s, tensor_id=TID_GATE, layer=layer, std=PLANT_NOISE * sd, dtype=DT_F32)
+        G += A @ B
+        gate = to_storage(G, dt)
+        p1 = to_storage(B, dt)
+        p2 = to_storage(C * np.float32(1.0 / math.sqrt(r)), dt)
+    else:
+        gate = normal((F, d), seed=s, tensor_id=TID_GATE, layer=layer, std=sd, dtype=dt)
+        p1 = normal((r, d), seed=s, tensor_id=TID_P1, layer=layer, std=sd, dtype=dt)
+        p2 = normal((nb, r), seed=s, tensor_id=TID_P2, layer=layer, std=1.0 / math.sqrt(r), dtype=dt)
     t = cfg.swiglu_threshold if threshold is None else threshold
     return LayerWeights(gate, up, down, bias, p1, p2, t)
 

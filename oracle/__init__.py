@@ -270,3 +270,62 @@ def _decoded_matrix(a: np.ndarray) -> np.ndarray:
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     return a.astype(np.float64)
+
+
+# ---- quality of the refined next-layer prediction (Sec. 6, the refinement-step validation) ----
+#
+# The paper measures, after each of K priority-ordered stages of a layer, how well the next
+# layer's prediction on the refined feature x~^(j) (Eq. 2) captures that layer's important
+# blocks: the importance ratio (importance captured by the predicted set, normalised by the
+# most a set of the same size can capture) and the top-10% recall.  Block importance is read
+# here as the size of the blocks' contribution to the output: sum over its neurons of
+# |a_j| * ||Wd[:, j]||_2 on the layer's complete input.
+
+def block_importance(w, h: np.ndarray, block: int, act: int, thresh: float = 0.0) -> np.ndarray:
+    """Importance of every block of a layer on input h (float64 [n_blk])."""
+    F = w.gate.shape[0]
+    _, _, a = activations(w, h, np.arange(F, dtype=np.int32), act, thresh)
+    wd = _decoded_matrix(_c(w.down))
+    col = np.sqrt((wd * wd).sum(axis=0))
+    return (np.abs(a) * col).reshape(F // block, block).sum(axis=1)
+
+
+def importance_ratio(imp: np.ndarray, predicted) -> float:
+    """Importance of the predicted blocks over the largest importance of as many blocks."""
+    predicted = np.asarray(predicted, np.int64)
+    best = np.sort(np.asarray(imp, np.float64))[::-1][:predicted.size].sum()
+    return float(imp[predicted].sum() / best) if best > 0 else 1.0
+
+
+def top_fraction_recall(imp: np.ndarray, predicted, frac: float = 0.1) -> float:
+    """Share of the ceil(frac * n_blk) most important blocks (ties to the smaller index) that
+    the predicted set holds."""
+    n = imp.shape[0]
+    m = max(1, math.ceil(frac * n))
+    top = np.lexsort((np.arange(n), -np.asarray(imp, np.float64)))[:m]
+    return float(np.isin(top, np.asarray(predicted)).sum() / m)
+
+
+def refinement_quality(w_n, w_next, cfg, x: np.ndarray, K: int, order=None, k: int | None = None):
+    """Per stage j = 0..K of layer n (j = 0: the one-shot prediction from x), the next layer's
+    top-k on the refined feature x~^(j) (Eq. 2) and its (importance ratio, top-10% recall)
+    against the next layer's block importance on the complete output x~^(K).  The stages run
+    over layer n's priority list, or over list[order] for another order of the same blocks.
+
+    Returns (metrics [(ratio, recall)] * (K+1), predicted sets, refined features)."""
+    k = cfg.k if k is None else k
+    h = mlp_input(x, cfg.prenorm)
+    s = predict(w_n.p1, w_n.p2, h)
+    idx = select(s, k=k, cap=k)[0][0]
+    lst = idx if order is None else idx[np.asarray(order)]
+    _, xt = staged_ffn(w_n, x, h, lst, cfg.block, K, cfg.act, w_n.threshold)
+    feats = [np.asarray(x, np.float32)] + [f.astype(np.float32) for f in xt]
+    imp = block_importance(w_next, mlp_input(feats[-1], cfg.prenorm), cfg.block, cfg.act,
+                           w_next.threshold)
+    out, sets = [], []
+    for f in feats:
+        sc = predict(w_next.p1, w_next.p2, mlp_input(f, cfg.prenorm))
+        P = select(sc, k=k, cap=k)[0][0]
+        sets.append(P)
+        out.append((importance_ratio(imp, P), top_fraction_recall(imp, P)))
+    return out, sets, feats

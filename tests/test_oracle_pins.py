@@ -410,8 +410,8 @@ def test_generator_rounding_to_storage_types():
 
 def test_workload_constants():
     cfgs = lsgen.CONFIGS
-    assert [c.k for c in cfgs.values()] == [10, 21, 56, 26, 23]
-    assert [c.n_blk for c in cfgs.values()] == [48, 172, 112, 216, 224]
+    assert [c.k for c in cfgs.values()] == [10, 21, 56, 26, 21, 23]
+    assert [c.n_blk for c in cfgs.values()] == [48, 172, 112, 216, 172, 224]
     from statistics import NormalDist
     assert NormalDist().cdf(cfgs["llama2_7b_ffn"].gate_bias) == pytest.approx(0.10, abs=1e-12)
     assert NormalDist().cdf(cfgs["llama2_70b_stream"].gate_bias) == pytest.approx(0.08, abs=1e-12)
@@ -449,3 +449,74 @@ def test_swiglu_threshold_gives_half_sparsity():
     w = lsgen.layer_weights(cfg, 0)
     t_emp = oracle.calibrate_threshold(w, cfg, lsgen.calib_tokens(cfg, 0), 0.5)
     assert t_emp == pytest.approx(cfg.swiglu_threshold, rel=0.05)
+
+
+# ------------------------------------------------------ refinement quality (Sec. 6 validation)
+
+def test_importance_ratio_brute_force_small():
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        n = int(rng.integers(2, 8))
+        imp = rng.random(n) * rng.integers(0, 2, n)  # some zero importances
+        m = int(rng.integers(1, n + 1))
+        P = rng.choice(n, m, replace=False)
+        best = max(sum(imp[list(c)]) for c in itertools.combinations(range(n), m))
+        expect = imp[P].sum() / best if best > 0 else 1.0
+        assert math.isclose(oracle.importance_ratio(imp, P), expect, rel_tol=1e-12)
+    imp = np.array([3.0, 1.0, 2.0])
+    assert oracle.importance_ratio(imp, [0, 2]) == 1.0  # the best set of two
+
+
+def test_top_fraction_recall_definition():
+    imp = np.array([5.0, 1.0, 5.0, 0.0, 2.0, 9.0, 0.5, 0.5, 0.5, 7.0, 4.0])  # n = 11: top 2
+    # top two by importance: 5 (9.0), 9 (7.0)
+    assert oracle.top_fraction_recall(imp, [5, 9, 0]) == 1.0
+    assert oracle.top_fraction_recall(imp, [5, 1]) == 0.5
+    assert oracle.top_fraction_recall(imp, [1, 2]) == 0.0
+    # ties go to the smaller index: top 3 of [1,1,1,1] at frac 0.75 is {0,1,2}
+    assert oracle.top_fraction_recall(np.ones(4), [0, 1, 2], frac=0.75) == 1.0
+    assert oracle.top_fraction_recall(np.ones(4), [3], frac=0.75) == 0.0
+
+
+def test_block_importance_invariants():
+    cfg, w = _small_layer(bias=-0.2)
+    x = lsgen.tokens(cfg, 0, 1, 1)[0, 0]
+    h = oracle.mlp_input(x, cfg.prenorm)
+    imp = oracle.block_importance(w, h, cfg.block, cfg.act)
+    assert imp.shape == (cfg.n_blk,) and np.all(imp >= 0)
+    # scaling the down projection by c scales every importance by |c| (c = -2: exact in fp32)
+    w2 = SimpleNamespace(**{**w.__dict__, "down": (w.down * np.float32(-2.0)).astype(w.down.dtype)})
+    assert np.allclose(oracle.block_importance(w2, h, cfg.block, cfg.act), 2 * imp, rtol=1e-12)
+    # permuting the neurons within a block (gate, up rows, down columns, bias together) keeps
+    # the block's importance (Sec. 3.2.2)
+    perm = np.arange(cfg.d_ff).reshape(cfg.n_blk, cfg.block)[:, ::-1].reshape(-1)
+    w3 = SimpleNamespace(gate=w.gate[perm], up=w.up[perm], down=np.ascontiguousarray(w.down[:, perm]),
+                         bias=None if w.bias is None else w.bias[perm], threshold=w.threshold)
+    assert np.allclose(oracle.block_importance(w3, h, cfg.block, cfg.act), imp, rtol=1e-12)
+    # a block whose neurons are all inactive has no importance: ReLU(g) = 0 for g + b <= 0
+    _, _, a = oracle.activations(w, h, np.arange(cfg.d_ff, dtype=np.int32), cfg.act)
+    dead = np.all(a.reshape(cfg.n_blk, cfg.block) == 0, axis=1)
+    assert np.all(imp[dead] == 0) and np.all(imp[~dead] > 0)
+
+
+def test_refinement_last_stage_is_the_complete_output_prediction():
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(n_layers=2, d_model=256, d_ff=1024, block=32, rank=64,
+                                               dtype=lsgen.DT_F32, predictor="planted")
+    ws = [lsgen.layer_weights(cfg, l) for l in range(2)]
+    x = lsgen.tokens(cfg, 0, 1, 1)[0, 0]
+    q1, s1, f1 = oracle.refinement_quality(ws[0], ws[1], cfg, x, 1)
+    q4, s4, f4 = oracle.refinement_quality(ws[0], ws[1], cfg, x, 4)
+    # stage 0 is the one-shot prediction from x in both; the last stage sees the whole output
+    # (Eq. 2 with j = K equals the complete layer), whatever the number of stages
+    assert np.array_equal(s1[0], s4[0]) and np.array_equal(f1[0], f4[0])
+    assert _rel(f1[-1], f4[-1]) < 1e-6
+    h = oracle.mlp_input(x, cfg.prenorm)
+    idx = oracle.select(oracle.predict(ws[0].p1, ws[0].p2, h), k=cfg.k, cap=cfg.k)[0][0]
+    full = x.astype(np.float64) + oracle.sparse_ffn(ws[0], h, idx, cfg.block, cfg.act)
+    assert _rel(f4[-1], full) < 1e-6
+    # the prediction on the complete output scored against the importance on that same output
+    # is what a stage-K refinement reports; a random predictor order is not pinned here
+    assert all(0.0 <= r <= 1.0 and 0.0 <= c <= 1.0 for r, c in q4)
+    # the reverse order visits the same blocks: same complete output
+    q4r, s4r, f4r = oracle.refinement_quality(ws[0], ws[1], cfg, x, 4, order=np.arange(cfg.k)[::-1])
+    assert _rel(f4r[-1], f4[-1]) < 1e-6 and np.array_equal(s4r[-1], s4[-1])
