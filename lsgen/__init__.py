@@ -31,6 +31,7 @@ DTYPE_NAMES = {DT_F32: "f32", DT_F16: "f16", DT_BF16: "bf16"}
 ACT_REGLU, ACT_SWIGLU_THRESH = 0, 1
 
 TID_GATE, TID_UP, TID_DOWN, TID_P1, TID_P2, TID_TOKEN, TID_CALIB, TID_SPREAD = 1, 2, 3, 5, 6, 7, 8, 9
+TID_HASH_W1, TID_HASH_WBIN, TID_HASH_TABLES, TID_HASH_HEAD = 10, 11, 12, 13
 
 
 def build(force: bool = True) -> str:
@@ -288,3 +289,41 @@ def adversarial_scores(rng: np.random.Generator, B: int, n_blk: int, kind: str) 
     else:
         raise ValueError(kind)
     return np.ascontiguousarray(s, dtype=np.float32)
+
+
+@dataclass
+class HashWeights:
+    """A stacked hashing predictor (5 layers, 8 hash bits, 256-wide binary features).
+
+    w1: fp32 [d_model, 8] real hyperplanes of the first layer; w_bin: uint32 [4, 8, 8] binary
+    hyperplanes of layers 2..5 (hash bit b's 256 signs, bit-packed, 1 = +1); tables: uint32
+    [4, 256, 8] feature tables T_1..T_4 (bucket i's 256 signs, bit-packed); head: uint8
+    [256, n_blk] block-priority levels of the final bucket."""
+    w1: np.ndarray
+    w_bin: np.ndarray
+    tables: np.ndarray
+    head: np.ndarray
+
+
+def _sign_bits(shape_words, *, seed, tensor_id, layer) -> np.ndarray:
+    """Random {-1,+1} vectors, bit-packed: bit j of word m is set iff element 32m + j of the
+    stream is >= 0 (a fair coin per element)."""
+    n_words = int(np.prod(shape_words))
+    z = normal((n_words * 32,), seed=seed, tensor_id=tensor_id, layer=layer, std=1.0, dtype=DT_F32)
+    bits = (z >= 0).reshape(n_words, 32).astype(np.uint64)
+    words = (bits << np.arange(32, dtype=np.uint64)[None, :]).sum(axis=1).astype(np.uint32)
+    return words.reshape(shape_words)
+
+
+def hash_weights(cfg: Config, layer: int) -> HashWeights:
+    """Random (untrained) weights of the hashing predictor of one layer: N(0, 1) first-layer
+    hyperplanes, fair-coin signs elsewhere, and head levels uniform on 0..255 (8-bit
+    equal-probability quantisation of an N(0, 1) draw)."""
+    s = cfg.seed
+    w1 = normal((cfg.d_model, 8), seed=s, tensor_id=TID_HASH_W1, layer=layer, std=1.0, dtype=DT_F32)
+    w_bin = _sign_bits((4, 8, 8), seed=s, tensor_id=TID_HASH_WBIN, layer=layer)
+    tables = _sign_bits((4, 256, 8), seed=s, tensor_id=TID_HASH_TABLES, layer=layer)
+    z = normal((256, cfg.n_blk), seed=s, tensor_id=TID_HASH_HEAD, layer=layer, std=1.0, dtype=DT_F32)
+    u = 0.5 * (1.0 + np.vectorize(math.erf)(z.astype(np.float64) / math.sqrt(2.0)))
+    head = np.minimum(np.floor(u * 256.0), 255).astype(np.uint8)
+    return HashWeights(w1, w_bin, tables, head)

@@ -11,6 +11,8 @@ gives them:
 * Sec. 3.2.2: the FFN output as a sum over hidden neurons, in any order.
 * Sec. 3.3.3: predictor = a linear input projection (PCA role), here followed
   by a linear head that scores neuron blocks (a reading, see the design notes).
+* Sec. 3.3.1: stacked learnable hashing at inference (Eq. hash_layer,
+  Eq. hashfunc_layer), as an alternative block scorer.
 
 Every function here is pinned by a ``-m "not gpu"`` test; none is "parity
 unpinned".
@@ -73,6 +75,8 @@ def _load():
         lib.orc_layer_step.argtypes = [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _D, _I,
                                        _I, _P, _P, _P, _P, _P]
         lib.orc_layer_step.restype = _I
+        lib.orc_hash_predict.argtypes = [_I, _I, _P, _P, _P, _P, _P, _P, _P]
+        lib.orc_hash_predict.restype = None
         _lib = lib
     return _lib
 
@@ -329,3 +333,25 @@ def refinement_quality(w_n, w_next, cfg, x: np.ndarray, K: int, order=None, k: i
         sets.append(P)
         out.append((importance_ratio(imp, P), top_fraction_recall(imp, P)))
     return out, sets, feats
+
+
+# ---- stacked learnable hashing (Sec. 3.3.1) ----
+
+HASH_TAU, HASH_DH, HASH_LAYERS = 8, 256, 5
+
+
+def hash_predict(hw, x: np.ndarray, n_blk: int):
+    """Block scores of the stacked hashing predictor for one token (fp32 [n_blk]) and the five
+    bucket indices.  ``hw`` has .w1 (fp32 [d, 8]), .w_bin (uint32 [4, 8, 8]), .tables (uint32
+    [4, 256, 8]), .head (uint8 [256, n_blk])."""
+    x = _c(x, np.float32)
+    w1, wb, tb, hd = _c(hw.w1, np.float32), _c(hw.w_bin, np.uint32), _c(hw.tables, np.uint32), \
+        _c(hw.head, np.uint8)
+    d = x.shape[0]
+    assert w1.shape == (d, HASH_TAU) and wb.shape == (4, HASH_TAU, HASH_DH // 32)
+    assert tb.shape == (4, HASH_DH, HASH_DH // 32) and hd.shape == (HASH_DH, n_blk)
+    codes = np.zeros(HASH_LAYERS, np.int32)
+    scores = np.empty(n_blk, np.float32)
+    _load().orc_hash_predict(d, n_blk, x.ctypes.data, w1.ctypes.data, wb.ctypes.data, tb.ctypes.data,
+                             hd.ctypes.data, codes.ctypes.data, scores.ctypes.data)
+    return scores, codes

@@ -321,3 +321,68 @@ int orc_layer_step(int d, int F, int r, int blk, const void* wg, const void* wu,
     free(h);
     return count;
 }
+
+/* ---------------------------------------------------------------------------
+ * Stacked learnable hashing, inference (Sec. 3.3.1, Eq. hash_layer and
+ * Eq. hashfunc_layer): five hashing layers, tau = 8 hash bits each, binary
+ * features of width 256 between them.
+ *
+ *   layer 1:    c = sign(x W_1), W_1 real [d][8]
+ *   layers 2-5: c = sign(x_k W_k), x_k and W_k in {-1,+1}, the product as
+ *               XNOR + bitcount: x.w = 256 - 2 * popcount(x XOR w)
+ *   index i = phi(c): the code read as an 8-bit number, first hash bit most
+ *               significant, +1 -> 1 (the sign-pattern enumeration of the
+ *               paper's matrix Z, Eq. hashfunc_mod)
+ *   y_k = T_k[i] for k = 1..4; the last layer's index selects a row of the
+ *   block-priority head (a reading: a regression output per block, quantised
+ *   to 8-bit levels), which gives the block scores.
+ * sign(0) = +1.  Bit-packed {-1,+1} vectors: element e is bit (e & 31) of word
+ * e >> 5, 1 meaning +1.
+ *
+ * The first layer's code is a floating-point decision, so it is taken in the
+ * GPU kernel's precision and order (binary32 fused multiply-adds): for each
+ * hash bit, 256 partial sums over j = t, t + 256, ... in increasing j, then
+ * the pairwise halving sum p[t] += p[t + s] for s = 128, 64, ..., 1.
+ * ------------------------------------------------------------------------- */
+enum { ORC_TAU = 8, ORC_DH = 256, ORC_DHW = ORC_DH / 32, ORC_NLAYERS = 5 };
+
+static int popcount32(uint32_t v) {
+    int c = 0;
+    while (v) {
+        v &= v - 1;
+        ++c;
+    }
+    return c;
+}
+
+/* codes[5]: the five bucket indices; scores[nblk] = head[codes[4]][b]. */
+void orc_hash_predict(int d, int nblk, const float* x, const float* w1, const uint32_t* w_bin,
+                      const uint32_t* tables, const uint8_t* head, int* codes, float* scores) {
+    int idx = 0;
+    for (int b = 0; b < ORC_TAU; ++b) {
+        float p[ORC_DH];
+        for (int t = 0; t < ORC_DH; ++t) {
+            float acc = 0.f;
+            for (int j = t; j < d; j += ORC_DH) acc = fmaf(x[j], w1[(size_t)j * ORC_TAU + b], acc);
+            p[t] = acc;
+        }
+        for (int s = ORC_DH / 2; s >= 1; s /= 2)
+            for (int t = 0; t < s; ++t) p[t] = p[t] + p[t + s];
+        idx = 2 * idx + (p[0] >= 0.f ? 1 : 0);
+    }
+    codes[0] = idx;
+    for (int k = 1; k < ORC_NLAYERS; ++k) {
+        const uint32_t* y = tables + ((size_t)(k - 1) * ORC_DH + (size_t)idx) * ORC_DHW; /* y_k = T_k[i] */
+        int next = 0;
+        for (int b = 0; b < ORC_TAU; ++b) {
+            const uint32_t* w = w_bin + ((size_t)(k - 1) * ORC_TAU + b) * ORC_DHW;
+            int mismatch = 0;
+            for (int m = 0; m < ORC_DHW; ++m) mismatch += popcount32(y[m] ^ w[m]);
+            const int dot = ORC_DH - 2 * mismatch;
+            next = 2 * next + (dot >= 0 ? 1 : 0);
+        }
+        idx = next;
+        codes[k] = idx;
+    }
+    for (int b = 0; b < nblk; ++b) scores[b] = (float)head[(size_t)idx * nblk + b];
+}

@@ -520,3 +520,76 @@ def test_refinement_last_stage_is_the_complete_output_prediction():
     # the reverse order visits the same blocks: same complete output
     q4r, s4r, f4r = oracle.refinement_quality(ws[0], ws[1], cfg, x, 4, order=np.arange(cfg.k)[::-1])
     assert _rel(f4r[-1], f4[-1]) < 1e-6 and np.array_equal(s4r[-1], s4[-1])
+
+
+# ------------------------------------------------------ stacked learnable hashing (Sec. 3.3.1)
+
+def _unpack_signs(words):
+    """bit-packed {-1,+1} vectors (uint32, last axis words) -> int64 arrays of +-1"""
+    w = np.asarray(words, np.uint64)
+    bits = (w[..., None] >> np.arange(32, dtype=np.uint64)) & 1
+    return (2 * bits.reshape(*w.shape[:-1], -1).astype(np.int64) - 1)
+
+
+def _Z(tau=8):
+    """The paper's sign-pattern matrix: row i enumerates the patterns in the order of its
+    example, (-1,...,-1), (-1,...,-1,+1), ..., (+1,...,+1) (Eq. hashfunc_mod)."""
+    return np.array(list(itertools.product([-1, 1], repeat=tau)), np.int64)
+
+
+def _hash_ref(hw, x, n_blk):
+    """Independent reading: fp64 first layer, +-1 integer products after it, and the index
+    as argmax_i Z[i] . code (Eq. hashfunc_mod) instead of a bit packing."""
+    Z = _Z()
+    dots = np.asarray(x, np.float64) @ hw.w1.astype(np.float64)
+    code = np.where(dots >= 0, 1, -1)
+    idx = [int(np.argmax(Z @ code))]
+    T, W = _unpack_signs(hw.tables), _unpack_signs(hw.w_bin)     # [4,256,256], [4,8,256]
+    for k in range(4):
+        y = T[k, idx[-1]]
+        code = np.where(W[k] @ y >= 0, 1, -1)
+        idx.append(int(np.argmax(Z @ code)))
+    return hw.head[idx[-1]].astype(np.float32), np.array(idx), dots
+
+
+def test_hash_index_is_the_papers_sign_pattern_enumeration():
+    # tau = 3 example of the paper: row 1 of Z is (-1, -1, +1), row 6 is (+1, +1, -1)
+    Z3 = _Z(3)
+    assert Z3[1].tolist() == [-1, -1, 1] and Z3[6].tolist() == [1, 1, -1]
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(d_model=256, d_ff=1024, block=64)
+    hw = lsgen.hash_weights(cfg, 0)
+    Z = _Z()
+    for j in range(0, 256, 37):  # one-hot inputs: layer 1's code is the sign pattern of W1[j]
+        x = np.zeros(256, np.float32)
+        x[j] = 1.0
+        _, codes = oracle.hash_predict(hw, x, cfg.n_blk)
+        code = np.where(hw.w1[j] >= 0, 1, -1)
+        assert codes[0] == int(np.argmax(Z @ code))
+    # x = 0: every product is 0 and sign(0) = +1, the all-plus bucket
+    _, codes = oracle.hash_predict(hw, np.zeros(256, np.float32), cfg.n_blk)
+    assert codes[0] == 255
+
+
+def test_hash_stack_matches_integer_products_and_argmax_reading():
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(d_model=1024, d_ff=4096, block=64)
+    rng = np.random.default_rng(11)
+    for layer in range(3):
+        hw = lsgen.hash_weights(cfg, layer)
+        for _ in range(20):
+            x = rng.standard_normal(1024).astype(np.float32)
+            s, codes = oracle.hash_predict(hw, x, cfg.n_blk)
+            s_ref, idx_ref, dots = _hash_ref(hw, x, cfg.n_blk)
+            # the fp32 first layer agrees with fp64 away from ties
+            assert np.min(np.abs(dots)) > 1e-3
+            assert codes.tolist() == idx_ref.tolist()
+            assert np.array_equal(s, s_ref)
+            assert np.array_equal(s, hw.head[codes[-1]].astype(np.float32))
+
+
+def test_hash_xnor_popcount_equals_signed_product():
+    rng = np.random.default_rng(5)
+    a = rng.integers(0, 2**32, size=(50, 8), dtype=np.uint64).astype(np.uint32)
+    b = rng.integers(0, 2**32, size=(50, 8), dtype=np.uint64).astype(np.uint32)
+    pa, pb = _unpack_signs(a), _unpack_signs(b)
+    mism = np.array([sum(bin(int(x) ^ int(y)).count("1") for x, y in zip(ra, rb)) for ra, rb in zip(a, b)])
+    assert np.array_equal((pa * pb).sum(axis=1), 256 - 2 * mism)
