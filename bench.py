@@ -377,6 +377,62 @@ def bench_refinement(args, cfg) -> int:
     return 0
 
 
+def bench_hash(args, cfg) -> int:
+    """Latency of the stacked hashing predictor (one workgroup per token) against the low-rank
+    predictor (the folded GEMV) on the same shape, per call, from the library's HIP-event
+    kernel timing, at B = 1 and B = args.batch."""
+    import numpy as np  # noqa: F401
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    Bmax = max(1, args.batch)
+    cfg = cfg.with_(n_layers=1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(0)
+    f = lsffn.Ffn(n_layers=1, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank,
+                  max_batch=Bmax, dtype=cfg.dtype, act=cfg.act, prenorm_rms=int(cfg.prenorm))
+    f.ls_ffn_set_layer(0, lsgen.layer_weights(cfg, 0))
+    f.ls_set_hash_predictor(0, lsgen.hash_weights(cfg, 0))
+    xs = torch.from_numpy(lsgen.tokens(cfg, 0, 1, Bmax)[0]).to(dev)
+    scores = torch.empty(Bmax, cfg.n_blk, dtype=torch.float32, device=dev)
+    res = {}
+    for B in sorted({1, Bmax}):
+        for name, call, kid in (("hash", lambda: f.ls_hash_predict(0, xs, B, scores), lsffn.LS_K_HASH),
+                                ("lowrank", lambda: f.ls_predict(0, xs, B, scores), lsffn.LS_K_PRED_P1)):
+            for _ in range(args.warmup):
+                call()
+            f.ls_set_kernel_timing(1)
+            f.ls_kernel_timing(kid, reset=True)
+            for _ in range(args.steps):
+                call()
+            ms, n = f.ls_kernel_timing(kid)
+            f.ls_set_kernel_timing(0)
+            res[f"{name}_B{B}_us"] = round(1e3 * ms / max(n, 1), 3)
+    # bytes one hashing call must read: x, the first layer's hyperplanes, the four binary layers'
+    # rows and hyperplanes, the head row, the scores written
+    hash_bytes = lambda B: B * (4 * cfg.d_model + 4 * cfg.n_blk) + 32 * cfg.d_model + 4 * (32 + 256) + cfg.n_blk
+    us1 = res["hash_B1_us"]
+    out = {
+        "metric": "stacked hashing predictor latency per call (Sec. 3.3.1), 1 GPU",
+        "value": us1, "unit": "us per call (B = 1)", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(us1 / 1e3, 6), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32 (first layer), binary", "data": "synthetic",
+        "config": {"workload": f"{cfg.name} layer shape: d_model {cfg.d_model}, {cfg.n_blk} blocks; 5 hashing "
+                               f"layers, 8 bits, 256-wide; random weights", "global_batch": Bmax,
+                   "seq_len": 1, "parallelism": "none (1 GPU)"},
+        "latency_us": res,
+        "roofline": {"bound": "latency", "kernel": "hash_predict", "achieved": round(hash_bytes(1) / us1 / 1e3, 3),
+                     "peak": 8000.0, "unit": "GB/s", "frac": round(hash_bytes(1) / us1 / 1e3 / 8000.0, 6),
+                     "traffic": None, "bytes_per_launch": hash_bytes(1)},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -397,6 +453,9 @@ def main() -> int:
                     help="host-resident workloads: cross-layer prefetch policy of the streamed step")
     ap.add_argument("--k-spec", type=int, default=0,
                     help="host-resident workloads: blocks per next-layer prediction (0: k)")
+    ap.add_argument("--hash-predict", action="store_true",
+                    help="instead of the benchmark: latency of the stacked hashing predictor against the "
+                         "low-rank predictor (B = 1 and --batch)")
     ap.add_argument("--refinement-quality", action="store_true",
                     help="instead of the benchmark: next-layer prediction quality per refinement "
                          "stage (use with --config llama2_7b_planted)")
@@ -420,6 +479,9 @@ def main() -> int:
     if args.refinement_quality:
         import lsgen
         return bench_refinement(args, lsgen.CONFIGS[args.config])
+    if args.hash_predict:
+        import lsgen
+        return bench_hash(args, lsgen.CONFIGS[args.config])
 
     import numpy as np
     import torch

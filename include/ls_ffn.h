@@ -155,6 +155,36 @@ ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int3
 ls_status ls_stream_weights(ls_ffn* ctx, int32_t layer, const int32_t* idx_host, int32_t n,
                             int32_t n_stages, ls_stream_stats* stats);
 
+/* Stacked learnable hashing predictor of one layer (Sec. 3.3.1, Eq. hash_layer,
+ * Eq. hashfunc_layer): five hashing layers of 8 hash bits with 256-wide binary
+ * features, an alternative block scorer to ls_predict.  Binary {-1,+1}
+ * vectors are bit-packed: element e is bit (e & 31) of word e >> 5, 1 = +1. */
+typedef struct {
+    const float* w1;        /* [d][8] real hyperplanes of the first layer */
+    const uint32_t* w_bin;  /* [4][8][8] binary hyperplanes of layers 2..5 (hash bit b: 256 signs) */
+    const uint32_t* tables; /* [4][256][8] feature tables T_1..T_4 (bucket i: 256 signs) */
+    const uint8_t* head;    /* [256][n_blk] block-priority levels of the last layer's bucket */
+} ls_hash_weights;
+
+/* Copy one layer's hashing predictor (host pointers) into the context.
+ * Synchronous.  LS_E_INVAL on null pointers or layer out of range. */
+ls_status ls_set_hash_predictor(ls_ffn* ctx, int32_t layer, const ls_hash_weights* w);
+
+/* Block scores of the hashing predictor for B tokens:
+ *   layer 1:    c = sign(x W_1)              (8 products over d, binary32)
+ *   layers 2-5: c = sign(y W_k), y = T_{k-1}[i], products as XNOR + bitcount
+ *   i = the code read as an 8-bit number, first hash bit most significant,
+ *       +1 -> 1; sign(0) = +1
+ *   scores[b] = head[i_5][b].
+ * The input is used as given (the codes are invariant to a positive scale, so
+ * no prenorm).  The first layer's products are summed in a fixed order (per
+ * hash bit: 256 partial sums of x_j W_1[j] over j = t, t + 256, ... with fused
+ * multiply-adds in increasing j, then pairwise halving), so the codes are
+ * reproducible.  x: dev fp32 [B, d]; scores: dev fp32 [B, n_blk] (integral
+ * values 0..255; rank them with ls_select_blocks).  1 <= B <= max_batch.
+ * LS_E_STATE if the layer has no hashing predictor. */
+ls_status ls_hash_predict(ls_ffn* ctx, int32_t layer, const float* x, int32_t B, float* scores);
+
 /* Cross-layer prefetch policy of ls_decode_step_streamed. */
 typedef enum {
     LS_PREFETCH_NONE = 0,    /* a layer's blocks are requested once its own list is known */
@@ -209,9 +239,10 @@ ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_
  * gate/up kernels, so nothing is launched under this id), 1 predictor projection
  * (or the folded predictor),
  * 2 predictor head (not launched when the predictor is folded),
- * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step. */
+ * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step,
+ * 7 stacked hashing predictor. */
 enum { LS_K_PRENORM = 0, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN,
-       LS_K_DECODE, LS_K_COUNT };
+       LS_K_DECODE, LS_K_HASH, LS_K_COUNT };
 ls_status ls_set_kernel_timing(ls_ffn* ctx, int32_t enable);
 ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* total_ms,
                            int64_t* launches);

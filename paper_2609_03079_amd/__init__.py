@@ -28,6 +28,7 @@ LS_PREFETCH_NONE, LS_PREFETCH_ONESHOT, LS_PREFETCH_REFINE = 0, 1, 2
 
 EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", "ls_select_blocks",
            "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step_streamed", "ls_decode_step",
+           "ls_set_hash_predictor", "ls_hash_predict",
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
@@ -36,7 +37,8 @@ PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_
           "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",
           "prefetch_issued", "partials_done", "next_list_ranked", "early_gateup_done",
           "worker_start", "worker_acts_seen")
-LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE = range(7)
+(LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE,
+ LS_K_HASH) = range(8)
 
 
 class LsFfnDesc(ctypes.Structure):
@@ -57,6 +59,11 @@ class LsLayerWeights(ctypes.Structure):
 class LsStreamStats(ctypes.Structure):
     _fields_ = [("hits", ctypes.c_int64), ("misses", ctypes.c_int64), ("bytes", ctypes.c_int64),
                 ("evictions", ctypes.c_int64)]
+
+
+class LsHashWeights(ctypes.Structure):
+    _fields_ = [("w1", ctypes.c_void_p), ("w_bin", ctypes.c_void_p), ("tables", ctypes.c_void_p),
+                ("head", ctypes.c_void_p)]
 
 
 class LsStreamReport(ctypes.Structure):
@@ -92,6 +99,8 @@ def load():
     lib.ls_stream_weights.argtypes = [P, I32, P, I32, I32, ctypes.POINTER(LsStreamStats)]
     lib.ls_decode_step.argtypes = [P, P, I32, I32]
     lib.ls_decode_step_streamed.argtypes = [P, P, I32, I32, I32, I32, ctypes.POINTER(LsStreamReport)]
+    lib.ls_set_hash_predictor.argtypes = [P, I32, ctypes.POINTER(LsHashWeights)]
+    lib.ls_hash_predict.argtypes = [P, I32, P, I32, P]
     lib.ls_debug_last_activations.argtypes = [P, P, I64, ctypes.POINTER(I64)]
     lib.ls_set_kernel_timing.argtypes = [P, I32]
     lib.ls_kernel_timing.argtypes = [P, I32, I32, ctypes.POINTER(ctypes.c_double),
@@ -185,6 +194,19 @@ class Ffn:
                                                               int(a.size), n_stages,
                                                               ctypes.byref(stats)))
         return stats
+
+    def ls_set_hash_predictor(self, layer: int, hw) -> None:
+        """hw: .w1 fp32 [d, 8], .w_bin uint32 [4, 8, 8], .tables uint32 [4, 256, 8], .head uint8 [256, n_blk]"""
+        arrs = [np.ascontiguousarray(hw.w1, np.float32), np.ascontiguousarray(hw.w_bin, np.uint32),
+                np.ascontiguousarray(hw.tables, np.uint32), np.ascontiguousarray(hw.head, np.uint8)]
+        if arrs[0].shape != (self.d_model, 8) or arrs[1].shape != (4, 8, 8) or \
+                arrs[2].shape != (4, 256, 8) or arrs[3].shape != (256, self.d_ff // self.block):
+            raise ValueError("hashing predictor arrays have the wrong shapes")
+        w = LsHashWeights(*[a.ctypes.data for a in arrs])
+        _check(self.lib, self.ctx, self.lib.ls_set_hash_predictor(self.ctx, layer, ctypes.byref(w)))
+
+    def ls_hash_predict(self, layer: int, x, B: int, scores) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_hash_predict(self.ctx, layer, _ptr(x), B, _ptr(scores)))
 
     def ls_decode_step_streamed(self, x, k: int, n_stages: int, mode: int, k_spec: int = 0
                                 ) -> LsStreamReport:

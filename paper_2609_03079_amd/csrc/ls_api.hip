@@ -28,6 +28,7 @@ struct ls_ffn {
     std::vector<uint8_t*> arena;  // device: [blocks][bias][predictor]  (resident mode)
     std::vector<ls::LayerDev> dev;
     std::vector<uint8_t> is_set;
+    std::vector<ls::HashDev> hash;  // per layer: stacked hashing predictor (null until set)
 
     // workspaces (device)
     float* z = nullptr;       // [maxB, r]
@@ -246,6 +247,8 @@ ls_status validate_desc(const ls_ffn_desc* d) {
 void free_all(ls_ffn* c) {
     for (auto p : c->arena) if (p) (void)hipFree(p);
     c->arena.clear();
+    for (auto& h : c->hash) if (h.w1) (void)hipFree(h.w1);  // one allocation per layer
+    c->hash.clear();
     for (void* p : {(void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
                     (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
                     (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err, (void*)c->spec_idx,
@@ -701,6 +704,47 @@ ls_status ls_stream_weights(ls_ffn* c, int32_t layer, const int32_t* idx_host, i
 static ls_status read_list(ls_ffn* c, const int32_t* dev, int32_t n, int32_t* host) {
     LS_HIP(c, hipMemcpyAsync(host, dev, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
     LS_HIP(c, hipStreamSynchronize(c->stream));
+    return LS_OK;
+}
+
+ls_status ls_set_hash_predictor(ls_ffn* c, int32_t layer, const ls_hash_weights* w) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!w || !w->w1 || !w->w_bin || !w->tables || !w->head) return fail(c, LS_E_INVAL, "null pointer");
+    if (c->hash.empty()) c->hash.assign((size_t)c->desc.n_layers, ls::HashDev{});
+    ls::HashDev& h = c->hash[(size_t)layer];
+    const size_t n_w1 = (size_t)s.d * 8 * sizeof(float), n_wb = 4 * 8 * 8 * sizeof(uint32_t),
+                 n_tb = 4 * 256 * 8 * sizeof(uint32_t), n_hd = 256 * (size_t)s.n_blk;
+    if (!h.w1) {
+        uint8_t* p = nullptr;
+        if (hipMalloc((void**)&p, n_w1 + n_wb + n_tb + n_hd) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(c, LS_E_NOMEM, "hashing predictor allocation failed");
+        }
+        h.w1 = reinterpret_cast<float*>(p);
+        h.w_bin = reinterpret_cast<uint32_t*>(p + n_w1);
+        h.tables = reinterpret_cast<uint32_t*>(p + n_w1 + n_wb);
+        h.head = p + n_w1 + n_wb + n_tb;
+    }
+    LS_HIP(c, hipMemcpy(h.w1, w->w1, n_w1, hipMemcpyHostToDevice));
+    LS_HIP(c, hipMemcpy(h.w_bin, w->w_bin, n_wb, hipMemcpyHostToDevice));
+    LS_HIP(c, hipMemcpy(h.tables, w->tables, n_tb, hipMemcpyHostToDevice));
+    LS_HIP(c, hipMemcpy(h.head, w->head, n_hd, hipMemcpyHostToDevice));
+    return LS_OK;
+}
+
+ls_status ls_hash_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, float* scores) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!x || !scores) return fail(c, LS_E_INVAL, "null pointer");
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    if (c->hash.empty() || !c->hash[(size_t)layer].w1) return fail(c, LS_E_STATE, "no hashing predictor for this layer");
+    const ls::HashDev& h = c->hash[(size_t)layer];
+    LS_HIP(c, timed(c, LS_K_HASH, [&] { return ls::launch_hash_predict(s.d, s.n_blk, x, B, h, scores, c->stream); }));
     return LS_OK;
 }
 

@@ -69,6 +69,16 @@ hipError_t launch_gemv_rows(ls_dtype t, const void* W, int rows, int cols, int G
 // fp32); P1 [r, d], P2 [n_blk, r] row-major in the weight type.
 hipError_t launch_fold_predictor(ls_dtype t, const void* P1, const void* P2, int r, int d, int n_blk,
                                  float* out, hipStream_t st);
+// Stacked hashing predictor of one layer (ls_hash.hip): device copies of its weights.
+struct HashDev {
+    float* w1 = nullptr;          // [d][8]
+    uint32_t* w_bin = nullptr;    // [4][8][8]
+    uint32_t* tables = nullptr;   // [4][256][8]
+    uint8_t* head = nullptr;      // [256][n_blk]
+};
+// scores[b, :] = the hashing predictor's block scores of token b of x [B, d]
+hipError_t launch_hash_predict(int d, int nblk, const float* x, int B, const HashDev& h, float* scores,
+                               hipStream_t st);
 hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k, float tau,
                          int union_batch, int cap, int32_t* idx, int32_t* count, hipStream_t st);
 // slot_table: null in resident mode (block b lives at blocks + b*block_bytes); else
