@@ -377,6 +377,142 @@ def bench_refinement(args, cfg) -> int:
     return 0
 
 
+def zero_skip_bytes(cfg, acts, n_entries: int):
+    """Gate/up/down bytes of one layer's n_entries list blocks, from the activations acts
+    ([B, n_entries * block] in list order; a neuron counts as active when its activation is
+    nonzero for some token).  Returns (block, neuron, kernel):
+      block  every row of the blocks (the block path);
+      neuron gate rows of all their neurons, up and down rows of the active ones;
+      kernel as neuron, but down rows come in groups of V = 16 / element-size neurons (one
+             16-byte vector of the down layout holds V neurons of one output column), and a
+             group with an active neuron costs all V."""
+    import numpy as np
+    s, d, blk = cfg.elem_bytes, cfg.d_model, cfg.block
+    V = 16 // s
+    row = d * s
+    if n_entries <= 0:
+        return 0, 0, 0
+    a = np.asarray(acts).reshape(-1, n_entries * blk)
+    act = (a != 0).any(axis=0)
+    n_act = int(act.sum())
+    n_grp = int(act.reshape(n_entries, blk // V, V).any(axis=2).sum())
+    gate = n_entries * blk * row
+    return 3 * gate, gate + 2 * n_act * row, gate + n_act * row + n_grp * V * row
+
+
+def bench_zero_skip(args, cfg) -> int:
+    """Row-level zero skip within the selected blocks on the per-kernel path: the bytes the
+    gate/up and down kernels must read with and without it (counted from the activations of
+    the same steps), the decode rate both ways, and a check that both give equal outputs."""
+    import numpy as np
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    L = args.layers or cfg.n_layers
+    cfg = cfg.with_(n_layers=L)
+    B, K, W = args.batch, args.steps, args.warmup
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    f = lsffn.Ffn(n_layers=L, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank,
+                  max_batch=B, dtype=cfg.dtype, act=cfg.act, prenorm_rms=int(cfg.prenorm), stream=stream)
+    f.ls_configure(lsffn.LS_CFG_DECODE_PATH, 1)
+    for l in range(L):
+        f.ls_ffn_set_layer(l, lsgen.layer_weights(cfg, l))
+        if (l + 1) % 8 == 0:
+            print(f"set-up: {l + 1}/{L} layers", file=sys.stderr, flush=True)
+    xs = torch.from_numpy(lsgen.tokens(cfg, 0, W + K, B)).to(dev)
+
+    # bytes and equality: the first T steps through the per-call entry points, both ways
+    T = min(K, args.zero_skip_tokens)
+    cap = min(cfg.n_blk, B * cfg.k)
+    scores = torch.empty(B, cfg.n_blk, dtype=torch.float32, device=dev)
+    idx = torch.empty(cap, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    y = [torch.empty(B, cfg.d_model, dtype=torch.float32, device=dev) for _ in range(2)]
+    act = torch.empty(B * cfg.d_ff, dtype=torch.float32, device=dev)
+    tot = np.zeros(3)
+    n_act = n_neur = 0
+    equal = True
+    for t in range(T):
+        x = xs[t].clone()
+        for l in range(L):
+            f.ls_predict(l, x, B, scores)
+            f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+            for zs in (0, 1):
+                f.ls_configure(lsffn.LS_CFG_ZERO_SKIP, zs)
+                f.ls_sparse_ffn_step(l, x, B, idx, cnt, 0, cap, y[zs])
+            n = f.ls_debug_last_activations(act)
+            U = int(cnt.item())
+            a = act[:B * n].view(B, n)[:, :U * cfg.block].cpu().numpy()
+            tot += zero_skip_bytes(cfg, a, U)
+            n_act += int((a != 0).any(axis=0).sum())
+            n_neur += U * cfg.block
+            equal &= bool(torch.equal(y[0], y[1]))
+            x = y[1].clone()
+        print(f"bytes: token {t + 1}/{T}", file=sys.stderr, flush=True)
+    per_tok = tot / T
+
+    res = {}
+    for zs in (0, 1):
+        f.ls_configure(lsffn.LS_CFG_ZERO_SKIP, zs)
+        for i in range(W):
+            f.ls_decode_step(xs[i].clone(), B, cfg.k)
+        torch.cuda.synchronize()
+        f.ls_set_kernel_timing(True)
+        f.ls_kernel_timing(0, reset=True)
+        xw = [xs[W + i].clone() for i in range(K)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            f.ls_decode_step(xw[i], B, cfg.k)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        f.ls_set_kernel_timing(False)
+        r = {"tokens_per_s": round(B * K / wall, 2), "ms_per_step": round(1e3 * wall / K, 4)}
+        for kid, name in ((lsffn.LS_K_GATEUP, "gateup"), (lsffn.LS_K_DOWN, "down")):
+            ms, n = f.ls_kernel_timing(kid)
+            r[f"{name}_avg_us"] = round(1e3 * ms / max(n, 1), 3)
+        res["on" if zs else "off"] = r
+        print(f"timed: zero skip {zs}", file=sys.stderr, flush=True)
+
+    on = res["on"]
+    U_mean = n_neur / (T * L * cfg.block)
+    s, row = cfg.elem_bytes, cfg.d_model * cfg.elem_bytes
+    gate_b = U_mean * cfg.block * row
+    act_rows = n_act / (T * L)
+    # the dominant kernel under zero skip and its bytes per launch (one launch per layer)
+    gu_bytes = gate_b + act_rows * row
+    dn_bytes = per_tok[2] / L - gu_bytes
+    dom, dom_bytes = (("gateup", gu_bytes) if on["gateup_avg_us"] >= on["down_avg_us"] else ("down", dn_bytes))
+    achieved = dom_bytes / (on[f"{dom}_avg_us"] * 1e-6) / 1e9
+    out = {
+        "metric": "row-level zero skip (per-kernel path): weight bytes per token and decode tokens/s, 1 GPU",
+        "value": on["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": on["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": lsgen.DTYPE_NAMES[cfg.dtype], "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {L} layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, block "
+                               f"{cfg.block} (k={cfg.k} of {cfg.n_blk}), rank {cfg.rank}, batch {B}",
+                   "global_batch": B, "seq_len": 1, "parallelism": "none (1 GPU)", "decode_path": "kernels"},
+        "zero_skip": {"outputs_equal": equal, "byte_tokens": T,
+                      "active_fraction_in_selected_blocks": round(n_act / max(n_neur, 1), 4),
+                      "ffn_bytes_per_token": {"block": int(per_tok[0]), "neuron": int(per_tok[1]),
+                                              "kernel": int(per_tok[2])},
+                      "kernel_over_block": round(per_tok[2] / per_tok[0], 4),
+                      "neuron_over_block": round(per_tok[1] / per_tok[0], 4),
+                      "off": res["off"], "on": on},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": int(dom_bytes), "avg_launch_us": on[f"{dom}_avg_us"]},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0 if equal else 1
+
+
 def bench_hash(args, cfg) -> int:
     """Latency of the stacked hashing predictor (one workgroup per token) against the low-rank
     predictor (the folded GEMV) on the same shape, per call, from the library's HIP-event
@@ -459,6 +595,11 @@ def main() -> int:
     ap.add_argument("--refinement-quality", action="store_true",
                     help="instead of the benchmark: next-layer prediction quality per refinement "
                          "stage (use with --config llama2_7b_planted)")
+    ap.add_argument("--zero-skip", action="store_true",
+                    help="instead of the benchmark: row-level zero skip on the per-kernel path (bytes "
+                         "per token with and without it, decode rate both ways)")
+    ap.add_argument("--zero-skip-tokens", type=int, default=8,
+                    help="with --zero-skip: tokens whose activations give the byte counts")
     ap.add_argument("--prefetch-compare", action="store_true",
                     help="host-resident workloads: also time every prefetch policy")
     ap.add_argument("--overlap-from-trace", default="", metavar="DIR",
@@ -482,6 +623,9 @@ def main() -> int:
     if args.hash_predict:
         import lsgen
         return bench_hash(args, lsgen.CONFIGS[args.config])
+    if args.zero_skip:
+        import lsgen
+        return bench_zero_skip(args, lsgen.CONFIGS[args.config])
 
     import numpy as np
     import torch

@@ -267,9 +267,20 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    parts, fp32 accumulation); 0 always uses the vector-ALU kernels.
  *  LS_CFG_TRACE_WG: -1 (default) off; otherwise the fused kernel records
  *    per-layer phase timestamps of that workgroup (see ls_debug_phase_trace).
+ *  LS_CFG_ZERO_SKIP: 0 (default) off; 1 row-level zero skip within the
+ *    selected blocks (the zero outputs of ReLU-family and thresholded-SiLU
+ *    gates that Sec. 2.1 builds on: a neuron whose gate output is zero adds
+ *    nothing to Eq. 1): the gate row is read first, the up row only when the gate output is nonzero for
+ *    some token of the batch, and a 16-byte down vector (V = 16 / element-size
+ *    neurons of one output column) only when one of its neurons has a nonzero
+ *    activation.  Results are equal to those with the knob off.  It applies to
+ *    the per-kernel sequence (ls_sparse_ffn_step, the streamed step, and
+ *    ls_decode_step on the per-kernel path), which then runs the vector-ALU
+ *    kernels at every batch size; the fused kernel reads rows before their
+ *    gate outputs are known and ignores it.
  * LS_E_INVAL on an unknown key or value. */
 enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3,
-       LS_CFG_BATCH_MFMA = 4 };
+       LS_CFG_BATCH_MFMA = 4, LS_CFG_ZERO_SKIP = 5 };
 ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
 
 /* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for

@@ -32,7 +32,7 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_last_error")
-LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA = range(5)
+LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA, LS_CFG_ZERO_SKIP = range(6)
 PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_gathered",
           "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",
           "prefetch_issued", "partials_done", "next_list_ranked", "early_gateup_done",

@@ -930,6 +930,11 @@ ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
         c->shape.batch_mfma = (int)value;
         return LS_OK;
     }
+    if (key == LS_CFG_ZERO_SKIP) {
+        if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "zero skip must be 0 or 1");
+        c->shape.zero_skip = (int)value;
+        return LS_OK;
+    }
     if (key == LS_CFG_COOPERATIVE) {
         if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "cooperative must be 0 or 1");
         c->cooperative = (int)value;

@@ -48,6 +48,10 @@ struct Shape {
     // 1: batches of kMfmaMinBatch or more tokens use the matrix-core gate/up and down
     // kernels when the shape allows (16-bit weights, block a multiple of 32).
     int batch_mfma = 1;
+    // 1: row-level zero skip in the vector-ALU gate/up and down kernels (up rows only for
+    // neurons with a nonzero gate output; down vectors only for groups with a nonzero
+    // activation); the batch then always runs on those kernels.
+    int zero_skip = 0;
 };
 
 constexpr int kMfmaMinBatch = 4;

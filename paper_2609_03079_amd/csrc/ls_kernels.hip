@@ -229,7 +229,64 @@ __device__ inline int list_end(const int32_t* count, int end, int n_blk) {
     return end < c ? end : c;
 }
 
-template <ls_dtype T, ls_act A, int B, bool RMS>
+// acc[i] += row . h[i] over this lane's 16-byte chunks (c = lane + 64 n), in the same order
+// whether or not the row is read alone; SS also sums h[i]^2 into ss[i].
+template <ls_dtype T, int B, bool SS>
+__device__ __forceinline__ void row_dot(const u32x4* row, const float* __restrict__ h, int d, int lane,
+                                        float (&acc)[B], float (&ss)[B]) {
+    constexpr int V = Wt<T>::V;
+    constexpr int U = 4;
+    const int nchunk = d / V;
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+        u32x4 rw[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            rw[u] = c < nchunk ? ld_stream(row + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            if (c < nchunk) {
+                float w[V];
+                Wt<T>::widen(rw[u], w);
+#pragma unroll
+                for (int i = 0; i < B; ++i) {
+                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
+#pragma unroll
+                    for (int qq = 0; qq < V / 4; ++qq) {
+                        const f32x4 x4 = hp[qq];
+                        acc[i] = fmaf(w[4 * qq + 0], x4.x, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 1], x4.y, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 2], x4.z, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 3], x4.w, acc[i]);
+                        if (SS) {
+                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
+                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
+                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
+                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Gate output of Eq. 1 before the up factor: ReLU(g), or SiLU(g) when |SiLU(g)| > thresh
+// (thresholded SiLU), else 0.
+template <ls_act A>
+__device__ __forceinline__ float gate_out(float g, float thresh) {
+    if (A == LS_ACT_REGLU) return fmaxf(g, 0.f);
+    const float sg = g / (1.f + expf(-g));
+    return fabsf(sg) > thresh ? sg : 0.f;
+}
+
+// ZS (row-level zero skip): the gate row is read first and the up row only when the gate
+// output of some token is nonzero; a neuron whose gate output is zero for every token then
+// costs its gate row alone.  The activations equal those of the one-pass form (same
+// accumulation order; a skipped product is an exact zero).
+template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS>
 __global__ __launch_bounds__(256) void gateup_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
@@ -261,6 +318,28 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     float ag[B], au[B], ss[B];  // h here is the layer input x; ss its sum of squares
 #pragma unroll
     for (int i = 0; i < B; ++i) ag[i] = au[i] = ss[i] = 0.f;
+    const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
+    if (ZS) {
+        row_dot<T, B, RMS>(grow, h, d, lane, ag, ss);
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
+            ag[i] = gate_out<A>(sc * wave_sum(ag[i]) + bj, thresh);
+            ss[i] = sc;
+            any |= ag[i] != 0.f;
+        }
+        if (any) {  // wave-uniform: every lane holds the same sums
+            float unused[B];
+            row_dot<T, B, false>(urow, h, d, lane, au, unused);
+        }
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            const float a = ag[i] != 0.f ? ag[i] * (ss[i] * wave_sum(au[i])) : 0.f;
+            if (lane == 0) a_buf[(size_t)i * F + apos] = a;
+        }
+        return;
+    }
     for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
         u32x4 rg[U], ru[U];
 #pragma unroll
@@ -302,7 +381,6 @@ __global__ __launch_bounds__(256) void gateup_kernel(
             }
         }
     }
-    const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
         const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
@@ -320,7 +398,10 @@ __global__ __launch_bounds__(256) void gateup_kernel(
 }
 
 // ---- down projection + residual -----------------------------------------------------------
-template <ls_dtype T, int B>
+// ZS (row-level zero skip): a lane's 16-byte vector holds V neurons of one column; it is read
+// only when one of those neurons has a nonzero activation for some token.  The sums equal
+// those of the full read (a skipped product is an exact zero).
+template <ls_dtype T, int B, bool ZS>
 __global__ __launch_bounds__(256) void down_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
@@ -352,20 +433,42 @@ __global__ __launch_bounds__(256) void down_kernel(
                                                     down_off);
         }
         for (int i0 = 0; i0 < per_lane; i0 += 2) {
+            bool use[EU][2];
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    use[u][r] = ent[u] >= 0 && c < nchunk;
+                    if (ZS && use[u][r]) {
+                        const float* ap = a_buf + (size_t)ent[u] * blk + (size_t)(c / kColTile) * V;
+                        bool nz = false;
+#pragma unroll
+                        for (int i = 0; i < B; ++i) {
+                            const f32x4* a4 = reinterpret_cast<const f32x4*>(ap + (size_t)i * F);
+#pragma unroll
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = a4[qq];
+                                nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
+                            }
+                        }
+                        use[u][r] = nz;
+                    }
+                }
             u32x4 raw[EU][2];
 #pragma unroll
             for (int u = 0; u < EU; ++u)
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
                     const int c = lane + 64 * (i0 + r);
-                    raw[u][r] = (ent[u] >= 0 && c < nchunk) ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
+                    raw[u][r] = use[u][r] ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
                 }
 #pragma unroll
             for (int u = 0; u < EU; ++u)
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
                     const int c = lane + 64 * (i0 + r);
-                    if (ent[u] >= 0 && c < nchunk) {
+                    if (use[u][r]) {
                         float w[V];
                         Wt<T>::widen(raw[u][r], w);
                         const int grp = c / kColTile;  // this lane's V neurons
@@ -510,16 +613,16 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
     if (tasks <= 0) return hipSuccess;
     const dim3 grid((unsigned)((tasks + 3) / 4)), blk(256);
     const size_t bb = s.block_elems * elem_size(s.dtype);
-#define LS_GU(NB)                                                                                 \
-    do {                                                                                          \
-        if (s.prenorm)                                                                            \
-            hipLaunchKernelGGL((gateup_kernel<T, A, NB, true>), grid, blk, 0, st, L.blocks, bb,   \
-                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx,  \
-                               count, begin, end, a_buf);                                         \
-        else                                                                                      \
-            hipLaunchKernelGGL((gateup_kernel<T, A, NB, false>), grid, blk, 0, st, L.blocks, bb,  \
-                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx,  \
-                               count, begin, end, a_buf);                                         \
+#define LS_GU_K(NB, RMS, ZS)                                                                       \
+    hipLaunchKernelGGL((gateup_kernel<T, A, NB, RMS, ZS>), grid, blk, 0, st, L.blocks, bb, slot_table, \
+                       L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, a_buf)
+#define LS_GU(NB)                                                                 \
+    do {                                                                          \
+        if (s.prenorm) {                                                          \
+            if (s.zero_skip) LS_GU_K(NB, true, true); else LS_GU_K(NB, true, false);   \
+        } else {                                                                  \
+            if (s.zero_skip) LS_GU_K(NB, false, true); else LS_GU_K(NB, false, false); \
+        }                                                                         \
     } while (0)
     switch (B) {
         case 1: LS_GU(1); break;
@@ -533,13 +636,14 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
         default: return hipErrorInvalidValue;
     }
 #undef LS_GU
+#undef LS_GU_K
     return hipGetLastError();
 }
 
 hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* h, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, float* a_buf, hipStream_t st) {
-    if (s.batch_mfma && mfma_path(s, B))
+    if (s.batch_mfma && !s.zero_skip && mfma_path(s, B))
         return launch_gateup_mfma(s, L, slot_table, h, B, idx, count, begin, end, a_buf, st);
     const bool relu = s.act == LS_ACT_REGLU;
     switch (s.dtype) {
@@ -562,9 +666,15 @@ static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_
                          int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
     const dim3 grid(s.d / kColTile), blk(256);
     const size_t bb = s.block_elems * elem_size(s.dtype);
-#define LS_DN(NB)                                                                             \
-    hipLaunchKernelGGL((down_kernel<T, NB>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
-                       s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc)
+#define LS_DN(NB)                                                                                   \
+    do {                                                                                            \
+        if (s.zero_skip)                                                                            \
+            hipLaunchKernelGGL((down_kernel<T, NB, true>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
+                               s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);      \
+        else                                                                                        \
+            hipLaunchKernelGGL((down_kernel<T, NB, false>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
+                               s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);      \
+    } while (0)
     switch (B) {
         case 1: LS_DN(1); break;
         case 2: LS_DN(2); break;
@@ -583,7 +693,7 @@ static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                        int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
-    if (s.batch_mfma && mfma_path(s, B))
+    if (s.batch_mfma && !s.zero_skip && mfma_path(s, B))
         return launch_down_mfma(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
     switch (s.dtype) {
         case LS_F32: return down_t<LS_F32>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);

@@ -158,3 +158,29 @@ def test_block_cache_invalidate(bc):
     assert np.all(c.table(0) == -1)
     ok, cnt, _ = c.request(0, [0, 1, 2])
     assert ok and cnt == [0, 3, 0]
+
+
+def test_zero_skip_byte_counts():
+    """The bench's zero-skip byte accounting on hand-made activations: no active neuron costs the
+    gate rows alone, all active costs the whole blocks, one active neuron adds its up row plus
+    one group of V down rows (V = 16 / element size)."""
+    import importlib.util
+    import lsgen
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"]
+    U, blk, row, V = 3, cfg.block, cfg.d_model * cfg.elem_bytes, 16 // cfg.elem_bytes
+    z = np.zeros((2, U * blk), np.float32)
+    assert bench.zero_skip_bytes(cfg, z, U) == (3 * U * blk * row, U * blk * row, U * blk * row)
+    full = np.ones_like(z)
+    assert bench.zero_skip_bytes(cfg, full, U) == (3 * U * blk * row,) * 3
+    one = z.copy()
+    one[1, blk + 5] = -0.25  # one neuron of the second entry, active for the second token only
+    blockb, neuron, kernel = bench.zero_skip_bytes(cfg, one, U)
+    assert neuron == U * blk * row + 2 * row
+    assert kernel == U * blk * row + row + V * row
+    neg_zero = z.copy()
+    neg_zero[0, 7] = -0.0  # a signed zero is no activation
+    assert bench.zero_skip_bytes(cfg, neg_zero, U)[2] == U * blk * row
+    assert bench.zero_skip_bytes(cfg, z[:, :0], 0) == (0, 0, 0)
