@@ -186,6 +186,8 @@ def bench_streaming(args, cfg) -> int:
     f = lsffn.Ffn(n_layers=L, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank,
                   max_batch=1, dtype=cfg.dtype, act=cfg.act, residency=lsffn.LS_WEIGHTS_HOST,
                   prenorm_rms=int(cfg.prenorm), hbm_cache_bytes=slots * block_bytes, stream=stream)
+    f.ls_configure(lsffn.LS_CFG_STREAM_SYNC, {"events": lsffn.LS_SYNC_EVENTS, "flags": lsffn.LS_SYNC_FLAGS,
+                                              "host": lsffn.LS_SYNC_HOST}[args.stream_sync])
     weights = []
     for l in range(L):
         w = lsgen.layer_weights(cfg, l)
@@ -237,6 +239,8 @@ def bench_streaming(args, cfg) -> int:
     compare = {}
     if args.prefetch_compare:
         for name in modes:
+            if args.stream_sync == "flags" and name == "refine":
+                continue  # re-scoring between stage launches needs per-stage launches
             w_, t_ = run(name)
             compare[name] = {"tokens_per_s": round(K / w_, 3),
                              "copied_GB_per_token": round(t_["bytes"] / K / 1e9, 4),
@@ -257,7 +261,7 @@ def bench_streaming(args, cfg) -> int:
                                f"block {cfg.block} (k={cfg.k} of {cfg.n_blk}), rank {cfg.rank}, batch 1, "
                                f"host-resident blocks, HBM cache {slots} slots ({100 * cache_frac:.1f}% of "
                                f"the blocks), {S} copy stages per layer, prefetch {args.prefetch} "
-                               f"({k_spec} blocks per prediction)",
+                               f"({k_spec} blocks per prediction), stage sync {args.stream_sync}",
                    "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)", "decode_path": "kernels"},
         "streaming": {"copied_GB_per_token": round(totals["bytes"] / K / 1e9, 4),
                       "late_GB_per_token": round(totals["late"] / K / 1e9, 4),
@@ -513,6 +517,99 @@ def bench_zero_skip(args, cfg) -> int:
     return 0 if equal else 1
 
 
+def bench_sync_overhead(args, cfg) -> int:
+    """Synchronisation overhead of one MLP layer split into K stages (the paper's Table 3
+    comparison), with host-resident weights whose blocks are all already in the HBM cache, so
+    no copy is waited for: per-layer time of the streamed decode step for K = 1..16 with a host
+    synchronisation after every stage, with per-stage events and launches, and with device
+    flags and one persistent launch per layer.  The overhead is the per-layer time minus that of
+    one launch pair per layer (events, K = 1); the MLP compute is the gate/up + down kernel
+    time of that case."""
+    import numpy as np
+    import torch
+
+    import lsgen
+    import paper_2609_03079_amd as lsffn
+
+    L = args.layers or 8
+    cfg = cfg.with_(n_layers=L)
+    k, nb = cfg.k, cfg.n_blk
+    bb = 3 * cfg.block * cfg.d_model * cfg.elem_bytes
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    f = lsffn.Ffn(n_layers=L, d_model=cfg.d_model, d_ff=cfg.d_ff, block=cfg.block, rank=cfg.rank, max_batch=1,
+                  dtype=cfg.dtype, act=cfg.act, prenorm_rms=int(cfg.prenorm), residency=lsffn.LS_WEIGHTS_HOST,
+                  hbm_cache_bytes=L * nb * bb, stream=stream)
+    for l in range(L):
+        f.ls_ffn_set_layer(l, lsgen.layer_weights(cfg, l))
+        print(f"set-up: {l + 1}/{L} layers", file=sys.stderr, flush=True)
+    every = np.arange(nb, dtype=np.int32)
+    for l in range(L):  # every block of every layer resident: the timed steps copy nothing
+        f.ls_stream_weights(l, every, 1)
+    f.ls_ffn_sync()
+    xs = torch.from_numpy(lsgen.tokens(cfg, 0, args.warmup + args.steps, 1)).to(dev)
+    Ks = (1, 2, 4, 8, 16)
+    names = {lsffn.LS_SYNC_HOST: "host_sync", lsffn.LS_SYNC_EVENTS: "events", lsffn.LS_SYNC_FLAGS: "device_flags"}
+    per_layer = {}
+    compute_us = None
+    stage_us = {}
+    copied = 0
+    for sync, name in names.items():
+        f.ls_configure(lsffn.LS_CFG_STREAM_SYNC, sync)
+        per_layer[name] = {}
+        for K in Ks:
+            for i in range(args.warmup):
+                f.ls_decode_step_streamed(xs[i].clone(), k, K, lsffn.LS_PREFETCH_NONE, k)
+            torch.cuda.synchronize()
+            timing = (name == "events" and K == 1) or name == "device_flags"
+            if timing:
+                f.ls_set_kernel_timing(True)
+                f.ls_kernel_timing(0, reset=True)
+            xw = [xs[args.warmup + i].clone() for i in range(args.steps)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(args.steps):
+                r = f.ls_decode_step_streamed(xw[i], k, K, lsffn.LS_PREFETCH_NONE, k)
+                copied += r.copied_bytes
+            f.ls_ffn_sync()
+            wall = time.perf_counter() - t0
+            per_layer[name][K] = 1e3 * wall / (args.steps * L)
+            if timing:
+                if name == "events":
+                    gu, n1 = f.ls_kernel_timing(lsffn.LS_K_GATEUP)
+                    dn, n2 = f.ls_kernel_timing(lsffn.LS_K_DOWN)
+                    compute_us = 1e3 * (gu / max(n1, 1) + dn / max(n2, 1))
+                else:
+                    ms, n = f.ls_kernel_timing(lsffn.LS_K_STAGE)
+                    stage_us[K] = round(1e3 * ms / max(n, 1), 2)
+                f.ls_set_kernel_timing(False)
+            if name == "device_flags":
+                assert all(f.ls_debug_stages_done(l) == K for l in range(L))
+            print(f"timed: {name} K={K}: {per_layer[name][K]:.4f} ms per layer", file=sys.stderr, flush=True)
+    base = per_layer["events"][1]
+    overhead = {name: {str(K): round(v[K] - base, 4) for K in Ks} for name, v in per_layer.items()}
+    out = {
+        "metric": "synchronisation overhead per MLP layer vs stages (Table 3 comparison), 1 GPU",
+        "value": overhead["device_flags"]["16"], "unit": "ms per layer at 16 stages (device flags)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(per_layer["device_flags"][16] * L, 4), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": lsgen.DTYPE_NAMES[cfg.dtype], "data": "synthetic",
+        "config": {"workload": f"{cfg.name} shape, host-resident weights, every block cached: {L} layers, d_model "
+                               f"{cfg.d_model}, d_ff {cfg.d_ff}, block {cfg.block} (k={k} of {nb}), batch 1",
+                   "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)"},
+        "sync_overhead_ms": overhead,
+        "per_layer_ms": {name: {str(K): round(v[K], 4) for K in Ks} for name, v in per_layer.items()},
+        "mlp_compute_ms": round(compute_us / 1e3, 4) if compute_us else None,
+        "stage_kernel_us": stage_us,
+        "bytes_copied_in_timed_steps": copied,
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out))
+    f.close()
+    return 0
+
+
 def bench_hash(args, cfg) -> int:
     """Latency of the stacked hashing predictor (one workgroup per token) against the low-rank
     predictor (the folded GEMV) on the same shape, per call, from the library's HIP-event
@@ -587,6 +684,10 @@ def main() -> int:
                     help="host-resident workloads: copy stages per layer (events the compute waits on)")
     ap.add_argument("--prefetch", choices=("none", "oneshot", "refine"), default="refine",
                     help="host-resident workloads: cross-layer prefetch policy of the streamed step")
+    ap.add_argument("--stream-sync", choices=("events", "flags", "host"), default="events",
+                    help="host-resident workloads: how a stage's compute waits for its copies (per-stage "
+                         "events and launches, device flags with one persistent launch per layer, or a host "
+                         "synchronisation after every stage)")
     ap.add_argument("--k-spec", type=int, default=0,
                     help="host-resident workloads: blocks per next-layer prediction (0: k)")
     ap.add_argument("--hash-predict", action="store_true",
@@ -595,6 +696,9 @@ def main() -> int:
     ap.add_argument("--refinement-quality", action="store_true",
                     help="instead of the benchmark: next-layer prediction quality per refinement "
                          "stage (use with --config llama2_7b_planted)")
+    ap.add_argument("--sync-overhead", action="store_true",
+                    help="instead of the benchmark: per-layer synchronisation overhead vs stage count with "
+                         "host synchronisation, events and device flags (use with --config mistral_7b_ffn)")
     ap.add_argument("--zero-skip", action="store_true",
                     help="instead of the benchmark: row-level zero skip on the per-kernel path (bytes "
                          "per token with and without it, decode rate both ways)")
@@ -623,6 +727,9 @@ def main() -> int:
     if args.hash_predict:
         import lsgen
         return bench_hash(args, lsgen.CONFIGS[args.config])
+    if args.sync_overhead:
+        import lsgen
+        return bench_sync_overhead(args, lsgen.CONFIGS[args.config])
     if args.zero_skip:
         import lsgen
         return bench_zero_skip(args, lsgen.CONFIGS[args.config])

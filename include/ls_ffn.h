@@ -212,12 +212,29 @@ typedef struct {
  * prediction), with layer n's blocks protected from eviction meanwhile.  The
  * result depends only on the final lists, so every mode gives the same x
  * bitwise; the modes differ in when and how many bytes cross the host link.
+ * How a stage's compute learns that its copies landed is LS_CFG_STREAM_SYNC:
+ * events and one gate/up + down launch pair per stage (default); device flags
+ * (Sec. 3.2.1, Alg. 1): the copy stream writes an arrival word after each
+ * stage and ONE persistent launch per layer consumes the stages as they land,
+ * the last workgroup to finish a stage writing a host-visible done word (then
+ * at most 64 stages, and LS_PREFETCH_REFINE, which re-scores between stage
+ * launches, is LS_E_UNSUPPORTED); or a host synchronisation after every stage
+ * launch (the device-wide synchronisation the paper compares against).  All
+ * three give the same x bitwise.
  * x: dev fp32 [d], updated in place.  report may be NULL.
  * LS_E_UNSUPPORTED with HBM-resident weights; LS_E_INVAL on bad arguments;
  * LS_E_CAPACITY if the cache cannot hold a layer's list (plus, while
- * prefetching, the next layer's) with the running layer's blocks protected. */
+ * prefetching, the next layer's) with the running layer's blocks protected;
+ * LS_E_DEVICE if a wait of the stage-consuming kernel ran out (2 s; reported
+ * by the next flagged layer or by ls_ffn_sync). */
 ls_status ls_decode_step_streamed(ls_ffn* ctx, float* x, int32_t k, int32_t n_stages, int32_t mode,
                                   int32_t k_spec, ls_stream_report* report);
+
+/* Debug: after a streamed step with device flags, the number of stages of
+ * `layer`'s latest request whose done word carries that request's tag (all of
+ * them once the layer's kernel has finished).  Synchronises the stream.
+ * LS_E_STATE if no flagged step has run the layer. */
+ls_status ls_debug_stages_done(ls_ffn* ctx, int32_t layer, int32_t* n_done);
 
 /* One decode step over every layer: for l in 0..L-1:
  *   scores = predict(l, x); idx = topk(scores, k) (union over the B tokens if B > 1);
@@ -240,9 +257,9 @@ ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_
  * (or the folded predictor),
  * 2 predictor head (not launched when the predictor is folded),
  * 3 selection, 4 gate/up gather, 5 down projection, 6 fused decode step,
- * 7 stacked hashing predictor. */
+ * 7 stacked hashing predictor, 8 stage-consuming kernel of the streamed step. */
 enum { LS_K_PRENORM = 0, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN,
-       LS_K_DECODE, LS_K_HASH, LS_K_COUNT };
+       LS_K_DECODE, LS_K_HASH, LS_K_STAGE, LS_K_COUNT };
 ls_status ls_set_kernel_timing(ls_ffn* ctx, int32_t enable);
 ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* total_ms,
                            int64_t* launches);
@@ -278,9 +295,14 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    ls_decode_step on the per-kernel path), which then runs the vector-ALU
  *    kernels at every batch size; the fused kernel reads rows before their
  *    gate outputs are known and ignores it.
+ *  LS_CFG_STREAM_SYNC: how ls_decode_step_streamed orders a stage's compute
+ *    after its copies: 0 (default) events, one launch pair per stage; 1 device
+ *    flags and one persistent launch per layer (allocates the flag words at
+ *    the first use); 2 a host synchronisation after every stage.  The
+ *    persistent launch is cooperative when LS_CFG_COOPERATIVE is 1.
  * LS_E_INVAL on an unknown key or value. */
 enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3,
-       LS_CFG_BATCH_MFMA = 4, LS_CFG_ZERO_SKIP = 5 };
+       LS_CFG_BATCH_MFMA = 4, LS_CFG_ZERO_SKIP = 5, LS_CFG_STREAM_SYNC = 6 };
 ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
 
 /* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for

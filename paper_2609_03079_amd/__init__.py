@@ -31,14 +31,16 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_set_hash_predictor", "ls_hash_predict",
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
-           "ls_last_error")
-LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA, LS_CFG_ZERO_SKIP = range(6)
+           "ls_debug_stages_done", "ls_last_error")
+(LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA, LS_CFG_ZERO_SKIP,
+ LS_CFG_STREAM_SYNC) = range(7)
+LS_SYNC_EVENTS, LS_SYNC_FLAGS, LS_SYNC_HOST = range(3)
 PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_gathered",
           "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",
           "prefetch_issued", "partials_done", "next_list_ranked", "early_gateup_done",
           "worker_start", "worker_acts_seen")
 (LS_K_PRENORM, LS_K_PRED_P1, LS_K_PRED_P2, LS_K_SELECT, LS_K_GATEUP, LS_K_DOWN, LS_K_DECODE,
- LS_K_HASH) = range(8)
+ LS_K_HASH, LS_K_STAGE) = range(9)
 
 
 class LsFfnDesc(ctypes.Structure):
@@ -232,6 +234,12 @@ class Ffn:
         _check(self.lib, self.ctx, self.lib.ls_debug_phase_trace(self.ctx, out.ctypes.data, out.size,
                                                                  ctypes.byref(n)))
         return out
+
+    def ls_debug_stages_done(self, layer: int) -> int:
+        """Stages of the layer's latest flagged request whose done word carries its tag."""
+        n = ctypes.c_int32()
+        _check(self.lib, self.ctx, self.lib.ls_debug_stages_done(self.ctx, layer, ctypes.byref(n)))
+        return n.value
 
     def ls_ffn_sync(self) -> None:
         _check(self.lib, self.ctx, self.lib.ls_ffn_sync(self.ctx))

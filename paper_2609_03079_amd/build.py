@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblsffn.so")
-SOURCES = ["ls_api.hip", "ls_kernels.hip", "ls_decode.hip", "ls_mfma.hip", "ls_hash.hip"]
+SOURCES = ["ls_api.hip", "ls_kernels.hip", "ls_decode.hip", "ls_mfma.hip", "ls_hash.hip", "ls_stage.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <thread>
 
@@ -90,6 +91,16 @@ struct ls_ffn {
     int spec_blocks = 0;          // LS_CFG_SPEC_BLOCKS
     int cooperative = 1;          // LS_CFG_COOPERATIVE
 
+    // streamed-step coordination (LS_CFG_STREAM_SYNC)
+    int stream_sync = 0;
+    uint32_t* arrive = nullptr;      // fine-grained device [L][kMaxStages]: copy-stage arrival words
+    size_t arrive_bytes = 0;
+    uint32_t* stage_done = nullptr;  // pinned coherent host [L][kMaxStages] done words, then the status word
+    uint32_t* stage_cnt = nullptr;   // device [2][kMaxStages]: the stage consumer's counters
+    uint32_t stage_tag = 0;          // last tag handed out
+    std::vector<uint32_t> layer_tag; // per layer: tag of its latest flagged request
+    std::vector<int> layer_stages;   // per layer: stages of that request
+
     ls_status sticky = LS_OK;
     std::string err;
 };
@@ -97,6 +108,35 @@ struct ls_ffn {
 namespace {
 
 std::string g_create_error;
+
+// Arrival words live in fine-grained device memory, which the library does not free while the
+// process runs: a released buffer goes back to this pool for the next context that needs one
+// of the same size.
+std::mutex g_arrive_mu;
+std::vector<std::pair<size_t, uint32_t*>> g_arrive_pool;
+
+uint32_t* arrive_take(size_t bytes) {
+    {
+        std::lock_guard<std::mutex> lk(g_arrive_mu);
+        for (size_t i = 0; i < g_arrive_pool.size(); ++i)
+            if (g_arrive_pool[i].first == bytes) {
+                uint32_t* p = g_arrive_pool[i].second;
+                g_arrive_pool.erase(g_arrive_pool.begin() + (long)i);
+                return p;
+            }
+    }
+    void* p = nullptr;
+    if (hipExtMallocWithFlags(&p, bytes, hipDeviceMallocFinegrained) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    return static_cast<uint32_t*>(p);
+}
+
+void arrive_give(uint32_t* p, size_t bytes) {
+    std::lock_guard<std::mutex> lk(g_arrive_mu);
+    g_arrive_pool.emplace_back(bytes, p);
+}
 
 ls_status fail(ls_ffn* c, ls_status st, const std::string& msg) {
     if (c) {
@@ -252,7 +292,7 @@ void free_all(ls_ffn* c) {
     for (void* p : {(void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
                     (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
                     (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err, (void*)c->spec_idx,
-                    (void*)c->trace})
+                    (void*)c->trace, (void*)c->stage_cnt})
         if (p) (void)hipFree(p);
     if (c->staging) (void)hipHostFree(c->staging);
     if (c->host_blocks) (void)hipHostFree(c->host_blocks);
@@ -262,6 +302,8 @@ void free_all(ls_ffn* c) {
     for (auto e : c->layer_done) if (e) (void)hipEventDestroy(e);
     for (auto e : c->spec_read) if (e) (void)hipEventDestroy(e);
     if (c->idx_pinned) (void)hipHostFree(c->idx_pinned);
+    if (c->stage_done) (void)hipHostFree(c->stage_done);
+    if (c->arrive) arrive_give(c->arrive, c->arrive_bytes);
     if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
     for (auto e : c->table_uploaded) if (e) (void)hipEventDestroy(e);
     for (auto& p : c->pending) {
@@ -625,8 +667,14 @@ ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t*
 // table it rewrites); compute of other layers keeps running under the copies.  The stages of
 // the latest request of a layer are what its sparse steps wait for (earlier requests' copies
 // precede them on the copy stream).  copied (may be null) receives the blocks copied.
+// With a nonzero arrive_tag (for the stage-consuming kernel) the tag is written into the
+// layer's arrival word of stage 0 and of every later stage that copies blocks, once its
+// copies are done; wait_on[s] receives the word stage s must wait for (the last one written
+// at or before it), and the request records one event after all its stages instead of one
+// per stage.
 static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_host, int32_t n, int32_t n_stages,
-                                ls_stream_stats* stats, std::vector<int32_t>* copied, int protect_layer = -1) {
+                                ls_stream_stats* stats, std::vector<int32_t>* copied, int protect_layer = -1,
+                                uint32_t arrive_tag = 0, uint8_t* wait_on = nullptr) {
     const Shape& s = c->shape;
     if (n > c->bcache->slots()) return fail(c, LS_E_CAPACITY, "request exceeds the HBM cache slots");
     std::vector<ls::BlockCache::Fill> fills;
@@ -660,8 +708,10 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
     ranges.clear();
     size_t fi = 0;
     const uint8_t* layer_host = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+    int written = 0;
     for (int sidx = 0; sidx < n_stages; ++sidx) {
         const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);
+        const size_t fi0 = fi;
         for (; fi < fills.size() && fills[fi].pos < hi; ++fi) {
             const auto& f = fills[fi];
             LS_HIP(c, hipMemcpyAsync(c->cache + (size_t)f.slot * c->block_bytes,
@@ -669,8 +719,21 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
                                      hipMemcpyHostToDevice, c->copy_stream));
             if (copied) copied->push_back(f.block);
         }
-        LS_HIP(c, hipEventRecord(events[sidx], c->copy_stream));
-        ranges.emplace_back(lo, hi);
+        if (!arrive_tag) {
+            LS_HIP(c, hipEventRecord(events[sidx], c->copy_stream));
+            ranges.emplace_back(lo, hi);
+            continue;
+        }
+        if (sidx == 0 || fi > fi0) {
+            LS_HIP(c, hipStreamWriteValue32(c->copy_stream, c->arrive + (size_t)layer * ls::kMaxStages + sidx,
+                                            arrive_tag, 0));
+            written = sidx;
+        }
+        wait_on[sidx] = (uint8_t)written;
+    }
+    if (arrive_tag) {  // per-call steps on this layer wait for the whole request
+        LS_HIP(c, hipEventRecord(events[0], c->copy_stream));
+        ranges.emplace_back(0, n);
     }
     c->streamed[layer] = 1;
     if (stats) {
@@ -748,6 +811,46 @@ ls_status ls_hash_predict(ls_ffn* c, int32_t layer, const float* x, int32_t B, f
     return LS_OK;
 }
 
+// One launch of the stage-consuming kernel for `layer` (its list is in c->idx, its copies and
+// arrival words queued with `tag`).  Every earlier consumer launch on the stream has finished
+// by now (the host read back a list enqueued after it), so its status word is final.
+static ls_status launch_stage_consumer(ls_ffn* c, int32_t layer, const float* x_in, float* x_out, int32_t n,
+                                       int32_t n_stages, uint32_t tag, const uint8_t* wait_on) {
+    const Shape& s = c->shape;
+    const size_t L = (size_t)c->desc.n_layers;
+    volatile uint32_t* status = c->stage_done + L * ls::kMaxStages;
+    if (*status) return fail(c, LS_E_DEVICE, "a bounded wait in the stage-consuming kernel timed out");
+    ls::StageArgs a{};
+    a.blocks = c->cache;
+    a.block_bytes = c->block_bytes;
+    a.slot_table = c->slot_tables + (size_t)layer * s.n_blk;
+    a.bias = c->dev[layer].bias;
+    a.thresh = c->dev[layer].threshold;
+    a.x_in = x_in;
+    a.x_acc = x_out;
+    a.a_buf = c->a;
+    a.idx = c->idx;
+    a.n = n;
+    a.K = n_stages;
+    a.d = s.d;
+    a.blk = s.blk;
+    a.n_blk = s.n_blk;
+    a.F = s.F;
+    a.arrive = c->arrive + (size_t)layer * ls::kMaxStages;
+    a.done = c->stage_done + (size_t)layer * ls::kMaxStages;
+    a.cnt = c->stage_cnt;
+    a.status = c->stage_done + L * ls::kMaxStages;
+    a.tag = tag;
+    for (int i = 0; i < n_stages; ++i) a.wait_on[i] = wait_on[i];
+    a.limit = 200000000ull;  // 2 s at 100 MHz
+    LS_HIP(c, timed(c, LS_K_STAGE, [&] { return ls::launch_stage_consumer(s, a, c->n_wg, c->cooperative != 0, c->stream); }));
+    LS_HIP(c, hipEventRecord(c->layer_done[(size_t)layer], c->stream));
+    c->layer_done_recorded[(size_t)layer] = 1;
+    c->last_act_n = (int64_t)n * s.blk;
+    c->last_act_B = 1;
+    return LS_OK;
+}
+
 ls_status ls_decode_step_streamed(ls_ffn* c, float* x, int32_t k, int32_t n_stages, int32_t mode,
                                   int32_t k_spec, ls_stream_report* report) {
     ls_status st = check_ctx(c);
@@ -760,6 +863,10 @@ ls_status ls_decode_step_streamed(ls_ffn* c, float* x, int32_t k, int32_t n_stag
     if (n_stages < 1) return fail(c, LS_E_INVAL, "n_stages must be >= 1");
     if (mode < LS_PREFETCH_NONE || mode > LS_PREFETCH_REFINE) return fail(c, LS_E_INVAL, "unknown prefetch mode");
     if (mode != LS_PREFETCH_NONE && (k_spec < 1 || k_spec > nb)) return fail(c, LS_E_INVAL, "k_spec must be in 1..n_blk");
+    const bool flags = c->stream_sync == 1;
+    if (flags && mode == LS_PREFETCH_REFINE)
+        return fail(c, LS_E_UNSUPPORTED, "refined prefetch needs per-stage launches (LS_CFG_STREAM_SYNC 0 or 2)");
+    if (flags && n_stages > ls::kMaxStages) return fail(c, LS_E_INVAL, "n_stages exceeds 64 with device flags");
     for (int l = 0; l < L; ++l)
         if (!c->is_set[l]) return fail(c, LS_E_STATE, "layer weights not set");
     ls_stream_report rep{};
@@ -779,7 +886,15 @@ ls_status ls_decode_step_streamed(ls_ffn* c, float* x, int32_t k, int32_t n_stag
         const bool next = l + 1 < L;
         std::copy(fin_h, fin_h + k, fin.begin());
         ls_stream_stats ss{};
-        if ((st = stream_request(c, l, fin.data(), k, n_stages, &ss, nullptr)) != LS_OK) return st;
+        uint8_t wait_on[ls::kMaxStages] = {};
+        uint32_t tag = 0;
+        if (flags) {
+            tag = ++c->stage_tag;
+            if (tag == 0) tag = ++c->stage_tag;
+            c->layer_tag[(size_t)l] = tag;
+            c->layer_stages[(size_t)l] = n_stages;
+        }
+        if ((st = stream_request(c, l, fin.data(), k, n_stages, &ss, nullptr, -1, tag, wait_on)) != LS_OK) return st;
         rep.final_bytes += (int64_t)k * bb;
         rep.late_bytes += ss.bytes;
         spec_copied.clear();
@@ -806,10 +921,12 @@ ls_status ls_decode_step_streamed(ls_ffn* c, float* x, int32_t k, int32_t n_stag
             if ((st = speculate(cur, 0)) != LS_OK || (st = prefetch(0)) != LS_OK) return st;
         }
         int pending = -1;  // a refined list read back but not yet requested
-        for (int j = 0; j < n_stages; ++j) {
+        if (flags && (st = launch_stage_consumer(c, l, cur, nxt, k, n_stages, tag, wait_on)) != LS_OK) return st;
+        for (int j = 0; j < (flags ? 0 : n_stages); ++j) {
             const int lo = (int)((int64_t)j * k / n_stages), hi = (int)((int64_t)(j + 1) * k / n_stages);
             if (hi > lo || j == 0)
                 if ((st = ls_sparse_ffn_step(c, l, cur, 1, c->idx, c->count, lo, hi, nxt)) != LS_OK) return st;
+            if (c->stream_sync == 2) LS_HIP(c, hipStreamSynchronize(c->stream));  // host waits for every stage
             if (next && mode == LS_PREFETCH_REFINE) {
                 // x~^(j+1) is in nxt: score layer l+1 on it; the list of the previous stage is
                 // requested meanwhile (the host waits for it while this stage runs)
@@ -930,6 +1047,32 @@ ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
         c->shape.batch_mfma = (int)value;
         return LS_OK;
     }
+    if (key == LS_CFG_STREAM_SYNC) {
+        if (value < 0 || value > 2) return fail(c, LS_E_INVAL, "stream sync must be 0, 1 or 2");
+        if (value == 1 && !c->arrive) {
+            const size_t L = (size_t)c->desc.n_layers, words = L * ls::kMaxStages;
+            c->arrive_bytes = words * sizeof(uint32_t);
+            c->arrive = arrive_take(c->arrive_bytes);
+            if (!c->arrive) return fail(c, LS_E_NOMEM, "fine-grained arrival words could not be allocated");
+            LS_HIP(c, hipMemset(c->arrive, 0, c->arrive_bytes));
+            if (hipHostMalloc(reinterpret_cast<void**>(&c->stage_done), (words + 1) * sizeof(uint32_t),
+                              hipHostMallocCoherent) != hipSuccess) {
+                (void)hipGetLastError();
+                c->stage_done = nullptr;
+                return fail(c, LS_E_NOMEM, "pinned done words could not be allocated");
+            }
+            std::memset(c->stage_done, 0, (words + 1) * sizeof(uint32_t));
+            if (dmalloc(&c->stage_cnt, 2 * (size_t)ls::kMaxStages) != hipSuccess) {
+                (void)hipGetLastError();
+                return fail(c, LS_E_NOMEM, "stage counters could not be allocated");
+            }
+            LS_HIP(c, hipMemset(c->stage_cnt, 0, 2 * (size_t)ls::kMaxStages * sizeof(uint32_t)));
+            c->layer_tag.assign(L, 0u);
+            c->layer_stages.assign(L, 0);
+        }
+        c->stream_sync = (int)value;
+        return LS_OK;
+    }
     if (key == LS_CFG_ZERO_SKIP) {
         if (value != 0 && value != 1) return fail(c, LS_E_INVAL, "zero skip must be 0 or 1");
         c->shape.zero_skip = (int)value;
@@ -979,6 +1122,20 @@ ls_status ls_debug_phase_trace(ls_ffn* c, int64_t* host_out, int64_t cap, int64_
     return LS_OK;
 }
 
+ls_status ls_debug_stages_done(ls_ffn* c, int32_t layer, int32_t* n_done) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (!n_done) return fail(c, LS_E_INVAL, "null pointer");
+    if (layer < 0 || layer >= c->desc.n_layers) return fail(c, LS_E_INVAL, "layer out of range");
+    if (!c->stage_done || !c->layer_tag[(size_t)layer]) return fail(c, LS_E_STATE, "no flagged step has run this layer");
+    LS_HIP(c, hipStreamSynchronize(c->stream));
+    const volatile uint32_t* w = c->stage_done + (size_t)layer * ls::kMaxStages;
+    int32_t n = 0;
+    for (int sidx = 0; sidx < c->layer_stages[(size_t)layer]; ++sidx) n += w[sidx] == c->layer_tag[(size_t)layer];
+    *n_done = n;
+    return LS_OK;
+}
+
 ls_status ls_ffn_sync(ls_ffn* c) {
     ls_status st = check_ctx(c);
     if (st != LS_OK) return st;
@@ -986,6 +1143,8 @@ ls_status ls_ffn_sync(ls_ffn* c) {
     int e = 0;
     LS_HIP(c, hipMemcpy(&e, c->dev_err, sizeof e, hipMemcpyDeviceToHost));
     if (e) return fail(c, LS_E_DEVICE, "a bounded wait in the fused decode kernel timed out");
+    if (c->stage_done && c->stage_done[(size_t)c->desc.n_layers * ls::kMaxStages])
+        return fail(c, LS_E_DEVICE, "a bounded wait in the stage-consuming kernel timed out");
     return LS_OK;
 }
 

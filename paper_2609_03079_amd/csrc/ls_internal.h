@@ -95,6 +95,32 @@ hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_ta
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                        int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
 
+// ---- persistent consumer of a streamed layer's copy stages (ls_stage.hip) ----------------
+constexpr int kMaxStages = 64;
+struct StageArgs {
+    const uint8_t* blocks;       // HBM cache arena
+    size_t block_bytes;
+    const int32_t* slot_table;   // device [n_blk]: cache slot of each block of the layer
+    const void* bias;
+    float thresh;
+    const float* x_in;           // [d] layer input
+    float* x_acc;                // [d] x_in + the partial outputs of the stages so far
+    float* a_buf;                // [F] activations in list order
+    const int32_t* idx;          // device priority list, n entries
+    int n, K;                    // list length, stages (stage s: entries [s n / K, (s+1) n / K))
+    int d, blk, n_blk, F;
+    const uint32_t* arrive;      // [K] arrival words (fine-grained device memory), or null
+    uint8_t wait_on[kMaxStages]; // stage s waits for arrive[wait_on[s]] (wait_on[s] <= s)
+    uint32_t* done;              // [K] host-visible done words, or null
+    uint32_t* cnt;               // device [2][kMaxStages]: per-stage done counts, then gate/up counts; zero between calls
+    uint32_t* status;            // host-visible: 0, or 2 / 4 when an arrival / barrier wait ran out
+    uint32_t tag;                // this call's arrival / done value
+    uint64_t limit;              // wall-clock ticks (100 MHz) any one wait may take
+};
+// One launch of `grid` workgroups (one per compute unit; cooperative when asked) consuming
+// the stages in order (B = 1).
+hipError_t launch_stage_consumer(const Shape& s, const StageArgs& p, int grid, bool cooperative, hipStream_t st);
+
 // ---- matrix-core variants for B >= kMfmaMinBatch (ls_mfma.hip) ---------------------------
 bool mfma_path(const Shape& s, int B);
 hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,

@@ -14,6 +14,7 @@
 // Every reduction has a fixed order: results are bitwise reproducible.
 #include "ls_device.h"
 #include "ls_internal.h"
+#include "ls_sparse.h"
 
 namespace ls {
 namespace {
@@ -222,289 +223,32 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
     if (tid == 0) count[0] = U;
 }
 
-// ---- gate/up gather + gating --------------------------------------------------------------
-__device__ inline int list_end(const int32_t* count, int end, int n_blk) {
-    int c = *count;
-    c = c < 0 ? 0 : (c > n_blk ? n_blk : c);
-    return end < c ? end : c;
-}
-
-// acc[i] += row . h[i] over this lane's 16-byte chunks (c = lane + 64 n), in the same order
-// whether or not the row is read alone; SS also sums h[i]^2 into ss[i].
-template <ls_dtype T, int B, bool SS>
-__device__ __forceinline__ void row_dot(const u32x4* row, const float* __restrict__ h, int d, int lane,
-                                        float (&acc)[B], float (&ss)[B]) {
-    constexpr int V = Wt<T>::V;
-    constexpr int U = 4;
-    const int nchunk = d / V;
-    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
-        u32x4 rw[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
-            rw[u] = c < nchunk ? ld_stream(row + c) : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
-            if (c < nchunk) {
-                float w[V];
-                Wt<T>::widen(rw[u], w);
-#pragma unroll
-                for (int i = 0; i < B; ++i) {
-                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
-#pragma unroll
-                    for (int qq = 0; qq < V / 4; ++qq) {
-                        const f32x4 x4 = hp[qq];
-                        acc[i] = fmaf(w[4 * qq + 0], x4.x, acc[i]);
-                        acc[i] = fmaf(w[4 * qq + 1], x4.y, acc[i]);
-                        acc[i] = fmaf(w[4 * qq + 2], x4.z, acc[i]);
-                        acc[i] = fmaf(w[4 * qq + 3], x4.w, acc[i]);
-                        if (SS) {
-                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
-                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
-                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
-                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
-                        }
-                    }
-                }
-            }
-        }
-    }
-}
-
-// Gate output of Eq. 1 before the up factor: ReLU(g), or SiLU(g) when |SiLU(g)| > thresh
-// (thresholded SiLU), else 0.
-template <ls_act A>
-__device__ __forceinline__ float gate_out(float g, float thresh) {
-    if (A == LS_ACT_REGLU) return fmaxf(g, 0.f);
-    const float sg = g / (1.f + expf(-g));
-    return fabsf(sg) > thresh ? sg : 0.f;
-}
-
-// ZS (row-level zero skip): the gate row is read first and the up row only when the gate
-// output of some token is nonzero; a neuron whose gate output is zero for every token then
-// costs its gate row alone.  The activations equal those of the one-pass form (same
-// accumulation order; a skipped product is an exact zero).
+// ---- gate/up gather + gating: one wave per neuron of list entries [begin, end) ------------
 template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS>
 __global__ __launch_bounds__(256) void gateup_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
     int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
     int end, float* __restrict__ a_buf) {
-    constexpr int V = Wt<T>::V;
-    constexpr int U = 4;
-    const int lane = threadIdx.x & 63;
     const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int e = begin + (int)(t / blk);
     const int q = (int)(t % blk);
     if (e >= list_end(count, end, n_blk)) return;
-    const int b = idx[e];
-    const size_t apos = (size_t)e * blk + q;
-    if (b < 0 || b >= n_blk) {  // invalid id: the entry contributes nothing
-        if (lane < B) a_buf[(size_t)lane * F + apos] = 0.f;
-        return;
-    }
-    const int slot = slot_table ? slot_table[b] : b;
-    if (slot < 0) {  // block not in the cache: contributes nothing
-        if (lane < B) a_buf[(size_t)lane * F + apos] = 0.f;
-        return;
-    }
-    const uint8_t* base = blocks + (size_t)slot * block_bytes;
-    const size_t row_bytes = (size_t)d * Wt<T>::kBytes;
-    const u32x4* grow = reinterpret_cast<const u32x4*>(base + (size_t)q * row_bytes);
-    const u32x4* urow = reinterpret_cast<const u32x4*>(base + (size_t)(blk + q) * row_bytes);
-    const int nchunk = d / V;
-    float ag[B], au[B], ss[B];  // h here is the layer input x; ss its sum of squares
-#pragma unroll
-    for (int i = 0; i < B; ++i) ag[i] = au[i] = ss[i] = 0.f;
-    const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
-    if (ZS) {
-        row_dot<T, B, RMS>(grow, h, d, lane, ag, ss);
-        bool any = false;
-#pragma unroll
-        for (int i = 0; i < B; ++i) {
-            const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
-            ag[i] = gate_out<A>(sc * wave_sum(ag[i]) + bj, thresh);
-            ss[i] = sc;
-            any |= ag[i] != 0.f;
-        }
-        if (any) {  // wave-uniform: every lane holds the same sums
-            float unused[B];
-            row_dot<T, B, false>(urow, h, d, lane, au, unused);
-        }
-#pragma unroll
-        for (int i = 0; i < B; ++i) {
-            const float a = ag[i] != 0.f ? ag[i] * (ss[i] * wave_sum(au[i])) : 0.f;
-            if (lane == 0) a_buf[(size_t)i * F + apos] = a;
-        }
-        return;
-    }
-    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
-        u32x4 rg[U], ru[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
-            const bool ok = c < nchunk;
-            rg[u] = ok ? ld_stream(grow + c) : u32x4{0u, 0u, 0u, 0u};
-            ru[u] = ok ? ld_stream(urow + c) : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 64;
-            if (c < nchunk) {
-                float wg[V], wu[V];
-                Wt<T>::widen(rg[u], wg);
-                Wt<T>::widen(ru[u], wu);
-#pragma unroll
-                for (int i = 0; i < B; ++i) {
-                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
-#pragma unroll
-                    for (int qq = 0; qq < V / 4; ++qq) {
-                        const f32x4 x4 = hp[qq];
-                        ag[i] = fmaf(wg[4 * qq + 0], x4.x, ag[i]);
-                        ag[i] = fmaf(wg[4 * qq + 1], x4.y, ag[i]);
-                        ag[i] = fmaf(wg[4 * qq + 2], x4.z, ag[i]);
-                        ag[i] = fmaf(wg[4 * qq + 3], x4.w, ag[i]);
-                        au[i] = fmaf(wu[4 * qq + 0], x4.x, au[i]);
-                        au[i] = fmaf(wu[4 * qq + 1], x4.y, au[i]);
-                        au[i] = fmaf(wu[4 * qq + 2], x4.z, au[i]);
-                        au[i] = fmaf(wu[4 * qq + 3], x4.w, au[i]);
-                        if (RMS) {
-                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
-                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
-                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
-                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
-                        }
-                    }
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-        const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
-        const float g = sc * wave_sum(ag[i]) + bj;
-        const float u = sc * wave_sum(au[i]);
-        float a;
-        if (A == LS_ACT_REGLU) {
-            a = fmaxf(g, 0.f) * u;  // exactly zero for g <= 0
-        } else {
-            const float sg = g / (1.f + expf(-g));
-            a = fabsf(sg) > thresh ? sg * u : 0.f;
-        }
-        if (lane == 0) a_buf[(size_t)i * F + apos] = a;
-    }
+    gateup_neuron<T, A, B, RMS, ZS>(blocks, block_bytes, slot_table, bias, thresh, h, d, blk, n_blk, F, idx[e], e,
+                                    q, a_buf, threadIdx.x & 63);
 }
 
-// ---- down projection + residual -----------------------------------------------------------
-// ZS (row-level zero skip): a lane's 16-byte vector holds V neurons of one column; it is read
-// only when one of those neurons has a nonzero activation for some token.  The sums equal
-// those of the full read (a skipped product is an exact zero).
+// ---- down projection + residual: one workgroup per 16-column tile ------------------------
 template <ls_dtype T, int B, bool ZS>
 __global__ __launch_bounds__(256) void down_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
     const float* __restrict__ x_in, float* __restrict__ x_acc) {
-    constexpr int V = Wt<T>::V;
-    constexpr int EU = 4;  // list entries in flight per wave
-    const int tile = blockIdx.x;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int n_end = list_end(count, end, n_blk);
-    const int nchunk = blk * Wt<T>::kBytes;  // 16-byte chunks of one (block, tile) piece
-    const int per_lane = (nchunk + 63) / 64;
-    const size_t down_off = (size_t)2 * blk * d * Wt<T>::kBytes +
-                            (size_t)tile * blk * kColTile * Wt<T>::kBytes;
-    float acc[B];
-#pragma unroll
-    for (int i = 0; i < B; ++i) acc[i] = 0.f;
-    for (int e0 = begin + wave; e0 < n_end; e0 += 4 * EU) {
-        const u32x4* src[EU];
-        int ent[EU];
-#pragma unroll
-        for (int u = 0; u < EU; ++u) {
-            const int e = e0 + 4 * u;
-            int b = e < n_end ? idx[e] : -1;
-            if (b >= n_blk) b = -1;
-            int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
-            ent[u] = slot < 0 ? -1 : e;
-            src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
-                                                    down_off);
-        }
-        for (int i0 = 0; i0 < per_lane; i0 += 2) {
-            bool use[EU][2];
-#pragma unroll
-            for (int u = 0; u < EU; ++u)
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    use[u][r] = ent[u] >= 0 && c < nchunk;
-                    if (ZS && use[u][r]) {
-                        const float* ap = a_buf + (size_t)ent[u] * blk + (size_t)(c / kColTile) * V;
-                        bool nz = false;
-#pragma unroll
-                        for (int i = 0; i < B; ++i) {
-                            const f32x4* a4 = reinterpret_cast<const f32x4*>(ap + (size_t)i * F);
-#pragma unroll
-                            for (int qq = 0; qq < V / 4; ++qq) {
-                                const f32x4 av = a4[qq];
-                                nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
-                            }
-                        }
-                        use[u][r] = nz;
-                    }
-                }
-            u32x4 raw[EU][2];
-#pragma unroll
-            for (int u = 0; u < EU; ++u)
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    raw[u][r] = use[u][r] ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
-                }
-#pragma unroll
-            for (int u = 0; u < EU; ++u)
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    if (use[u][r]) {
-                        float w[V];
-                        Wt<T>::widen(raw[u][r], w);
-                        const int grp = c / kColTile;  // this lane's V neurons
-                        const float* ap = a_buf + (size_t)ent[u] * blk + (size_t)grp * V;
-#pragma unroll
-                        for (int i = 0; i < B; ++i) {
-                            const f32x4* a4 = reinterpret_cast<const f32x4*>(ap + (size_t)i * F);
-#pragma unroll
-                            for (int qq = 0; qq < V / 4; ++qq) {
-                                const f32x4 av = a4[qq];
-                                acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
-                                acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
-                                acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
-                                acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
-                            }
-                        }
-                    }
-                }
-        }
-    }
-    // lanes l, l+16, l+32, l+48 hold the same column
     __shared__ float part[4][kMaxBatch][kColTile];
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-        float v = acc[i];
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
-        if (lane < kColTile) part[wave][i][lane] = v;
-    }
-    __syncthreads();
-    if (threadIdx.x < B * kColTile) {
-        const int i = threadIdx.x / kColTile, col = threadIdx.x % kColTile;
-        const float y = ((part[0][i][col] + part[1][i][col]) + part[2][i][col]) + part[3][i][col];
-        const size_t m = (size_t)i * d + (size_t)tile * kColTile + col;
-        x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
-    }
+    down_tile<T, B, ZS, false>(blocks, block_bytes, slot_table, a_buf, F, d, blk, n_blk, idx, begin,
+                               list_end(count, end, n_blk), x_in, x_acc, blockIdx.x, threadIdx.x >> 6,
+                               threadIdx.x & 63, true, part, [] { __syncthreads(); });
 }
 
 }  // namespace

@@ -1,0 +1,315 @@
+// ls_sparse.h - device bodies of the sparse FFN step shared by the per-call kernels and the
+// stage-consuming persistent kernel: one neuron's gate/up dot products and gating (Eq. 1),
+// one column tile of the down projection over a range of the priority list (the sum over
+// hidden neurons of Sec. 3.2.2).  Both kernels run the same code, so their results agree bit
+// for bit.
+#pragma once
+
+#include "ls_device.h"
+#include "ls_internal.h"
+
+namespace ls {
+
+// Activation words.  COH: relaxed atomics at agent scope, coherent across the compute units
+// of every XCD without cache maintenance (a persistent kernel that exchanges activations
+// between its own workgroups); otherwise plain accesses (the next kernel launch orders them).
+template <bool COH>
+__device__ __forceinline__ void act_store(float* p, float v) {
+    if (COH) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
+template <bool COH>
+__device__ __forceinline__ f32x4 act_load4(const float* p) {
+    if (!COH) return *reinterpret_cast<const f32x4*>(p);
+    f32x4 r;
+    r.x = __hip_atomic_load(p + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    r.y = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    r.z = __hip_atomic_load(p + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    r.w = __hip_atomic_load(p + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return r;
+}
+
+// ---- gate/up gather + gating (one wave per neuron) --------------------------------------------------------------
+__device__ inline int list_end(const int32_t* count, int end, int n_blk) {
+    int c = *count;
+    c = c < 0 ? 0 : (c > n_blk ? n_blk : c);
+    return end < c ? end : c;
+}
+
+// acc[i] += row . h[i] over this lane's 16-byte chunks (c = lane + 64 n), in the same order
+// whether or not the row is read alone; SS also sums h[i]^2 into ss[i].
+template <ls_dtype T, int B, bool SS>
+__device__ __forceinline__ void row_dot(const u32x4* row, const float* __restrict__ h, int d, int lane,
+                                        float (&acc)[B], float (&ss)[B]) {
+    constexpr int V = Wt<T>::V;
+    constexpr int U = 4;
+    const int nchunk = d / V;
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+        u32x4 rw[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            rw[u] = c < nchunk ? ld_stream(row + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            if (c < nchunk) {
+                float w[V];
+                Wt<T>::widen(rw[u], w);
+#pragma unroll
+                for (int i = 0; i < B; ++i) {
+                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
+#pragma unroll
+                    for (int qq = 0; qq < V / 4; ++qq) {
+                        const f32x4 x4 = hp[qq];
+                        acc[i] = fmaf(w[4 * qq + 0], x4.x, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 1], x4.y, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 2], x4.z, acc[i]);
+                        acc[i] = fmaf(w[4 * qq + 3], x4.w, acc[i]);
+                        if (SS) {
+                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
+                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
+                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
+                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Gate output of Eq. 1 before the up factor: ReLU(g), or SiLU(g) when |SiLU(g)| > thresh
+// (thresholded SiLU), else 0.
+template <ls_act A>
+__device__ __forceinline__ float gate_out(float g, float thresh) {
+    if (A == LS_ACT_REGLU) return fmaxf(g, 0.f);
+    const float sg = g / (1.f + expf(-g));
+    return fabsf(sg) > thresh ? sg : 0.f;
+}
+
+// Neuron q of list entry e (block b) for B tokens of h: a_buf[i F + e blk + q] = its
+// activation.  Called by one whole wave.
+// ZS (row-level zero skip): the gate row is read first and the up row only when the gate
+// output of some token is nonzero; a neuron whose gate output is zero for every token then
+// costs its gate row alone.  The activations equal those of the one-pass form (same
+// accumulation order; a skipped product is an exact zero).
+template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS, bool COH = false>
+__device__ __forceinline__ void gateup_neuron(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
+    int n_blk, int F, int b, int e, int q, float* __restrict__ a_buf, int lane) {
+    constexpr int V = Wt<T>::V;
+    constexpr int U = 4;
+    const size_t apos = (size_t)e * blk + q;
+    if (b < 0 || b >= n_blk) {  // invalid id: the entry contributes nothing
+        if (lane < B) act_store<COH>(a_buf + (size_t)lane * F + apos, 0.f);
+        return;
+    }
+    const int slot = slot_table ? slot_table[b] : b;
+    if (slot < 0) {  // block not in the cache: contributes nothing
+        if (lane < B) act_store<COH>(a_buf + (size_t)lane * F + apos, 0.f);
+        return;
+    }
+    const uint8_t* base = blocks + (size_t)slot * block_bytes;
+    const size_t row_bytes = (size_t)d * Wt<T>::kBytes;
+    const u32x4* grow = reinterpret_cast<const u32x4*>(base + (size_t)q * row_bytes);
+    const u32x4* urow = reinterpret_cast<const u32x4*>(base + (size_t)(blk + q) * row_bytes);
+    const int nchunk = d / V;
+    float ag[B], au[B], ss[B];  // h here is the layer input x; ss its sum of squares
+#pragma unroll
+    for (int i = 0; i < B; ++i) ag[i] = au[i] = ss[i] = 0.f;
+    const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
+    if (ZS) {
+        row_dot<T, B, RMS>(grow, h, d, lane, ag, ss);
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
+            ag[i] = gate_out<A>(sc * wave_sum(ag[i]) + bj, thresh);
+            ss[i] = sc;
+            any |= ag[i] != 0.f;
+        }
+        if (any) {  // wave-uniform: every lane holds the same sums
+            float unused[B];
+            row_dot<T, B, false>(urow, h, d, lane, au, unused);
+        }
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            const float a = ag[i] != 0.f ? ag[i] * (ss[i] * wave_sum(au[i])) : 0.f;
+            if (lane == 0) act_store<COH>(a_buf + (size_t)i * F + apos, a);
+        }
+        return;
+    }
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+        u32x4 rg[U], ru[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            const bool ok = c < nchunk;
+            rg[u] = ok ? ld_stream(grow + c) : u32x4{0u, 0u, 0u, 0u};
+            ru[u] = ok ? ld_stream(urow + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * 64;
+            if (c < nchunk) {
+                float wg[V], wu[V];
+                Wt<T>::widen(rg[u], wg);
+                Wt<T>::widen(ru[u], wu);
+#pragma unroll
+                for (int i = 0; i < B; ++i) {
+                    const f32x4* hp = reinterpret_cast<const f32x4*>(h + (size_t)i * d + (size_t)c * V);
+#pragma unroll
+                    for (int qq = 0; qq < V / 4; ++qq) {
+                        const f32x4 x4 = hp[qq];
+                        ag[i] = fmaf(wg[4 * qq + 0], x4.x, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 1], x4.y, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 2], x4.z, ag[i]);
+                        ag[i] = fmaf(wg[4 * qq + 3], x4.w, ag[i]);
+                        au[i] = fmaf(wu[4 * qq + 0], x4.x, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 1], x4.y, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 2], x4.z, au[i]);
+                        au[i] = fmaf(wu[4 * qq + 3], x4.w, au[i]);
+                        if (RMS) {
+                            ss[i] = fmaf(x4.x, x4.x, ss[i]);
+                            ss[i] = fmaf(x4.y, x4.y, ss[i]);
+                            ss[i] = fmaf(x4.z, x4.z, ss[i]);
+                            ss[i] = fmaf(x4.w, x4.w, ss[i]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+        const float sc = RMS ? rms_scale(wave_sum(ss[i]), d) : 1.f;
+        const float g = sc * wave_sum(ag[i]) + bj;
+        const float u = sc * wave_sum(au[i]);
+        float a;
+        if (A == LS_ACT_REGLU) {
+            a = fmaxf(g, 0.f) * u;  // exactly zero for g <= 0
+        } else {
+            const float sg = g / (1.f + expf(-g));
+            a = fabsf(sg) > thresh ? sg * u : 0.f;
+        }
+        if (lane == 0) act_store<COH>(a_buf + (size_t)i * F + apos, a);
+    }
+}
+
+// ---- down projection + residual -----------------------------------------------------------
+// Column tile `tile` of the down projection over list entries [begin, n_end), by 4 waves
+// (wave 0..3) that own `part`; x_acc = (begin == 0 ? x_in : x_acc) + y for the tile's columns.
+// The activation of neuron j of entry e is a_buf[i F + (e - a_off) blk + j].
+// sync() is the barrier of the waves that share `part` (the workgroup's, or the group's);
+// a group with active == false only takes part in it.
+// ZS (row-level zero skip): a lane's 16-byte vector holds V neurons of one column; it is read
+// only when one of those neurons has a nonzero activation for some token.  The sums equal
+// those of the full read (a skipped product is an exact zero).
+template <ls_dtype T, int B, bool ZS, bool COH, typename Sync>
+__device__ __forceinline__ void down_tile(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
+    const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
+    const int32_t* __restrict__ idx, int begin, int n_end,
+    const float* __restrict__ x_in, float* __restrict__ x_acc, int tile, int wave, int lane, bool active,
+    float (&part)[4][kMaxBatch][kColTile], Sync sync, int a_off = 0) {
+    constexpr int V = Wt<T>::V;
+    constexpr int EU = 4;  // list entries in flight per wave
+    if (!active) n_end = begin;
+    const int nchunk = blk * Wt<T>::kBytes;  // 16-byte chunks of one (block, tile) piece
+    const int per_lane = (nchunk + 63) / 64;
+    const size_t down_off = (size_t)2 * blk * d * Wt<T>::kBytes +
+                            (size_t)tile * blk * kColTile * Wt<T>::kBytes;
+    float acc[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) acc[i] = 0.f;
+    for (int e0 = begin + wave; e0 < n_end; e0 += 4 * EU) {
+        const u32x4* src[EU];
+        int ent[EU];
+#pragma unroll
+        for (int u = 0; u < EU; ++u) {
+            const int e = e0 + 4 * u;
+            int b = e < n_end ? idx[e] : -1;
+            if (b >= n_blk) b = -1;
+            int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
+            ent[u] = slot < 0 ? -1 : e;
+            src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
+                                                    down_off);
+        }
+        for (int i0 = 0; i0 < per_lane; i0 += 2) {
+            bool use[EU][2];
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    use[u][r] = ent[u] >= 0 && c < nchunk;
+                    if (ZS && use[u][r]) {
+                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)(c / kColTile) * V;
+                        bool nz = false;
+#pragma unroll
+                        for (int i = 0; i < B; ++i) {
+#pragma unroll
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                                nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
+                            }
+                        }
+                        use[u][r] = nz;
+                    }
+                }
+            u32x4 raw[EU][2];
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    raw[u][r] = use[u][r] ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+            for (int u = 0; u < EU; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = lane + 64 * (i0 + r);
+                    if (use[u][r]) {
+                        float w[V];
+                        Wt<T>::widen(raw[u][r], w);
+                        const int grp = c / kColTile;  // this lane's V neurons
+                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)grp * V;
+#pragma unroll
+                        for (int i = 0; i < B; ++i) {
+#pragma unroll
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                                acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
+                                acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
+                                acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
+                                acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
+                            }
+                        }
+                    }
+                }
+        }
+    }
+    // lanes l, l+16, l+32, l+48 hold the same column
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+        float v = acc[i];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        if (lane < kColTile) part[wave][i][lane] = v;
+    }
+    sync();
+    const int tid = wave * 64 + lane;
+    if (active && tid < B * kColTile) {
+        const int i = tid / kColTile, col = tid % kColTile;
+        const float y = ((part[0][i][col] + part[1][i][col]) + part[2][i][col]) + part[3][i][col];
+        const size_t m = (size_t)i * d + (size_t)tile * kColTile + col;
+        x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
+    }
+}
+
+
+}  // namespace ls
