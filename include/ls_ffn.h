@@ -225,8 +225,9 @@ typedef struct {
  * LS_E_UNSUPPORTED with HBM-resident weights; LS_E_INVAL on bad arguments;
  * LS_E_CAPACITY if the cache cannot hold a layer's list (plus, while
  * prefetching, the next layer's) with the running layer's blocks protected;
- * LS_E_DEVICE if a wait of the stage-consuming kernel ran out (2 s; reported
- * by the next flagged layer or by ls_ffn_sync). */
+ * LS_E_DEVICE if a wait of the stage-consuming kernel ran out
+ * (LS_CFG_STAGE_WAIT_US; reported by the next flagged layer or by
+ * ls_ffn_sync; the context then stays failed). */
 ls_status ls_decode_step_streamed(ls_ffn* ctx, float* x, int32_t k, int32_t n_stages, int32_t mode,
                                   int32_t k_spec, ls_stream_report* report);
 
@@ -300,9 +301,12 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    flags and one persistent launch per layer (allocates the flag words at
  *    the first use); 2 a host synchronisation after every stage.  The
  *    persistent launch is cooperative when LS_CFG_COOPERATIVE is 1.
+ *  LS_CFG_STAGE_WAIT_US: how long any one wait of the stage-consuming kernel
+ *    may take, in microseconds (default 2000000, range 1 .. 60000000); a wait
+ *    that runs out ends the kernel and the call fails with LS_E_DEVICE.
  * LS_E_INVAL on an unknown key or value. */
 enum { LS_CFG_DECODE_PATH = 0, LS_CFG_SPEC_BLOCKS = 1, LS_CFG_TRACE_WG = 2, LS_CFG_COOPERATIVE = 3,
-       LS_CFG_BATCH_MFMA = 4, LS_CFG_ZERO_SKIP = 5, LS_CFG_STREAM_SYNC = 6 };
+       LS_CFG_BATCH_MFMA = 4, LS_CFG_ZERO_SKIP = 5, LS_CFG_STREAM_SYNC = 6, LS_CFG_STAGE_WAIT_US = 7 };
 ls_status ls_configure(ls_ffn* ctx, int32_t key, int64_t value);
 
 /* Debug: after a fused ls_decode_step (B = 1), copy what it exchanged for

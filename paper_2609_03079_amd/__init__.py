@@ -33,7 +33,7 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
            "ls_debug_stages_done", "ls_last_error")
 (LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA, LS_CFG_ZERO_SKIP,
- LS_CFG_STREAM_SYNC) = range(7)
+ LS_CFG_STREAM_SYNC, LS_CFG_STAGE_WAIT_US) = range(8)
 LS_SYNC_EVENTS, LS_SYNC_FLAGS, LS_SYNC_HOST = range(3)
 PHASES = ("layer_start", "input_ready", "scores_published", "all_scores", "acts_gathered",
           "exact_ranked", "slot_map", "misses_done", "partials_ready", "output_published",

@@ -98,6 +98,7 @@ struct ls_ffn {
     uint32_t* stage_done = nullptr;  // pinned coherent host [L][kMaxStages] done words, then the status word
     uint32_t* stage_cnt = nullptr;   // device [2][kMaxStages]: the stage consumer's counters
     uint32_t stage_tag = 0;          // last tag handed out
+    int64_t stage_wait_us = 2000000; // LS_CFG_STAGE_WAIT_US
     std::vector<uint32_t> layer_tag; // per layer: tag of its latest flagged request
     std::vector<int> layer_stages;   // per layer: stages of that request
 
@@ -842,7 +843,7 @@ static ls_status launch_stage_consumer(ls_ffn* c, int32_t layer, const float* x_
     a.status = c->stage_done + L * ls::kMaxStages;
     a.tag = tag;
     for (int i = 0; i < n_stages; ++i) a.wait_on[i] = wait_on[i];
-    a.limit = 200000000ull;  // 2 s at 100 MHz
+    a.limit = (uint64_t)c->stage_wait_us * 100u;  // wall-clock ticks at 100 MHz
     LS_HIP(c, timed(c, LS_K_STAGE, [&] { return ls::launch_stage_consumer(s, a, c->n_wg, c->cooperative != 0, c->stream); }));
     LS_HIP(c, hipEventRecord(c->layer_done[(size_t)layer], c->stream));
     c->layer_done_recorded[(size_t)layer] = 1;
@@ -1071,6 +1072,11 @@ ls_status ls_configure(ls_ffn* c, int32_t key, int64_t value) {
             c->layer_stages.assign(L, 0);
         }
         c->stream_sync = (int)value;
+        return LS_OK;
+    }
+    if (key == LS_CFG_STAGE_WAIT_US) {
+        if (value < 1 || value > 60000000) return fail(c, LS_E_INVAL, "stage wait limit must be 1 us .. 60 s");
+        c->stage_wait_us = value;
         return LS_OK;
     }
     if (key == LS_CFG_ZERO_SKIP) {

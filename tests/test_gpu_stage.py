@@ -152,3 +152,23 @@ def test_flags_full_size_70b_layers_and_oracle():
                                       cfg.act, ws[0].threshold)
             assert rel_l2(host(x1)[0].astype(np.float64) - x0[0], y_ref) <= Y_TOL[cfg.dtype]
     assert np.array_equal(outs[lsffn.LS_SYNC_EVENTS], outs[lsffn.LS_SYNC_FLAGS])
+
+
+def test_flags_wait_timeout_fails_the_call_instead_of_hanging():
+    """A 1 us wait limit against a cold cache: the first stage's copies cannot land in time, so
+    the kernel's bounded arrival wait runs out, the kernel ends, and the call (or the sync)
+    reports a device error; the context stays failed and can still be destroyed."""
+    ws = [lsgen.layer_weights(CFG, l) for l in range(CFG.n_layers)]
+    f = _host_ctx(CFG, ws, SLOTS)
+    f.ls_configure(lsffn.LS_CFG_STREAM_SYNC, lsffn.LS_SYNC_FLAGS)
+    with pytest.raises(lsffn.LsError):
+        f.ls_configure(lsffn.LS_CFG_STAGE_WAIT_US, 0)
+    f.ls_configure(lsffn.LS_CFG_STAGE_WAIT_US, 1)
+    x = dev_f32(lsgen.tokens(CFG, 5, 1, 1)[0])
+    with pytest.raises(lsffn.LsError) as err:
+        f.ls_decode_step_streamed(x, CFG.k, 4, lsffn.LS_PREFETCH_NONE, CFG.k)
+        f.ls_ffn_sync()
+    assert "timed out" in str(err.value)
+    with pytest.raises(lsffn.LsError):
+        f.ls_ffn_sync()  # the failure is sticky
+    f.close()
