@@ -189,10 +189,20 @@ __global__ __launch_bounds__(64 * kStageWaves) void stage_consumer_kernel(StageA
     }
 }
 
+// The copy stream's own small kernels must find room on some compute unit while this kernel
+// occupies every one of them (the arrival words wait for them): a build whose waves would
+// leave fewer than 64 of a SIMD's 512 registers free is refused.
+constexpr int kFreeRegsPerSimd = 64;
+
 template <ls_dtype T, ls_act A>
 hipError_t launch_t(const Shape& s, const StageArgs& p, int grid, bool cooperative, hipStream_t st) {
     const void* fn = s.prenorm ? reinterpret_cast<const void*>(&stage_consumer_kernel<T, A, true>)
                                : reinterpret_cast<const void*>(&stage_consumer_kernel<T, A, false>);
+    hipFuncAttributes fa{};
+    hipError_t e = hipFuncGetAttributes(&fa, fn);
+    if (e != hipSuccess) return e;
+    const int regs = (fa.numRegs + 7) / 8 * 8;  // allocation granule of 8
+    if (regs * (kStageWaves / 4) > 512 - kFreeRegsPerSimd) return hipErrorInvalidConfiguration;
     StageArgs arg = p;
     void* args[] = {&arg};
     if (cooperative) return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(64 * kStageWaves), args, 0, st);
