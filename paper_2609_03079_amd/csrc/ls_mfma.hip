@@ -82,12 +82,21 @@ __device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
 }
 
 constexpr int kWaves = 4;
-constexpr int kUnroll = 8;  // K steps in flight per wave
+constexpr int kUnroll = 8;    // gate/up: K steps in flight per wave
+constexpr int kUnrollDn = 8;  // down: (entry, K step) items in flight per wave
+constexpr int kWavesDn = 8;   // down: waves per workgroup (one 16-column tile)
 
-// One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry); the 4 waves split
-// the d / 32 K steps.  a_buf[tok * F + e * blk + q] as the VALU kernel writes it.
-// x is the layer input; with RMS each lane also sums the squares of the x values it loads
-// (every (token, k) exactly once per workgroup) and the dot products are scaled at the end.
+// One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry).  The gate and up
+// rows of the group stream through LDS in chunks of 512 K values: each load instruction reads
+// one kilobyte of one row (row-contiguous reads stream far better than the 16-row x 64-byte
+// pattern of an MFMA operand), the 4 waves write them to LDS rows padded to 1040 bytes (so
+// that the 16 lanes reading one fragment column hit different banks), and each wave then runs
+// a quarter of the chunk's K steps from LDS while the next chunk's loads are in flight.
+// a_buf[tok * F + e * blk + q] as the VALU kernel writes it.  x is the layer input; with RMS
+// each lane also sums the squares of the x values it loads (every (token, k) exactly once per
+// workgroup) and the dot products are scaled at the end.
+constexpr int kChunkK = 512;                 // K values per chunk (1 KB of a 16-bit row)
+constexpr int kRowPitch = 2 * kChunkK + 16;  // LDS bytes per staged row
 template <ls_dtype T, ls_act A, bool RMS>
 __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
@@ -95,6 +104,7 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
     int end, float* __restrict__ a_buf) {
     using S = Split<T>;
+    __shared__ __attribute__((aligned(16))) uint8_t stage[32 * kRowPitch];  // rows 0-15 gate, 16-31 up
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int groups_per_entry = blk / 16;
     const int e = begin + (int)blockIdx.x / groups_per_entry;
@@ -111,45 +121,54 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     }
     const size_t row_bytes = (size_t)d * 2;
     const uint8_t* base = blocks + (size_t)slot * block_bytes;
-    const int row = r0 + (lane & 15);
-    const uint8_t* grow = base + (size_t)row * row_bytes;
-    const uint8_t* urow = base + (size_t)(blk + row) * row_bytes;
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
     const float* hrow = h + (size_t)(tok_ok ? tok : 0) * d;
-    const int ksteps = d / 32;
+    // staged row j of this wave's 8 loads: gate row r0 + j (j < 16) or up row r0 + j - 16
+    auto row_ptr = [&](int j) {
+        return base + (size_t)(j < 16 ? r0 + j : blk + r0 + j - 16) * row_bytes;
+    };
+    auto load_chunk = [&](int c0, u32x4 (&rw)[8]) {
+        const int bytes = 2 * min(kChunkK, d - c0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int j = wave + 4 * i;
+            rw[i] = lane * 16 < bytes ? ld_stream(reinterpret_cast<const u32x4*>(row_ptr(j) + (size_t)c0 * 2 + lane * 16))
+                                      : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
     f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
-    for (int k0 = wave; k0 < ksteps; k0 += kWaves * kUnroll) {
-        u32x4 rg[kUnroll], ru[kUnroll];
-        f32x4 hx[kUnroll][2];
+    u32x4 rw[8];
+    load_chunk(0, rw);
+    for (int c0 = 0; c0 < d; c0 += kChunkK) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int ks = k0 + kWaves * u;
-            const int kk = ks * 32 + 8 * (lane >> 4);  // this lane's 8 K values
-            const bool ok = ks < ksteps;
-            rg[u] = ok ? ld_stream(reinterpret_cast<const u32x4*>(grow + (size_t)kk * 2)) : u32x4{0u, 0u, 0u, 0u};
-            ru[u] = ok ? ld_stream(reinterpret_cast<const u32x4*>(urow + (size_t)kk * 2)) : u32x4{0u, 0u, 0u, 0u};
+        for (int i = 0; i < 8; ++i)
+            *reinterpret_cast<u32x4*>(stage + (wave + 4 * i) * kRowPitch + lane * 16) = rw[i];
+        __syncthreads();
+        if (c0 + kChunkK < d) load_chunk(c0 + kChunkK, rw);  // in flight while this chunk runs
+        const int steps = min(kChunkK, d - c0) / 32;
+        for (int s0 = wave; s0 < steps; s0 += 4) {
+            const int kc = 32 * s0 + 8 * (lane >> 4);  // this lane's 8 K values in the chunk
             const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-            hx[u][0] = ok && tok_ok ? reinterpret_cast<const f32x4*>(hrow + kk)[0] : z;
-            hx[u][1] = ok && tok_ok ? reinterpret_cast<const f32x4*>(hrow + kk)[1] : z;
-        }
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const float xv[8] = {hx[u][0].x, hx[u][0].y, hx[u][0].z, hx[u][0].w,
-                                 hx[u][1].x, hx[u][1].y, hx[u][1].z, hx[u][1].w};
+            const f32x4 h0 = tok_ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[0] : z;
+            const f32x4 h1 = tok_ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[1] : z;
+            const float xv[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
             if (RMS) {
 #pragma unroll
                 for (int i = 0; i < 8; ++i) ss = fmaf(xv[i], xv[i], ss);
             }
             typename S::vec hi, lo;
             S::run(xv, hi, lo);
-            const typename S::vec wg = S::from_raw(rg[u]), wu = S::from_raw(ru[u]);
+            const u32x4 wg4 = *reinterpret_cast<const u32x4*>(stage + (lane & 15) * kRowPitch + kc * 2);
+            const u32x4 wu4 = *reinterpret_cast<const u32x4*>(stage + (16 + (lane & 15)) * kRowPitch + kc * 2);
+            const typename S::vec wg = S::from_raw(wg4), wu = S::from_raw(wu4);
             cg = S::mfma(wg, hi, cg);
             cg = S::mfma(wg, lo, cg);
             cu = S::mfma(wu, hi, cu);
             cu = S::mfma(wu, lo, cu);
         }
+        __syncthreads();  // every wave is done with the chunk before it is overwritten
     }
     // lane l holds rows 4 (l / 16) + i, token l % 16 of this wave's partial sums
     __shared__ float pg[kWaves][16][16], pu[kWaves][16][16], pss[kWaves][16];
@@ -185,7 +204,7 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
 // of a block for one tile is [blk/8][16][8]: K step s of an entry is the contiguous kilobyte
 // of chunks 64 s .. 64 s + 63, exactly one A fragment.
 template <ls_dtype T>
-__global__ __launch_bounds__(256) void down_mfma_kernel(
+__global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int B, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
@@ -198,40 +217,44 @@ __global__ __launch_bounds__(256) void down_mfma_kernel(
     const int ksteps = blk / 32;
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
+    // the cache slot of every entry of the range (-1: invalid id or absent), resolved once so
+    // that each work item waits only for its weight load
+    __shared__ int slots[kMaxBlocks];
+    for (int e = begin + (int)threadIdx.x; e < n_end; e += 64 * kWavesDn) {
+        const int b = idx[e];
+        slots[e - begin] = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
+    }
+    __syncthreads();
     f32x4v c = {0.f, 0.f, 0.f, 0.f};
-    // work items (entry, K step) of the list range, dealt to the waves round-robin; kUnroll
+    // work items (entry, K step) of the list range, dealt to the waves round-robin; kUnrollDn
     // items per wave are in flight together
     const long items = (long)(n_end - begin) * ksteps;
-    for (long i0 = wave; i0 < items; i0 += (long)kWaves * kUnroll) {
-        const u32x4* src[kUnroll];
-        const float* arow[kUnroll];
-        bool live[kUnroll];
+    for (long i0 = wave; i0 < items; i0 += (long)kWavesDn * kUnrollDn) {
+        const u32x4* src[kUnrollDn];
+        const float* arow[kUnrollDn];
+        bool live[kUnrollDn];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const long it = i0 + (long)kWaves * u;
+        for (int u = 0; u < kUnrollDn; ++u) {
+            const long it = i0 + (long)kWavesDn * u;
             const int e = begin + (int)(it / ksteps), s = (int)(it % ksteps);
             live[u] = it < items;
-            int slot = -1;
-            if (live[u]) {
-                const int b = idx[e];
-                slot = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
-            }
+            const int slot = live[u] ? slots[e - begin] : -1;
             live[u] = live[u] && slot >= 0;  // an invalid or absent block contributes nothing
             src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
                                                     down_off) + 64 * s + lane;
             arow[u] = a_buf + (size_t)(tok_ok ? tok : 0) * F + (size_t)e * blk + 32 * s + 8 * (lane >> 4);
         }
-        u32x4 w[kUnroll];
-        f32x4 av[kUnroll][2];
+        u32x4 w[kUnrollDn];
+        f32x4 av[kUnrollDn][2];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kUnrollDn; ++u) {
             const f32x4 z = {0.f, 0.f, 0.f, 0.f};
             w[u] = live[u] ? ld_stream(src[u]) : u32x4{0u, 0u, 0u, 0u};
             av[u][0] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[0] : z;
             av[u][1] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[1] : z;
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kUnrollDn; ++u) {
             const float xv[8] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w,
                                  av[u][1].x, av[u][1].y, av[u][1].z, av[u][1].w};
             typename S::vec hi, lo;
@@ -242,13 +265,15 @@ __global__ __launch_bounds__(256) void down_mfma_kernel(
         }
     }
     // lane l holds columns 4 (l / 16) + i of the tile for token l % 16
-    __shared__ float part[kWaves][16][16];
+    __shared__ float part[kWavesDn][16][16];
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[wave][4 * (lane >> 4) + i][lane & 15] = c[i];
     __syncthreads();
     if (threadIdx.x < 16 * B) {
         const int t = threadIdx.x / 16, col = threadIdx.x % 16;
-        const float y = ((part[0][col][t] + part[1][col][t]) + part[2][col][t]) + part[3][col][t];
+        float y = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWavesDn; ++w) y += part[w][col][t];
         const size_t m = (size_t)t * d + (size_t)tile * kColTile + col;
         x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
     }
@@ -296,7 +321,7 @@ hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* sl
                             const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                             int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
     const size_t bb = s.block_elems * elem_size(s.dtype);
-    const dim3 grid(s.d / kColTile), blk(256);
+    const dim3 grid(s.d / kColTile), blk(64 * kWavesDn);
     if (s.dtype == LS_F16)
         hipLaunchKernelGGL(down_mfma_kernel<LS_F16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
                            B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
