@@ -83,8 +83,8 @@ __device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
 
 constexpr int kWaves = 4;
 constexpr int kUnroll = 8;    // gate/up: K steps in flight per wave
-constexpr int kUnrollDn = 8;  // down: (entry, K step) items in flight per wave
-constexpr int kWavesDn = 8;   // down: waves per workgroup (one 16-column tile)
+constexpr int kUnrollDn = 4;  // down: (entry, K step) items in flight per wave
+constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
 
 // One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry).  The gate and up
 // rows of the group stream through LDS in chunks of 512 K values: each load instruction reads
@@ -171,7 +171,12 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
         __syncthreads();  // every wave is done with the chunk before it is overwritten
     }
     // lane l holds rows 4 (l / 16) + i, token l % 16 of this wave's partial sums
-    __shared__ float pg[kWaves][16][16], pu[kWaves][16][16], pss[kWaves][16];
+    // the partial sums reuse the staging buffer (every wave is past the last chunk), so that
+    // four workgroups fit in a compute unit's LDS
+    static_assert(sizeof(float) * (2 * kWaves * 16 * 16 + kWaves * 16) <= sizeof(stage), "epilogue fits the stage");
+    float (&pg)[kWaves][16][16] = *reinterpret_cast<float (*)[kWaves][16][16]>(stage);
+    float (&pu)[kWaves][16][16] = *reinterpret_cast<float (*)[kWaves][16][16]>(stage + sizeof(float) * kWaves * 16 * 16);
+    float (&pss)[kWaves][16] = *reinterpret_cast<float (*)[kWaves][16]>(stage + 2 * sizeof(float) * kWaves * 16 * 16);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         pg[wave][4 * (lane >> 4) + i][lane & 15] = cg[i];
