@@ -21,46 +21,61 @@ namespace {
 
 // ---- GEMV over rows: out[b, row] = c_b * sum_c W[row, c] * v[b, c] ------------------------
 // c_b = rms_scale of v[b, :] when RMS (the MLP input of a prenorm stack), else 1.
-template <ls_dtype T, int B, bool RMS>
+// One workgroup per R rows; its 4 waves split the rows' 16-byte chunks, then a fixed-order
+// sum of the 4 wave totals.  The R rows share the input reads (with B tokens the input is B
+// times the bytes of a row); every row's dot product is summed in the same order for any R.
+template <ls_dtype T, int B, bool RMS, int R>
 __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
                                                         int cols, int G, int rpw,
                                                         const float* __restrict__ v,
                                                         float* __restrict__ out) {
-    // one workgroup per row; its 4 waves split the row's 16-byte chunks, then a fixed-order
-    // sum of the 4 wave totals
     constexpr int V = Wt<T>::V;
-    constexpr int U = 4;  // 16-byte loads in flight per lane
+    constexpr int U = 4;  // 16-byte loads in flight per lane and row
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int row = blockIdx.x;
+    const int row0 = blockIdx.x * R;
     const int nchunk = cols / V;
-    const int srow = (row % G) * rpw + row / G;
-    const u32x4* wr = reinterpret_cast<const u32x4*>(W + (size_t)srow * cols * Wt<T>::kBytes);
-    float acc[B], ss[B];
+    const u32x4* wr[R];
 #pragma unroll
-    for (int b = 0; b < B; ++b) acc[b] = ss[b] = 0.f;
+    for (int r = 0; r < R; ++r) {
+        const int row = min(row0 + r, rows - 1);  // rows past the end repeat the last one, unstored
+        const int srow = (row % G) * rpw + row / G;
+        wr[r] = reinterpret_cast<const u32x4*>(W + (size_t)srow * cols * Wt<T>::kBytes);
+    }
+    float acc[R][B], ss[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        ss[b] = 0.f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r][b] = 0.f;
+    }
     for (int c0 = threadIdx.x; c0 < nchunk; c0 += 256 * U) {
-        u32x4 raw[U];
+        u32x4 raw[U][R];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 256;
-            raw[u] = c < nchunk ? ld_stream(wr + c) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int r = 0; r < R; ++r) raw[u][r] = c < nchunk ? ld_stream(wr[r] + c) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 256;
             if (c < nchunk) {
-                float w[V];
-                Wt<T>::widen(raw[u], w);
+                float w[R][V];
+#pragma unroll
+                for (int r = 0; r < R; ++r) Wt<T>::widen(raw[u][r], w[r]);
 #pragma unroll
                 for (int b = 0; b < B; ++b) {
                     const f32x4* vp = reinterpret_cast<const f32x4*>(v + (size_t)b * cols + (size_t)c * V);
 #pragma unroll
                     for (int q = 0; q < V / 4; ++q) {
                         const f32x4 x4 = vp[q];
-                        acc[b] = fmaf(w[4 * q + 0], x4.x, acc[b]);
-                        acc[b] = fmaf(w[4 * q + 1], x4.y, acc[b]);
-                        acc[b] = fmaf(w[4 * q + 2], x4.z, acc[b]);
-                        acc[b] = fmaf(w[4 * q + 3], x4.w, acc[b]);
+#pragma unroll
+                        for (int r = 0; r < R; ++r) {
+                            acc[r][b] = fmaf(w[r][4 * q + 0], x4.x, acc[r][b]);
+                            acc[r][b] = fmaf(w[r][4 * q + 1], x4.y, acc[r][b]);
+                            acc[r][b] = fmaf(w[r][4 * q + 2], x4.z, acc[r][b]);
+                            acc[r][b] = fmaf(w[r][4 * q + 3], x4.w, acc[r][b]);
+                        }
                         if (RMS) {
                             ss[b] = fmaf(x4.x, x4.x, ss[b]);
                             ss[b] = fmaf(x4.y, x4.y, ss[b]);
@@ -72,22 +87,23 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
             }
         }
     }
-    __shared__ float part[4][B], pss[4][B];
+    __shared__ float part[4][R][B], pss[4][B];
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-        const float s = wave_sum_dpp(acc[b]);
-        const float q = RMS ? wave_sum_dpp(ss[b]) : 0.f;
-        if (lane == 0) {
-            part[wave][b] = s;
-            pss[wave][b] = q;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float s = wave_sum_dpp(acc[r][b]);
+            if (lane == 0) part[wave][r][b] = s;
         }
+        const float q = RMS ? wave_sum_dpp(ss[b]) : 0.f;
+        if (lane == 0) pss[wave][b] = q;
     }
     __syncthreads();
-    if (threadIdx.x < B) {
-        const int b = threadIdx.x;
-        const float dot = ((part[0][b] + part[1][b]) + part[2][b]) + part[3][b];
+    if (threadIdx.x < R * B) {
+        const int r = threadIdx.x / B, b = threadIdx.x % B;
+        const float dot = ((part[0][r][b] + part[1][r][b]) + part[2][r][b]) + part[3][r][b];
         const float sc = RMS ? rms_scale(((pss[0][b] + pss[1][b]) + pss[2][b]) + pss[3][b], cols) : 1.f;
-        out[(size_t)b * rows + row] = dot * sc;
+        if (row0 + r < rows) out[(size_t)b * rows + row0 + r] = dot * sc;
     }
 }
 
@@ -257,19 +273,23 @@ __global__ __launch_bounds__(256) void down_kernel(
 template <ls_dtype T, bool RMS>
 static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, const float* v, int B,
                          float* out, hipStream_t st) {
-    const dim3 grid(rows), blk(256);
+    // four rows per workgroup once the batch makes the input reads dominate
+    const int R = B >= 4 ? 4 : 1;
+    const dim3 grid((unsigned)((rows + R - 1) / R)), blk(256);
     const uint8_t* w = static_cast<const uint8_t*>(W);
+#define LS_GEMV(NB, NR) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
     switch (B) {
-        case 1: hipLaunchKernelGGL((gemv_rows_kernel<T, 1, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 2: hipLaunchKernelGGL((gemv_rows_kernel<T, 2, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 3: hipLaunchKernelGGL((gemv_rows_kernel<T, 3, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 4: hipLaunchKernelGGL((gemv_rows_kernel<T, 4, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 5: hipLaunchKernelGGL((gemv_rows_kernel<T, 5, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 6: hipLaunchKernelGGL((gemv_rows_kernel<T, 6, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 7: hipLaunchKernelGGL((gemv_rows_kernel<T, 7, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
-        case 8: hipLaunchKernelGGL((gemv_rows_kernel<T, 8, RMS>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out); break;
+        case 1: LS_GEMV(1, 1); break;
+        case 2: LS_GEMV(2, 1); break;
+        case 3: LS_GEMV(3, 1); break;
+        case 4: LS_GEMV(4, 4); break;
+        case 5: LS_GEMV(5, 4); break;
+        case 6: LS_GEMV(6, 4); break;
+        case 7: LS_GEMV(7, 4); break;
+        case 8: LS_GEMV(8, 4); break;
         default: return hipErrorInvalidValue;
     }
+#undef LS_GEMV
     return hipGetLastError();
 }
 

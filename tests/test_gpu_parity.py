@@ -72,16 +72,19 @@ def _check_y(f, ws_l, cfg, xin, yg, blocks, tol, tag):
         assert rel_l2(yg[b], y_ref) <= tol, (tag, b, rel_l2(yg[b], y_ref))
 
 
+@pytest.mark.parametrize("B", [1, 4, 7, 8])
 @pytest.mark.parametrize("name", list(SMALL))
-def test_predict_parity(name):
+def test_predict_parity(name, B):
+    """Batches of 4+ compute four predictor rows per workgroup; the shapes include row counts
+    that are not a multiple of four (50 and 27 blocks) and both the folded and factored forms."""
     cfg = SMALL[name]
-    f, ws = make_ffn(cfg, max_batch=4)
-    xs = lsgen.tokens(cfg, 0, 1, 4)[0]
-    scores = empty_f32(4, cfg.n_blk)
+    f, ws = make_ffn(cfg, max_batch=B)
+    xs = lsgen.tokens(cfg, 0, 1, B)[0]
+    scores = empty_f32(B, cfg.n_blk)
     for l in range(cfg.n_layers):
-        f.ls_predict(l, dev_f32(xs), 4, scores)
+        f.ls_predict(l, dev_f32(xs), B, scores)
         got = host(scores)
-        for b in range(4):
+        for b in range(B):
             ref = oracle.predict(ws[l].p1, ws[l].p2, oracle.mlp_input(xs[b], cfg.prenorm))
             assert rel_l2(got[b], ref) <= SCORE_TOL, (name, l, b)
 
