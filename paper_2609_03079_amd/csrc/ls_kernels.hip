@@ -115,34 +115,58 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
 // are compacted by ballot prefix, then ranked among themselves (key descending, index
 // ascending) so the output is in priority order.  Union: the OR of the tokens' sets, ranked
 // by each block's largest key over all tokens.
+// Ranking packs (key, 0xffff - index) into one 64-bit word, so the priority order is the
+// descending order of distinct words and a member's rank is the count of larger words; the
+// lists are padded with zero words (below every member) to a multiple of 8 so the count
+// runs 8 independent LDS reads at a time.
 // Q: keys per lane (n <= 64 Q); small lists get a small unrolled body.
+__device__ inline uint64_t rank_word(uint32_t key, int i) {
+    return ((uint64_t)key << 32) | (uint32_t)(0xffff - i);
+}
+
+__device__ inline int rank_in(const uint64_t* __restrict__ w, int n_pad, uint64_t mine) {
+    int rank = 0;
+#pragma unroll 1
+    for (int j = 0; j < n_pad; j += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rank += w[j + u] > mine;
+    }
+    return rank;
+}
+
 template <int Q>
-__global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ scores, int B,
+__global__ __launch_bounds__(Q > 8 ? 512 : 1024) void select_kernel(const float* __restrict__ scores, int B,
                                                       int n, int mode, int k, float tau,
                                                       int union_batch, int cap,
                                                       int32_t* __restrict__ idx,
                                                       int32_t* __restrict__ count) {
-    __shared__ uint32_t key[kMaxBatch][kMaxBlocks];
-    __shared__ uint8_t memb[kMaxBatch][kMaxBlocks];
-    __shared__ int16_t mlist[kMaxBatch][kMaxBlocks];
-    __shared__ int16_t ulist[kMaxBlocks];
-    __shared__ uint32_t ukey[kMaxBlocks];  // union member p: largest key over all tokens
+    // per token: its members' rank words; with a union, row 0 holds the union's instead
+    __shared__ uint64_t mk[kMaxBatch][kMaxBlocks];
+    __shared__ uint32_t bkey[kMaxBlocks];           // union: largest key of block i over all tokens
+    __shared__ uint32_t umask[kMaxBlocks / 32];     // union: OR of the tokens' member sets
     __shared__ int ucount;
     const int tid = threadIdx.x, nt = blockDim.x;
     const int wave = tid >> 6, lane = tid & 63, nwaves = nt >> 6;
     const bool do_union = union_batch && B > 1;
     const uint64_t below = (1ull << lane) - 1ull;
     const int Qn = (n + 63) / 64;
+    if (do_union) {
+        for (int i = tid; i < n; i += nt) bkey[i] = 0u;
+        for (int i = tid; i < (n + 31) / 32; i += nt) umask[i] = 0u;
+        __syncthreads();
+    }
     for (int b = wave; b < B; b += nwaves) {
+        // all Q loads in flight before the first use (indices past n re-read entry n - 1, n >= 1)
+        float sv[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) sv[q] = scores[(size_t)b * n + min(q * 64 + lane, n - 1)];
+        // entries past n get key 0: below every search candidate (>= 1) and never > T
         uint32_t ok[Q];
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
             const int i = q * 64 + lane;
-            ok[q] = 0u;
-            if (q < Qn && i < n) {
-                ok[q] = order_key(scores[(size_t)b * n + i]);
-                key[b][i] = ok[q];
-            }
+            ok[q] = i < n ? order_key(sv[q]) : 0u;
+            if (do_union && i < n) atomicMax(&bkey[i], ok[q]);
         }
         // membership rule: key > T, or key == T among the first `rem` such by index
         uint32_t T = 0u;
@@ -153,14 +177,12 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
                 const uint32_t c = T | (1u << bit);
                 int cnt = 0;
 #pragma unroll
-                for (int q = 0; q < Q; ++q)
-                    if (q < Qn) cnt += __popcll(__ballot(ok[q] >= c));
+                for (int q = 0; q < Q; ++q) cnt += __popcll(__ballot(ok[q] >= c));
                 if (cnt >= k) T = c;
             }
             int gt = 0;
 #pragma unroll
-            for (int q = 0; q < Q; ++q)
-                if (q < Qn) gt += __popcll(__ballot(ok[q] > T));
+            for (int q = 0; q < Q; ++q) gt += __popcll(__ballot(ok[q] > T));
             rem = k - gt;
         }
         const uint32_t ktau = isnan(tau) ? 0xffffffffu : order_key(tau);
@@ -180,61 +202,47 @@ __global__ __launch_bounds__(1024) void select_kernel(const float* __restrict__ 
                     eq_before += __popcll(eqb);
                 }
                 const uint64_t mb = __ballot(mem);
-                if (valid) memb[b][i] = mem ? 1 : 0;
-                if (mem) mlist[b][m + __popcll(mb & below)] = (int16_t)i;
+                if (mem) {
+                    if (do_union)
+                        atomicOr(&umask[i >> 5], 1u << (i & 31));
+                    else
+                        mk[b][m + __popcll(mb & below)] = rank_word(ok[q], i);
+                }
                 m += __popcll(mb);
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
         if (!do_union) {
+            const int m_pad = (m + 7) & ~7;
+            if (lane < m_pad - m) mk[b][m + lane] = 0ull;
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
             for (int p = lane; p < m; p += 64) {
-                const int ip = mlist[b][p];
-                const uint32_t kp = key[b][ip];
-                int rank = 0;
-                for (int j = 0; j < m; ++j) {
-                    const int ij = mlist[b][j];
-                    const uint32_t kj = key[b][ij];
-                    rank += (kj > kp) | ((kj == kp) & (ij < ip));
-                }
-                idx[(size_t)b * cap + rank] = ip;
+                const uint64_t mine = mk[b][p];
+                idx[(size_t)b * cap + rank_in(mk[b], m_pad, mine)] = 0xffff - (int)(uint32_t)mine;
             }
             if (lane == 0) count[b] = m;
         }
     }
     if (!do_union) return;
     __syncthreads();
-    // union members and their keys (largest over all tokens), compacted by wave 0
+    // union members with their largest keys, compacted by wave 0 into row 0
     if (wave == 0) {
         int u = 0;
         for (int q = 0; q < Qn; ++q) {
             const int i = q * 64 + lane;
-            bool in = false;
-            if (i < n)
-                for (int b = 0; b < B; ++b) in |= memb[b][i] != 0;
+            const bool in = i < n && ((umask[i >> 5] >> (i & 31)) & 1u);
             const uint64_t ub = __ballot(in);
-            if (in) ulist[u + __popcll(ub & below)] = (int16_t)i;
+            if (in) mk[0][u + __popcll(ub & below)] = rank_word(bkey[i], i);
             u += __popcll(ub);
         }
+        const int u_pad = (u + 7) & ~7;
+        if (lane < u_pad - u) mk[0][u + lane] = 0ull;
         if (lane == 0) ucount = u;
     }
     __syncthreads();
-    const int U = ucount;
+    const int U = ucount, U_pad = (U + 7) & ~7;
     for (int p = tid; p < U; p += nt) {
-        const int ip = ulist[p];
-        uint32_t kp = 0u;
-        for (int b = 0; b < B; ++b) kp = key[b][ip] > kp ? key[b][ip] : kp;
-        ukey[p] = kp;
-    }
-    __syncthreads();
-    for (int p = tid; p < U; p += nt) {
-        const int ip = ulist[p];
-        const uint32_t kp = ukey[p];
-        int rank = 0;
-        for (int j = 0; j < U; ++j) {
-            const uint32_t kj = ukey[j];
-            rank += (kj > kp) | ((kj == kp) & ((int)ulist[j] < ip));
-        }
-        idx[rank] = ip;
+        const uint64_t mine = mk[0][p];
+        idx[rank_in(mk[0], U_pad, mine)] = 0xffff - (int)(uint32_t)mine;
     }
     if (tid == 0) count[0] = U;
 }
@@ -361,7 +369,8 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
     // one wave per token; more waves share the union ranking
     int waves = (n_blk + 63) / 64;
     waves = waves < B ? B : waves;
-    waves = waves > 16 ? 16 : waves;
+    const int max_waves = n_blk <= 512 ? 16 : 8;  // the widest body needs 256 registers a lane
+    waves = waves > max_waves ? max_waves : waves;
     const int threads = 64 * waves;
     auto fn = n_blk <= 256 ? select_kernel<4> : n_blk <= 512 ? select_kernel<8> : select_kernel<kMaxBlocks / 64>;
     hipLaunchKernelGGL(fn, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
