@@ -38,6 +38,7 @@ struct ls_ffn {
     int32_t* count = nullptr; // [maxB]
     float* a = nullptr;       // [maxB, F]
     float* xbuf = nullptr;    // [maxB, d]  ping-pong partner of the decode step
+    float* dn_part = nullptr; // [kDownSplits, maxB, d]  parts of the split down projection
     int64_t last_act_n = 0;
     int32_t last_act_B = 0;
 
@@ -291,7 +292,7 @@ void free_all(ls_ffn* c) {
     for (auto& h : c->hash) if (h.w1) (void)hipFree(h.w1);  // one allocation per layer
     c->hash.clear();
     for (void* p : {(void*)c->z, (void*)c->scores, (void*)c->idx, (void*)c->count,
-                    (void*)c->a, (void*)c->xbuf, (void*)c->cache, (void*)c->slot_tables,
+                    (void*)c->a, (void*)c->xbuf, (void*)c->dn_part, (void*)c->cache, (void*)c->slot_tables,
                     (void*)c->mailbox, (void*)c->layer_tab, (void*)c->dev_err, (void*)c->spec_idx,
                     (void*)c->trace, (void*)c->stage_cnt})
         if (p) (void)hipFree(p);
@@ -441,7 +442,8 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
     if (dmalloc(&c->z, (size_t)B * (s.fold ? 1 : s.r)) != hipSuccess ||
         dmalloc(&c->scores, (size_t)B * s.n_blk) != hipSuccess ||
         dmalloc(&c->idx, (size_t)B * s.n_blk) != hipSuccess || dmalloc(&c->count, (size_t)B) != hipSuccess ||
-        dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess) {
+        dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess ||
+        dmalloc(&c->dn_part, (size_t)ls::kDownSplits * B * s.d) != hipSuccess) {
         (void)hipGetLastError();
         return bail(LS_E_NOMEM, "workspace allocation failed");
     }
@@ -639,7 +641,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
         if (st != LS_OK) return st;
     }
     LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, x_in, B, idx, count, begin, end, c->a, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->stream); }));
+    LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->dn_part, c->stream); }));
     if (c->desc.residency == LS_WEIGHTS_HOST) {
         LS_HIP(c, hipEventRecord(c->layer_done[layer], c->stream));
         c->layer_done_recorded[layer] = 1;
@@ -1015,7 +1017,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count, c->stream);
         }));
         LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, nullptr, cur, B, c->idx, c->count, 0, cap, c->a, c->stream); }));
-        LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->stream); }));
+        LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->dn_part, c->stream); }));
         std::swap(cur, nxt);
     }
     if (cur != x)

@@ -91,9 +91,12 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
 hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* x, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, float* a_buf, hipStream_t st);
+// part: [kDownSplits, B, d] floats of scratch for the matrix-core path's split list (may be
+// null: no split)
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
-                       int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
+                       int begin, int end, const float* x_in, float* x_acc, float* part,
+                       hipStream_t st);
 
 // ---- persistent consumer of a streamed layer's copy stages (ls_stage.hip) ----------------
 constexpr int kMaxStages = 64;
@@ -126,8 +129,10 @@ bool mfma_path(const Shape& s, int B);
 hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                               const float* x, int B, const int32_t* idx, const int32_t* count,
                               int begin, int end, float* a_buf, hipStream_t st);
+constexpr int kDownSplits = 4;  // list parts of the matrix-core down projection (divides 16)
 hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                             const float* a_buf, int B, const int32_t* idx, const int32_t* count,
-                            int begin, int end, const float* x_in, float* x_acc, hipStream_t st);
+                            int begin, int end, const float* x_in, float* x_acc, float* part,
+                            hipStream_t st);
 
 }  // namespace ls

@@ -465,9 +465,10 @@ static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_
 
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
-                       int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+                       int begin, int end, const float* x_in, float* x_acc, float* part,
+                       hipStream_t st) {
     if (s.batch_mfma && !s.zero_skip && mfma_path(s, B))
-        return launch_down_mfma(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
+        return launch_down_mfma(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, part, st);
     switch (s.dtype) {
         case LS_F32: return down_t<LS_F32>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);
         case LS_F16: return down_t<LS_F16>(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, st);

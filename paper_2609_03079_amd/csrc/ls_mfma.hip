@@ -205,45 +205,54 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
     }
 }
 
-// One workgroup per 16-column tile of y; the waves split the list entries.  The down piece
-// of a block for one tile is [blk/8][16][8]: K step s of an entry is the contiguous kilobyte
-// of chunks 64 s .. 64 s + 63, exactly one A fragment.
+// One workgroup per 16-column tile of y and part of the list; its waves split that part's
+// entries.  The down piece of a block for one tile is [blk/8][16][8]: K step s of an entry
+// is the contiguous kilobyte of chunks 64 s .. 64 s + 63, exactly one A fragment.
+// With splits > 1 the list range is cut into `splits` equal parts (workgroup
+// tile + n_tiles * part) so that the workgroup count is a multiple of the CU count even when
+// the tile count is not; each part's sum goes to part_out[part][token][column] and
+// down_finish_kernel adds the parts in order.  The wave count is blockDim.x / 64.
 template <ls_dtype T>
 __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int B, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
-    const float* __restrict__ x_in, float* __restrict__ x_acc) {
+    const float* __restrict__ x_in, float* __restrict__ x_acc, int splits,
+    float* __restrict__ part_out) {
     using S = Split<T>;
-    const int tile = blockIdx.x;
+    const int n_tiles = d / kColTile;
+    const int tile = (int)blockIdx.x % n_tiles, sp = (int)blockIdx.x / n_tiles;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int n_end = list_end_m(count, end, n_blk);
+    const int n_waves = (int)(blockDim.x >> 6);
+    const int len = max(0, list_end_m(count, end, n_blk) - begin);
+    const int e0 = begin + (int)((long)len * sp / splits);
+    const int e1 = begin + (int)((long)len * (sp + 1) / splits);
     const size_t down_off = (size_t)2 * blk * d * 2 + (size_t)tile * blk * kColTile * 2;
     const int ksteps = blk / 32;
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
-    // the cache slot of every entry of the range (-1: invalid id or absent), resolved once so
+    // the cache slot of every entry of the part (-1: invalid id or absent), resolved once so
     // that each work item waits only for its weight load
     __shared__ int slots[kMaxBlocks];
-    for (int e = begin + (int)threadIdx.x; e < n_end; e += 64 * kWavesDn) {
+    for (int e = e0 + (int)threadIdx.x; e < e1; e += (int)blockDim.x) {
         const int b = idx[e];
-        slots[e - begin] = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
+        slots[e - e0] = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
     }
     __syncthreads();
     f32x4v c = {0.f, 0.f, 0.f, 0.f};
-    // work items (entry, K step) of the list range, dealt to the waves round-robin; kUnrollDn
-    // items per wave are in flight together
-    const long items = (long)(n_end - begin) * ksteps;
-    for (long i0 = wave; i0 < items; i0 += (long)kWavesDn * kUnrollDn) {
+    // work items (entry, K step) of the part, dealt to the waves round-robin; kUnrollDn items
+    // per wave are in flight together
+    const long items = (long)(e1 - e0) * ksteps;
+    for (long i0 = wave; i0 < items; i0 += (long)n_waves * kUnrollDn) {
         const u32x4* src[kUnrollDn];
         const float* arow[kUnrollDn];
         bool live[kUnrollDn];
 #pragma unroll
         for (int u = 0; u < kUnrollDn; ++u) {
-            const long it = i0 + (long)kWavesDn * u;
-            const int e = begin + (int)(it / ksteps), s = (int)(it % ksteps);
+            const long it = i0 + (long)n_waves * u;
+            const int e = e0 + (int)(it / ksteps), s = (int)(it % ksteps);
             live[u] = it < items;
-            const int slot = live[u] ? slots[e - begin] : -1;
+            const int slot = live[u] ? slots[e - e0] : -1;
             live[u] = live[u] && slot >= 0;  // an invalid or absent block contributes nothing
             src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
                                                     down_off) + 64 * s + lane;
@@ -277,11 +286,24 @@ __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     if (threadIdx.x < 16 * B) {
         const int t = threadIdx.x / 16, col = threadIdx.x % 16;
         float y = 0.f;
-#pragma unroll
-        for (int w = 0; w < kWavesDn; ++w) y += part[w][col][t];
+        for (int w = 0; w < n_waves; ++w) y += part[w][col][t];
         const size_t m = (size_t)t * d + (size_t)tile * kColTile + col;
-        x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
+        if (splits == 1)
+            x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
+        else
+            part_out[(size_t)sp * B * d + m] = y;
     }
+}
+
+// x_acc[m] = (x_in or x_acc)[m] + the parts' sums for m in order of part
+__global__ __launch_bounds__(256) void down_finish_kernel(const float* __restrict__ part, int splits,
+                                                          int n, const float* __restrict__ x_in,
+                                                          float* __restrict__ x_acc, int first) {
+    const int m = (int)blockIdx.x * 256 + (int)threadIdx.x;
+    if (m >= n) return;
+    float y = 0.f;
+    for (int p = 0; p < splits; ++p) y += part[(size_t)p * n + m];
+    x_acc[m] = (first ? x_in[m] : x_acc[m]) + y;
 }
 
 }  // namespace
@@ -322,19 +344,36 @@ hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* 
     return hipGetLastError();
 }
 
+int down_splits(const Shape& s) {
+    // tiles that do not fill whole rounds of the CUs: cut the list in kDownSplits parts
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        return 1;
+    return (s.d / kColTile) % cus == 0 ? 1 : kDownSplits;
+}
+
 hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                             const float* a_buf, int B, const int32_t* idx, const int32_t* count,
-                            int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
+                            int begin, int end, const float* x_in, float* x_acc, float* part,
+                            hipStream_t st) {
     const size_t bb = s.block_elems * elem_size(s.dtype);
-    const dim3 grid(s.d / kColTile), blk(64 * kWavesDn);
+    const int splits = part ? down_splits(s) : 1;
+    // the same number of waves per tile either way: 16 in one workgroup or 16 / splits in each
+    const dim3 grid((unsigned)(s.d / kColTile * splits)), blk(64 * kWavesDn / splits);
     if (s.dtype == LS_F16)
         hipLaunchKernelGGL(down_mfma_kernel<LS_F16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
-                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, splits, part);
     else if (s.dtype == LS_BF16)
         hipLaunchKernelGGL(down_mfma_kernel<LS_BF16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
-                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, splits, part);
     else
         return hipErrorInvalidValue;
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int n = B * s.d;
+    hipLaunchKernelGGL(down_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, splits, n,
+                       x_in, x_acc, begin == 0 ? 1 : 0);
     return hipGetLastError();
 }
 

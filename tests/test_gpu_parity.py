@@ -343,6 +343,9 @@ MFMA_CMP = {
     "f16_b64": SMALL["f16_b64"],
     "bf16_reglu": C["mistral_7b_ffn"].with_(n_layers=1, d_model=512, d_ff=2048, block=128, rank=128,
                                             keep_pct=50, act=lsgen.ACT_REGLU),
+    # 256 column tiles: the down projection runs unsplit (the two above split the list in 4)
+    "f16_d4096": C["llama2_7b_ffn"].with_(n_layers=1, d_model=4096, d_ff=2048, block=64, rank=128,
+                                          keep_pct=30),
 }
 
 
@@ -367,8 +370,18 @@ def test_batch_matrix_core_path_matches_vector_path(name, B):
         x_out = empty_f32(B, cfg.d_model)
         f.ls_sparse_ffn_step(0, x_in, B, idx, cnt, 0, cap, x_out)
         ys.append(host(x_out).astype(np.float64) - xs.astype(np.float64))
+    # the same list in three ranges: the first range adds the residual, the others accumulate
+    n = int(host(cnt)[0])
+    cuts = [0, n // 3, (2 * n) // 3, cap]
+    for mfma in (1, 0):
+        f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, mfma)
+        x_out = empty_f32(B, cfg.d_model)
+        for r in range(3):
+            f.ls_sparse_ffn_step(0, x_in, B, idx, cnt, cuts[r], cuts[r + 1], x_out)
+        ys.append(host(x_out).astype(np.float64) - xs.astype(np.float64))
     tol = 1e-5 if cfg.dtype == lsgen.DT_F16 else 1e-4
     for b in range(B):
-        assert rel_l2(ys[0][b], ys[1][b]) <= tol, (name, B, b, rel_l2(ys[0][b], ys[1][b]))
+        for y in ys[1:]:
+            assert rel_l2(ys[0][b], y[b]) <= tol, (name, B, b, rel_l2(ys[0][b], y[b]))
     with pytest.raises(lsffn.LsError):
         f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, 2)
