@@ -779,12 +779,41 @@ def main() -> int:
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
 
+    kernel_ids = {"prenorm": lsffn.LS_K_PRENORM, "pred_p1": lsffn.LS_K_PRED_P1,
+                  "pred_p2": lsffn.LS_K_PRED_P2, "select": lsffn.LS_K_SELECT,
+                  "gateup": lsffn.LS_K_GATEUP, "down": lsffn.LS_K_DOWN,
+                  "decode_fused": lsffn.LS_K_DECODE}
+
+    def kernel_times():
+        out = {}
+        for name, kid in kernel_ids.items():
+            ms, n = f.ls_kernel_timing(kid)
+            if n:
+                out[name] = {"total_ms": ms, "launches": n, "avg_us": 1e3 * ms / n}
+        return out
+
+    # warm-up; its last steps (at most 16) bracket every launch with HIP events for the
+    # per-kernel breakdown
+    n_bd = min(W, 16)
+    per_kernel = {}
     for i in range(W):
+        if i == W - n_bd:
+            torch.cuda.synchronize()
+            f.ls_set_kernel_timing(True)
+            f.ls_kernel_timing(0, reset=True)
         f.ls_decode_step(x_dev[i], B, cfg.k)
     torch.cuda.synchronize()
+    if n_bd:
+        per_kernel = kernel_times()
+        f.ls_set_kernel_timing(False)
 
-    # timed region: K decode steps; kernel timing records HIP event pairs around each launch
-    f.ls_set_kernel_timing(True)
+    # timed region: K decode steps; HIP event pairs bracket the launches of the dominant kernel
+    # (the largest share of the warm-up's time), or of every kernel without a warm-up
+    dom_name = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])[0] if per_kernel else None
+    if dom_name:
+        f.ls_set_kernel_timing(True, kernels=[kernel_ids[dom_name]])
+    else:
+        f.ls_set_kernel_timing(True)
     f.ls_kernel_timing(0, reset=True)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -795,16 +824,12 @@ def main() -> int:
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    live = kernel_times()
     f.ls_set_kernel_timing(False)
     gpu_ms = ev0.elapsed_time(ev1)
-    per_kernel = {}
-    for kid, name in ((lsffn.LS_K_PRENORM, "prenorm"), (lsffn.LS_K_PRED_P1, "pred_p1"),
-                      (lsffn.LS_K_PRED_P2, "pred_p2"), (lsffn.LS_K_SELECT, "select"),
-                      (lsffn.LS_K_GATEUP, "gateup"), (lsffn.LS_K_DOWN, "down"),
-                      (lsffn.LS_K_DECODE, "decode_fused")):
-        ms, n = f.ls_kernel_timing(kid)
-        if n:
-            per_kernel[name] = {"total_ms": ms, "launches": n, "avg_us": 1e3 * ms / n}
+    if not per_kernel:
+        per_kernel = live
+        dom_name = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])[0]
 
     step_s = wall / K
     tok_s = B * K / wall
@@ -817,8 +842,7 @@ def main() -> int:
     bytes_step = int(round(sum(algorithmic_bytes_per_layer(cfg, U) for _ in range(cfg.n_layers))))
     eff_gbs = bytes_step / step_s / 1e9
 
-    # dominant kernel: the one with the largest share of time; its algorithmic bytes per launch
-    dom = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])
+    # dominant kernel: its algorithmic bytes per launch over its launch time in the timed region
     s = cfg.elem_bytes
     per_launch_bytes = {
         "gateup": int(s * (U * cfg.block * cfg.d_model * 2 + (U * cfg.block if cfg.gate_bias else 0))),
@@ -828,7 +852,7 @@ def main() -> int:
         "pred_p2": s * cfg.rank * cfg.n_blk,
         "decode_fused": bytes_step,
     }
-    dom_name, dom_t = dom
+    dom_t = live[dom_name]
     dom_bytes = per_launch_bytes.get(dom_name)
     roofline = None
     if dom_bytes:
@@ -868,6 +892,8 @@ def main() -> int:
         "gpu_event_ms": round(gpu_ms, 3),
         "kernels": {k: {kk: round(vv, 3) if isinstance(vv, float) else vv for kk, vv in v.items()}
                     for k, v in per_kernel.items()},
+        "kernels_from": (f"the last {n_bd} warm-up steps, every launch bracketed by HIP events" if n_bd
+                         else "the timed steps, every launch bracketed by HIP events"),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "setup_s": round(setup_s, 1),

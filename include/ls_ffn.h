@@ -250,7 +250,8 @@ ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_
 
 /* Per-kernel timing (tracing aid).  While enabled, every kernel launch the
  * context makes is bracketed by a pair of HIP events recorded on the context's
- * stream.  ls_kernel_timing synchronises the stream, folds the finished event
+ * stream.  enable: 0 off; 1 or -1 every kernel; otherwise a mask with bit
+ * (1 << id) set for each kernel id to bracket, the others run unbracketed.  ls_kernel_timing synchronises the stream, folds the finished event
  * pairs into per-kernel totals and returns the total milliseconds and launch
  * count of one kernel id since the last reset; reset != 0 clears all totals.
  * Kernel ids: 0 MLP input (the RMS prenorm is computed inside the predictor and

@@ -244,8 +244,15 @@ class Ffn:
     def ls_ffn_sync(self) -> None:
         _check(self.lib, self.ctx, self.lib.ls_ffn_sync(self.ctx))
 
-    def ls_set_kernel_timing(self, enable: bool) -> None:
-        _check(self.lib, self.ctx, self.lib.ls_set_kernel_timing(self.ctx, int(bool(enable))))
+    def ls_set_kernel_timing(self, enable: bool, kernels=None) -> None:
+        """enable: bracket launches with HIP events; kernels: the LS_K_* ids to bracket
+        (default: every kernel)."""
+        mask = 0
+        if enable:
+            mask = 1 if kernels is None else sum(1 << int(k) for k in set(kernels) if int(k) != LS_K_PRENORM)
+            if mask == 0:
+                raise ValueError("no launching kernel id given")
+        _check(self.lib, self.ctx, self.lib.ls_set_kernel_timing(self.ctx, mask))
 
     def ls_kernel_timing(self, kernel: int, reset: bool = False):
         """(total milliseconds, launches) of one kernel id since the last reset."""

@@ -67,7 +67,7 @@ struct ls_ffn {
     std::vector<hipEvent_t> table_uploaded;  // per layer: last slot-table upload
 
     // kernel timing
-    bool timing = false;
+    uint32_t timing = 0;      // bit i: bracket launches of kernel id i with events
     struct Pending {
         int kernel;
         hipEvent_t start, stop;
@@ -186,7 +186,7 @@ hipError_t take_event(ls_ffn* c, hipEvent_t* e) {
 // Launch `fn` (returning hipError_t); when timing is on, bracket it with an event pair.
 template <typename Fn>
 hipError_t timed(ls_ffn* c, int kernel, Fn&& fn) {
-    if (!c->timing) return fn();
+    if (!((c->timing >> kernel) & 1u)) return fn();
     hipEvent_t a, b;
     hipError_t e = take_event(c, &a);
     if (e != hipSuccess) return e;
@@ -1159,7 +1159,8 @@ ls_status ls_ffn_sync(ls_ffn* c) {
 ls_status ls_set_kernel_timing(ls_ffn* c, int32_t enable) {
     ls_status st = check_ctx(c);
     if (st != LS_OK) return st;
-    c->timing = enable != 0;
+    // 1 (the bit of the prenorm id, which launches nothing) and -1: every kernel
+    c->timing = (enable == 1 || enable == -1) ? ~0u : (uint32_t)enable;
     return LS_OK;
 }
 
