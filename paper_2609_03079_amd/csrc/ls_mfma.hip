@@ -97,8 +97,9 @@ constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
 // workgroup) and the dot products are scaled at the end.
 constexpr int kChunkK = 512;                 // K values per chunk (1 KB of a 16-bit row)
 constexpr int kRowPitch = 2 * kChunkK + 16;  // LDS bytes per staged row
+// three waves per SIMD (at most 168 registers a lane): three workgroups per CU
 template <ls_dtype T, ls_act A, bool RMS>
-__global__ __launch_bounds__(256) void gateup_mfma_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void gateup_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int B, int d, int blk,
     int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
@@ -137,22 +138,47 @@ __global__ __launch_bounds__(256) void gateup_mfma_kernel(
                                       : u32x4{0u, 0u, 0u, 0u};
         }
     };
+    // x of this wave's K steps of a chunk (s0 = wave + kWaves j), fetched one chunk ahead with
+    // the weights: waiting for them never waits for the next chunk's weight loads (the counter
+    // of outstanding loads drains in issue order)
+    constexpr int kStepsW = kChunkK / 32 / kWaves;
+    auto load_x = [&](int c0, f32x4 (&hx)[kStepsW][2]) {
+        const int steps = min(kChunkK, d - c0) / 32;
+#pragma unroll
+        for (int j = 0; j < kStepsW; ++j) {
+            const int s0 = wave + kWaves * j;
+            const int kc = 32 * s0 + 8 * (lane >> 4);  // this lane's 8 K values in the chunk
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+            const bool ok = tok_ok && s0 < steps;
+            hx[j][0] = ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[0] : z;
+            hx[j][1] = ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[1] : z;
+        }
+    };
     f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
     u32x4 rw[8];
+    f32x4 hx[kStepsW][2];
     load_chunk(0, rw);
+    load_x(0, hx);
     for (int c0 = 0; c0 < d; c0 += kChunkK) {
+        const int steps = min(kChunkK, d - c0) / 32;
+        f32x4 hc[kStepsW][2];
+#pragma unroll
+        for (int j = 0; j < kStepsW; ++j) hc[j][0] = hx[j][0], hc[j][1] = hx[j][1];
 #pragma unroll
         for (int i = 0; i < 8; ++i)
             *reinterpret_cast<u32x4*>(stage + (wave + 4 * i) * kRowPitch + lane * 16) = rw[i];
         __syncthreads();
-        if (c0 + kChunkK < d) load_chunk(c0 + kChunkK, rw);  // in flight while this chunk runs
-        const int steps = min(kChunkK, d - c0) / 32;
-        for (int s0 = wave; s0 < steps; s0 += 4) {
-            const int kc = 32 * s0 + 8 * (lane >> 4);  // this lane's 8 K values in the chunk
-            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-            const f32x4 h0 = tok_ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[0] : z;
-            const f32x4 h1 = tok_ok ? reinterpret_cast<const f32x4*>(hrow + c0 + kc)[1] : z;
+        if (c0 + kChunkK < d) {  // in flight while this chunk runs
+            load_chunk(c0 + kChunkK, rw);
+            load_x(c0 + kChunkK, hx);
+        }
+#pragma unroll
+        for (int j = 0; j < kStepsW; ++j) {
+            const int s0 = wave + kWaves * j;
+            if (s0 >= steps) break;
+            const int kc = 32 * s0 + 8 * (lane >> 4);
+            const f32x4 h0 = hc[j][0], h1 = hc[j][1];
             const float xv[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
             if (RMS) {
 #pragma unroll
