@@ -792,9 +792,9 @@ def main() -> int:
                 out[name] = {"total_ms": ms, "launches": n, "avg_us": 1e3 * ms / n}
         return out
 
-    # warm-up; its last steps (at most 16) bracket every launch with HIP events for the
-    # per-kernel breakdown
-    n_bd = min(W, 16)
+    # warm-up; its second half (at most 16 steps; the first steps run cold) brackets every
+    # launch with HIP events for the per-kernel breakdown
+    n_bd = min(W // 2, 16)
     per_kernel = {}
     for i in range(W):
         if i == W - n_bd:
