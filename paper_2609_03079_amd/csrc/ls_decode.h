@@ -19,7 +19,8 @@ struct FusedArgs {
     int L, d, nb, blk, F, k, kp, prenorm;
     size_t block_bytes;
     float* x;                 // [d]: input at entry, output at exit
-    uint64_t* xmb;            // [L][d]      tagged x of every layer input (row 0: the input)
+    uint64_t* xmb;            // [L][d]      tagged x of every layer input (row 0: the input,
+                              //             unused when L >= 2: layer 0 then reads x itself)
     uint64_t* smb;            // [L][2 n_blk] tagged scores (exact | speculative)
     uint64_t* amb;            // [L][2F]     tagged activations: list positions, then misses
     uint32_t tag;             // launch epoch (>= 1)

@@ -296,19 +296,32 @@ __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int*
 }
 
 // X, one quarter per wave: words [wave*D/4, (wave+1)*D/4) of the layer input into xin (and
-// this workgroup's tile into xt), and the quarter's sum of squares into ssp.
+// this workgroup's tile into xt), and the quarter's sum of squares into ssp.  With two or
+// more layers, layer 0 reads the caller's x directly (written before the launch).  That is
+// safe because the output goes into x only at the last layer.  No workgroup gets past layer
+// 1's input before every workgroup has finished its layer-0 gather: that gather precedes
+// the workgroup's own layer-0 output tile, which every layer-1 gather waits for.  With one
+// layer, a small kernel first tags x into the mailbox row 0.
 template <int D>
 __device__ __forceinline__ void gather_input(const FusedArgs& P, Smem& sm, const Geo& g, int l, int wave,
                                              int lane) {
     constexpr int Q = D / kWaves;
     constexpr int W = Q / 64;
-    uint64_t v[W];
-    wait_words<W>(P.xmb + (size_t)l * D + wave * Q, Q, g.tag, lane, P.err, v);
+    float xv[W];
+    if (l == 0 && P.L >= 2) {
+#pragma unroll
+        for (int u = 0; u < W; ++u) xv[u] = P.x[wave * Q + u * 64 + lane];
+    } else {
+        uint64_t v[W];
+        wait_words<W>(P.xmb + (size_t)l * D + wave * Q, Q, g.tag, lane, P.err, v);
+#pragma unroll
+        for (int u = 0; u < W; ++u) xv[u] = word_value(v[u]);
+    }
     float ss = 0.f;
 #pragma unroll
     for (int u = 0; u < W; ++u) {
         const int i = wave * Q + u * 64 + lane;
-        const float x = word_value(v[u]);
+        const float x = xv[u];
         ss = fmaf(x, x, ss);
         sm.xin[i] = x;
         if (g.has_tile && (i >> 4) == g.w) sm.xt[i & (kColTile - 1)] = x;
@@ -953,9 +966,11 @@ hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hip
     if (nc == 2) fn = reinterpret_cast<void*>(decode_fused_kernel<T, A, 2>);
     else if (nc == 8) fn = reinterpret_cast<void*>(decode_fused_kernel<T, A, 8>);
     else return hipErrorNotSupported;
-    hipLaunchKernelGGL(tag_input_kernel, dim3((s.d + 255) / 256), dim3(256), 0, st, a.x, s.d, a.tag, a.xmb);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (a.L < 2) {  // with two or more layers, layer 0 reads x itself
+        hipLaunchKernelGGL(tag_input_kernel, dim3((s.d + 255) / 256), dim3(256), 0, st, a.x, s.d, a.tag, a.xmb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     FusedArgs copy = a;
     void* args[] = {&copy};
     if (coop) return hipLaunchCooperativeKernel(fn, dim3(n_wg), dim3(kThreads), args, 0, st);
