@@ -385,3 +385,30 @@ def test_batch_matrix_core_path_matches_vector_path(name, B):
             assert rel_l2(ys[0][b], y[b]) <= tol, (name, B, b, rel_l2(ys[0][b], y[b]))
     with pytest.raises(lsffn.LsError):
         f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, 2)
+
+
+def test_kernel_timing_mask():
+    """ls_set_kernel_timing with a kernel-id mask brackets only those kernels' launches; the
+    default brackets every launch; a mask of only the prenorm id (which launches nothing) is
+    refused by the binding."""
+    cfg = SMALL["f16_b64"]
+    f, _ = make_ffn(cfg, max_batch=4)
+    f.ls_configure(lsffn.LS_CFG_DECODE_PATH, 1)
+    xs = lsgen.tokens(cfg, 2, 2, 4)
+    launched = (lsffn.LS_K_PRED_P1, lsffn.LS_K_SELECT, lsffn.LS_K_GATEUP, lsffn.LS_K_DOWN)
+    f.ls_set_kernel_timing(True, kernels=[lsffn.LS_K_GATEUP])
+    f.ls_kernel_timing(0, reset=True)
+    f.ls_decode_step(dev_f32(xs[0]), 4, cfg.k)
+    ms, n = f.ls_kernel_timing(lsffn.LS_K_GATEUP)
+    assert n == cfg.n_layers and ms > 0
+    for kid in launched:
+        if kid != lsffn.LS_K_GATEUP:
+            assert f.ls_kernel_timing(kid)[1] == 0, kid
+    f.ls_set_kernel_timing(True)
+    f.ls_kernel_timing(0, reset=True)
+    f.ls_decode_step(dev_f32(xs[1]), 4, cfg.k)
+    for kid in launched:
+        assert f.ls_kernel_timing(kid)[1] == cfg.n_layers, kid
+    f.ls_set_kernel_timing(False)
+    with pytest.raises(ValueError):
+        f.ls_set_kernel_timing(True, kernels=[lsffn.LS_K_PRENORM])
