@@ -21,11 +21,12 @@ namespace {
 
 // ---- GEMV over rows: out[b, row] = c_b * sum_c W[row, c] * v[b, c] ------------------------
 // c_b = rms_scale of v[b, :] when RMS (the MLP input of a prenorm stack), else 1.
-// One workgroup per R rows; its 4 waves split the rows' 16-byte chunks, then a fixed-order
-// sum of the 4 wave totals.  The R rows share the input reads (with B tokens the input is B
-// times the bytes of a row); every row's dot product is summed in the same order for any R.
-template <ls_dtype T, int B, bool RMS, int R>
-__global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
+// One workgroup of NW waves per R rows; the waves split the rows' 16-byte chunks, then a
+// fixed-order sum of the wave totals.  The R rows share the input reads (with B tokens the
+// input is B times the bytes of a row); every row's dot product is summed in the same order
+// for any R.
+template <ls_dtype T, int B, bool RMS, int R, int NW>
+__global__ __launch_bounds__(64 * NW) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
                                                         int cols, int G, int rpw,
                                                         const float* __restrict__ v,
                                                         float* __restrict__ out) {
@@ -48,17 +49,17 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][b] = 0.f;
     }
-    for (int c0 = threadIdx.x; c0 < nchunk; c0 += 256 * U) {
+    for (int c0 = threadIdx.x; c0 < nchunk; c0 += 64 * NW * U) {
         u32x4 raw[U][R];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 256;
+            const int c = c0 + u * 64 * NW;
 #pragma unroll
             for (int r = 0; r < R; ++r) raw[u][r] = c < nchunk ? ld_stream(wr[r] + c) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * 256;
+            const int c = c0 + u * 64 * NW;
             if (c < nchunk) {
                 float w[R][V];
 #pragma unroll
@@ -87,7 +88,7 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
             }
         }
     }
-    __shared__ float part[4][R][B], pss[4][B];
+    __shared__ float part[NW][R][B], pss[NW][B];
 #pragma unroll
     for (int b = 0; b < B; ++b) {
 #pragma unroll
@@ -101,8 +102,10 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const uint8_t* __restric
     __syncthreads();
     if (threadIdx.x < R * B) {
         const int r = threadIdx.x / B, b = threadIdx.x % B;
-        const float dot = ((part[0][r][b] + part[1][r][b]) + part[2][r][b]) + part[3][r][b];
-        const float sc = RMS ? rms_scale(((pss[0][b] + pss[1][b]) + pss[2][b]) + pss[3][b], cols) : 1.f;
+        float dot = 0.f, q = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) dot += part[w][r][b], q += pss[w][b];
+        const float sc = RMS ? rms_scale(q, cols) : 1.f;
         if (row0 + r < rows) out[(size_t)b * rows + row0 + r] = dot * sc;
     }
 }
@@ -281,20 +284,20 @@ __global__ __launch_bounds__(256) void down_kernel(
 template <ls_dtype T, bool RMS>
 static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, const float* v, int B,
                          float* out, hipStream_t st) {
-    // four rows per workgroup once the batch makes the input reads dominate
-    const int R = B >= 4 ? 4 : 1;
-    const dim3 grid((unsigned)((rows + R - 1) / R)), blk(256);
+    // four rows and eight waves per workgroup once the batch makes the input reads dominate
+    const int R = B >= 4 ? 4 : 1, NW = B >= 4 ? 8 : 4;
+    const dim3 grid((unsigned)((rows + R - 1) / R)), blk(64 * NW);
     const uint8_t* w = static_cast<const uint8_t*>(W);
-#define LS_GEMV(NB, NR) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
+#define LS_GEMV(NB, NR, NWV) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR, NWV>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
     switch (B) {
-        case 1: LS_GEMV(1, 1); break;
-        case 2: LS_GEMV(2, 1); break;
-        case 3: LS_GEMV(3, 1); break;
-        case 4: LS_GEMV(4, 4); break;
-        case 5: LS_GEMV(5, 4); break;
-        case 6: LS_GEMV(6, 4); break;
-        case 7: LS_GEMV(7, 4); break;
-        case 8: LS_GEMV(8, 4); break;
+        case 1: LS_GEMV(1, 1, 4); break;
+        case 2: LS_GEMV(2, 1, 4); break;
+        case 3: LS_GEMV(3, 1, 4); break;
+        case 4: LS_GEMV(4, 4, 8); break;
+        case 5: LS_GEMV(5, 4, 8); break;
+        case 6: LS_GEMV(6, 4, 8); break;
+        case 7: LS_GEMV(7, 4, 8); break;
+        case 8: LS_GEMV(8, 4, 8); break;
         default: return hipErrorInvalidValue;
     }
 #undef LS_GEMV
