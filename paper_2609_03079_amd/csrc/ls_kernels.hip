@@ -176,13 +176,25 @@ __global__ __launch_bounds__(Q > 8 ? 512 : 1024) void select_kernel(const float*
         int rem = 0;
         bool thr_mode = mode != LS_SEL_TOPK;
         if (!thr_mode) {
-            for (int bit = 31; bit >= 0; --bit) {
+            auto step = [&](int bit) {
                 const uint32_t c = T | (1u << bit);
                 int cnt = 0;
 #pragma unroll
                 for (int q = 0; q < Q; ++q) cnt += __popcll(__ballot(ok[q] >= c));
                 if (cnt >= k) T = c;
+            };
+            int bit = 31;
+            for (; bit >= 16; --bit) step(bit);
+            // top 16 bits decided: with exactly k keys at or above them the members are every
+            // such key whatever T's low bits become (ties at T are then all taken), so the low
+            // steps are skipped; T != 0 keeps the padding out of the count
+            int ge = 0;
+            if (T != 0u) {
+#pragma unroll
+                for (int q = 0; q < Q; ++q) ge += __popcll(__ballot(ok[q] >= T));
             }
+            if (ge != k)
+                for (; bit >= 0; --bit) step(bit);
             int gt = 0;
 #pragma unroll
             for (int q = 0; q < Q; ++q) gt += __popcll(__ballot(ok[q] > T));
