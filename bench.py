@@ -715,7 +715,11 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              f"(this build has no multi-GPU path).", file=sys.stderr)
+              f"(the library has no multi-GPU path).", file=sys.stderr)
+        return 2
+    if args.stream_sync == "flags" and args.prefetch == "refine":
+        print("--stream-sync flags runs one persistent launch per layer, which refined prefetch "
+              "(per-stage launches) cannot use: pass --prefetch none or oneshot.", file=sys.stderr)
         return 2
 
     if args.overlap_from_trace:

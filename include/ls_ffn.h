@@ -38,7 +38,7 @@ typedef enum {
     LS_E_NOMEM = 2,       /* host or device allocation failed */
     LS_E_DEVICE = 3,      /* a HIP call failed; sticky until ls_ffn_destroy */
     LS_E_STATE = 4,       /* call not valid in the context's state (e.g. layer not set) */
-    LS_E_UNSUPPORTED = 5, /* valid request this build does not implement */
+    LS_E_UNSUPPORTED = 5, /* valid request the library does not implement */
     LS_E_CAPACITY = 6     /* request larger than the HBM block cache */
 } ls_status;
 
