@@ -39,7 +39,7 @@ def build(force: bool = True) -> str:
     """Compile the oracle with gcc (-O2, plain C, no intrinsics)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
-        subprocess.run(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"],
+        subprocess.run(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm", "-lpthread"],
                        check=True)
         os.replace(tmp, _LIB)
     return _LIB
@@ -75,7 +75,10 @@ def _load():
         lib.orc_layer_step.argtypes = [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _D, _I,
                                        _I, _P, _P, _P, _P, _P]
         lib.orc_layer_step.restype = _I
-        lib.orc_hash_predict.argtypes = [_I, _I, _P, _P, _P, _P, _P, _P, _P]
+        lib.orc_layer_step_mt.argtypes = [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _D, _I,
+                                          _I, _P, _P, _P, _P, _P, _I]
+        lib.orc_layer_step_mt.restype = _I
+        lib.orc_hash_predict.argtypes = [_I, _I, _P, _P, _P, _P, _P, _I, _P, _P, _P]
         lib.orc_hash_predict.restype = None
         _lib = lib
     return _lib
@@ -233,8 +236,10 @@ def staged_ffn(w, x: np.ndarray, h: np.ndarray, blocks, block: int, K: int, act:
     return dms, xt
 
 
-def layer_step(w, cfg, x: np.ndarray, k: int | None = None):
-    """One layer for one token via the C composition: returns (scores, idx, y, x_out)."""
+def layer_step(w, cfg, x: np.ndarray, k: int | None = None, n_threads: int = 0):
+    """One layer for one token via the C composition: returns (scores, idx, y, x_out).
+    n_threads > 0: the same composition with its output loops split over that many threads
+    (identical results)."""
     d, F, r, blk = cfg.d_model, cfg.d_ff, cfg.rank, cfg.block
     k = cfg.k if k is None else k
     nblk = F // blk
@@ -245,11 +250,14 @@ def layer_step(w, cfg, x: np.ndarray, k: int | None = None):
     idx = np.empty(k, np.int32)
     y = np.empty(d, np.float64)
     x_out = np.empty(d, np.float32)
-    n = _load().orc_layer_step(d, F, r, blk, gate.ctypes.data, up.ctypes.data, wd.ctypes.data,
-                               _ptr(bias), p1.ctypes.data, p2.ctypes.data, storage_code(gate),
-                               cfg.act, float(w.threshold), int(cfg.prenorm), k, x.ctypes.data,
-                               scores.ctypes.data, idx.ctypes.data, y.ctypes.data,
-                               x_out.ctypes.data)
+    args = (d, F, r, blk, gate.ctypes.data, up.ctypes.data, wd.ctypes.data, _ptr(bias),
+            p1.ctypes.data, p2.ctypes.data, storage_code(gate), cfg.act, float(w.threshold),
+            int(cfg.prenorm), k, x.ctypes.data, scores.ctypes.data, idx.ctypes.data, y.ctypes.data,
+            x_out.ctypes.data)
+    if n_threads > 0:
+        n = _load().orc_layer_step_mt(*args, int(n_threads))
+    else:
+        n = _load().orc_layer_step(*args)
     if n < 0:
         raise RuntimeError("orc_layer_step failed")
     return scores, idx[:n], y, x_out
@@ -340,18 +348,23 @@ def refinement_quality(w_n, w_next, cfg, x: np.ndarray, K: int, order=None, k: i
 HASH_TAU, HASH_DH, HASH_LAYERS = 8, 256, 5
 
 
-def hash_predict(hw, x: np.ndarray, n_blk: int):
-    """Block scores of the stacked hashing predictor for one token (fp32 [n_blk]) and the five
-    bucket indices.  ``hw`` has .w1 (fp32 [d, 8]), .w_bin (uint32 [4, 8, 8]), .tables (uint32
-    [4, 256, 8]), .head (uint8 [256, n_blk])."""
+def hash_predict(hw, x: np.ndarray, n_blk: int, code0: int | None = None):
+    """Block scores of the stacked hashing predictor for one token (fp32 [n_blk]), the five
+    bucket indices and the first layer's real products x . W_1[:, b] (float64 [8]).  The first
+    bucket is phi(sign(x W_1)) from those float64 products, or ``code0`` when given (the later
+    layers are then evaluated from it).  ``hw`` has .w1 (fp32 [d, 8]), .w_bin (uint32 [4, 8, 8]),
+    .tables (uint32 [4, 256, 8]), .head (uint8 [256, n_blk])."""
     x = _c(x, np.float32)
     w1, wb, tb, hd = _c(hw.w1, np.float32), _c(hw.w_bin, np.uint32), _c(hw.tables, np.uint32), \
         _c(hw.head, np.uint8)
     d = x.shape[0]
     assert w1.shape == (d, HASH_TAU) and wb.shape == (4, HASH_TAU, HASH_DH // 32)
     assert tb.shape == (4, HASH_DH, HASH_DH // 32) and hd.shape == (HASH_DH, n_blk)
+    assert code0 is None or 0 <= code0 < 256
     codes = np.zeros(HASH_LAYERS, np.int32)
+    prods = np.zeros(HASH_TAU, np.float64)
     scores = np.empty(n_blk, np.float32)
     _load().orc_hash_predict(d, n_blk, x.ctypes.data, w1.ctypes.data, wb.ctypes.data, tb.ctypes.data,
-                             hd.ctypes.data, codes.ctypes.data, scores.ctypes.data)
-    return scores, codes
+                             hd.ctypes.data, -1 if code0 is None else int(code0), prods.ctypes.data,
+                             codes.ctypes.data, scores.ctypes.data)
+    return scores, codes, prods

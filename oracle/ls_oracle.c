@@ -29,6 +29,7 @@
  * routines, closed forms, brute force, invariants); none is "parity unpinned".
  */
 #include <math.h>
+#include <pthread.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -88,19 +89,29 @@ void orc_mlp_input(int d, const float* x, int rms, double* h) {
  * (P2 is [n_blk, r]).  Scores are handed out rounded to binary32, which is the
  * score interface both sides agree on.
  * ------------------------------------------------------------------------- */
-void orc_predict(int d, int r, int nblk, const void* p1, const void* p2, int dtype,
-                 const double* h, double* z_out, float* scores) {
-    double* z = z_out ? z_out : (double*)malloc(sizeof(double) * (size_t)r);
-    for (int i = 0; i < r; ++i) {
+static void predict_z_rows(int d, const void* p1, int dtype, const double* h, int lo, int hi,
+                           double* z) {
+    for (int i = lo; i < hi; ++i) {
         double acc = 0.0;
         for (int c = 0; c < d; ++c) acc += orc_decode(p1, dtype, (size_t)i * d + c) * h[c];
         z[i] = acc;
     }
-    for (int b = 0; b < nblk; ++b) {
+}
+
+static void predict_s_rows(int r, const void* p2, int dtype, const double* z, int lo, int hi,
+                           float* scores) {
+    for (int b = lo; b < hi; ++b) {
         double acc = 0.0;
         for (int i = 0; i < r; ++i) acc += orc_decode(p2, dtype, (size_t)b * r + i) * z[i];
         scores[b] = (float)acc;
     }
+}
+
+void orc_predict(int d, int r, int nblk, const void* p1, const void* p2, int dtype,
+                 const double* h, double* z_out, float* scores) {
+    double* z = z_out ? z_out : (double*)malloc(sizeof(double) * (size_t)r);
+    predict_z_rows(d, p1, dtype, h, 0, r, z);
+    predict_s_rows(r, p2, dtype, z, 0, nblk, scores);
     if (!z_out) free(z);
 }
 
@@ -245,14 +256,19 @@ void orc_activations(int d, int F, const void* wg, const void* wu, const void* b
  * Down projection (Eq. 1; Sec. 3.2.2): y_m = sum_t a_t * Wd[m, neurons[t]],
  * Wd is [d, F] (nn.Linear layout), summed in list order.
  * ------------------------------------------------------------------------- */
-void orc_down(int d, int F, const void* wd, int dtype, int n, const int* neurons,
-              const double* a, double* y) {
-    for (int m = 0; m < d; ++m) {
+static void down_cols(int F, const void* wd, int dtype, int n, const int* neurons, const double* a,
+                      int lo, int hi, double* y) {
+    for (int m = lo; m < hi; ++m) {
         double acc = 0.0;
         for (int t = 0; t < n; ++t)
             acc += a[t] * orc_decode(wd, dtype, (size_t)m * F + neurons[t]);
         y[m] = acc;
     }
+}
+
+void orc_down(int d, int F, const void* wd, int dtype, int n, const int* neurons,
+              const double* a, double* y) {
+    down_cols(F, wd, dtype, n, neurons, a, 0, d, y);
 }
 
 /* ---------------------------------------------------------------------------
@@ -323,6 +339,102 @@ int orc_layer_step(int d, int F, int r, int blk, const void* wg, const void* wu,
 }
 
 /* ---------------------------------------------------------------------------
+ * The same layer step with its loops over output elements split into n_threads
+ * contiguous ranges on POSIX threads (predictor rows, then block scores, then
+ * neurons, then output columns; the selection stays on the calling thread).
+ * Every output element is the same sum in the same order as in orc_layer_step,
+ * so the results are identical; only the wall time changes.  Used to time the
+ * oracle on every host core.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int phase, lo, hi;
+    int d, F, r, dtype, act, nblk;
+    const void *wg, *wu, *wd, *bias, *p1, *p2;
+    double thresh;
+    const double* h;
+    double* z;
+    float* scores;
+    const int* neurons;
+    double* a;
+    double* y;
+    int n;
+} mt_job;
+
+static void* mt_run(void* arg) {
+    mt_job* j = (mt_job*)arg;
+    if (j->phase == 0) {
+        predict_z_rows(j->d, j->p1, j->dtype, j->h, j->lo, j->hi, j->z);
+    } else if (j->phase == 1) {
+        predict_s_rows(j->r, j->p2, j->dtype, j->z, j->lo, j->hi, j->scores);
+    } else if (j->phase == 2) {
+        orc_activations(j->d, j->F, j->wg, j->wu, j->bias, j->dtype, j->act, j->thresh, j->h,
+                        j->hi - j->lo, j->neurons + j->lo, NULL, NULL, j->a + j->lo);
+    } else {
+        down_cols(j->F, j->wd, j->dtype, j->n, j->neurons, j->a, j->lo, j->hi, j->y);
+    }
+    return NULL;
+}
+
+/* runs one phase over [0, total) split into nt contiguous ranges */
+static void mt_phase(const mt_job* base, int phase, int total, int nt) {
+    pthread_t th[256];
+    int made[256];
+    mt_job jobs[256];
+    if (nt > 256) nt = 256;
+    if (nt > total) nt = total > 0 ? total : 1;
+    for (int t = 0; t < nt; ++t) {
+        jobs[t] = *base;
+        jobs[t].phase = phase;
+        jobs[t].lo = (int)((int64_t)t * total / nt);
+        jobs[t].hi = (int)((int64_t)(t + 1) * total / nt);
+    }
+    for (int t = 1; t < nt; ++t) {
+        made[t] = pthread_create(&th[t], NULL, mt_run, &jobs[t]) == 0;
+        if (!made[t]) mt_run(&jobs[t]); /* no thread: run the range here */
+    }
+    mt_run(&jobs[0]);
+    for (int t = 1; t < nt; ++t)
+        if (made[t]) pthread_join(th[t], NULL);
+}
+
+int orc_layer_step_mt(int d, int F, int r, int blk, const void* wg, const void* wu, const void* wd,
+                      const void* bias, const void* p1, const void* p2, int dtype, int act,
+                      double thresh, int rms, int k, const float* x, float* scores, int* idx,
+                      double* y, float* x_out, int n_threads) {
+    int nblk = F / blk;
+    double* h = (double*)malloc(sizeof(double) * (size_t)d);
+    double* z = (double*)malloc(sizeof(double) * (size_t)r);
+    orc_mlp_input(d, x, rms, h);
+    mt_job job;
+    memset(&job, 0, sizeof job);
+    job.d = d; job.F = F; job.r = r; job.dtype = dtype; job.act = act; job.nblk = nblk;
+    job.wg = wg; job.wu = wu; job.wd = wd; job.bias = bias; job.p1 = p1; job.p2 = p2;
+    job.thresh = thresh; job.h = h; job.z = z; job.scores = scores;
+    mt_phase(&job, 0, r, n_threads);
+    mt_phase(&job, 1, nblk, n_threads);
+    int count = 0;
+    if (orc_select(scores, 1, nblk, ORC_SEL_TOPK, k, 0.0f, 0, k, idx, &count) != 0) {
+        free(z);
+        free(h);
+        return -1;
+    }
+    int n = count * blk;
+    int* neurons = (int*)malloc(sizeof(int) * (size_t)n);
+    double* a = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int p = 0; p < count; ++p)
+        for (int q = 0; q < blk; ++q) neurons[p * blk + q] = idx[p] * blk + q;
+    job.neurons = neurons; job.a = a; job.y = y; job.n = n;
+    mt_phase(&job, 2, n, n_threads);
+    mt_phase(&job, 3, d, n_threads);
+    for (int m = 0; m < d; ++m) x_out[m] = (float)((double)x[m] + y[m]);
+    free(a);
+    free(neurons);
+    free(z);
+    free(h);
+    return count;
+}
+
+/* ---------------------------------------------------------------------------
  * Stacked learnable hashing, inference (Sec. 3.3.1, Eq. hash_layer and
  * Eq. hashfunc_layer): five hashing layers, tau = 8 hash bits each, binary
  * features of width 256 between them.
@@ -339,10 +451,13 @@ int orc_layer_step(int d, int F, int r, int blk, const void* wg, const void* wu,
  * sign(0) = +1.  Bit-packed {-1,+1} vectors: element e is bit (e & 31) of word
  * e >> 5, 1 meaning +1.
  *
- * The first layer's code is a floating-point decision, so it is taken in the
- * GPU kernel's precision and order (binary32 fused multiply-adds): for each
- * hash bit, 256 partial sums over j = t, t + 256, ... in increasing j, then
- * the pairwise halving sum p[t] += p[t + s] for s = 128, 64, ..., 1.
+ * The first layer is the definition itself: each hash bit is the sign of the
+ * real product x . W_1[:, b], summed in double precision in increasing j over
+ * exactly represented binary32 operands.  The products are returned, so that a
+ * caller comparing with a binary32 evaluation can see which decisions sit
+ * within rounding distance of zero; a caller may also impose the first
+ * layer's bucket (code0 >= 0) and have only the later, integer layers
+ * evaluated from it.
  * ------------------------------------------------------------------------- */
 enum { ORC_TAU = 8, ORC_DH = 256, ORC_DHW = ORC_DH / 32, ORC_NLAYERS = 5 };
 
@@ -355,21 +470,21 @@ static int popcount32(uint32_t v) {
     return c;
 }
 
-/* codes[5]: the five bucket indices; scores[nblk] = head[codes[4]][b]. */
+/* codes[5]: the five bucket indices; scores[nblk] = head[codes[4]][b].
+ * prods[8] (may be NULL): the first layer's real products in double.
+ * code0 < 0: the first bucket is phi(sign(x W_1)); code0 in [0, 255]: it is
+ * code0 (the products are still returned). */
 void orc_hash_predict(int d, int nblk, const float* x, const float* w1, const uint32_t* w_bin,
-                      const uint32_t* tables, const uint8_t* head, int* codes, float* scores) {
+                      const uint32_t* tables, const uint8_t* head, int code0, double* prods,
+                      int* codes, float* scores) {
     int idx = 0;
     for (int b = 0; b < ORC_TAU; ++b) {
-        float p[ORC_DH];
-        for (int t = 0; t < ORC_DH; ++t) {
-            float acc = 0.f;
-            for (int j = t; j < d; j += ORC_DH) acc = fmaf(x[j], w1[(size_t)j * ORC_TAU + b], acc);
-            p[t] = acc;
-        }
-        for (int s = ORC_DH / 2; s >= 1; s /= 2)
-            for (int t = 0; t < s; ++t) p[t] = p[t] + p[t + s];
-        idx = 2 * idx + (p[0] >= 0.f ? 1 : 0);
+        double acc = 0.0;
+        for (int j = 0; j < d; ++j) acc += (double)x[j] * (double)w1[(size_t)j * ORC_TAU + b];
+        if (prods) prods[b] = acc;
+        idx = 2 * idx + (acc >= 0.0 ? 1 : 0);
     }
+    if (code0 >= 0) idx = code0;
     codes[0] = idx;
     for (int k = 1; k < ORC_NLAYERS; ++k) {
         const uint32_t* y = tables + ((size_t)(k - 1) * ORC_DH + (size_t)idx) * ORC_DHW; /* y_k = T_k[i] */

@@ -499,6 +499,35 @@ def test_block_importance_invariants():
     assert np.all(imp[dead] == 0) and np.all(imp[~dead] > 0)
 
 
+def test_threaded_layer_step_is_identical():
+    """The oracle's thread-split layer step (used to time it on every host core) gives the very
+    same scores, list and outputs as the single-thread one, for any thread count."""
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(n_layers=1, d_model=256, d_ff=1024, block=32, rank=64)
+    w = lsgen.layer_weights(cfg, 0)
+    x = lsgen.tokens(cfg, 2, 1, 1)[0, 0]
+    ref = oracle.layer_step(w, cfg, x)
+    for nt in (1, 3, 8, 64):
+        got = oracle.layer_step(w, cfg, x, n_threads=nt)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b), nt
+
+
+def test_block_importance_hand_computed_value():
+    # d = 2, F = 4, two blocks of 2 neurons, ReGLU, no bias, h = (1, 2):
+    #   g = (1, 2, 3, -1), u = (2, 2, 1, 6), a = max(g, 0) * u = (2, 4, 3, 0)
+    #   W_down columns (3,4), (0,1), (1,1), (5,12) have L2 norms 5, 1, sqrt(2), 13
+    #   block 0: |2|*5 + |4|*1 = 14; block 1: |3|*sqrt(2) + 0*13 = 3*sqrt(2)
+    # An L1 column norm would give 18 and 6; the norm of the block's summed contribution
+    # 2*(3,4) + 4*(0,1) = (6,12) would give sqrt(180) for block 0.
+    f32 = np.float32
+    w = SimpleNamespace(gate=np.array([[1, 0], [0, 1], [1, 1], [-1, 0]], f32),
+                        up=np.array([[2, 0], [0, 1], [1, 0], [0, 3]], f32),
+                        down=np.array([[3, 0, 1, 5], [4, 1, 1, 12]], f32),
+                        bias=None, threshold=0.0)
+    imp = oracle.block_importance(w, np.array([1.0, 2.0]), 2, lsgen.ACT_REGLU)
+    assert np.allclose(imp, [14.0, 3.0 * math.sqrt(2.0)], rtol=1e-14, atol=0)
+
+
 def test_refinement_last_stage_is_the_complete_output_prediction():
     cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(n_layers=2, d_model=256, d_ff=1024, block=32, rank=64,
                                                dtype=lsgen.DT_F32, predictor="planted")
@@ -562,11 +591,11 @@ def test_hash_index_is_the_papers_sign_pattern_enumeration():
     for j in range(0, 256, 37):  # one-hot inputs: layer 1's code is the sign pattern of W1[j]
         x = np.zeros(256, np.float32)
         x[j] = 1.0
-        _, codes = oracle.hash_predict(hw, x, cfg.n_blk)
+        _, codes, _ = oracle.hash_predict(hw, x, cfg.n_blk)
         code = np.where(hw.w1[j] >= 0, 1, -1)
         assert codes[0] == int(np.argmax(Z @ code))
     # x = 0: every product is 0 and sign(0) = +1, the all-plus bucket
-    _, codes = oracle.hash_predict(hw, np.zeros(256, np.float32), cfg.n_blk)
+    _, codes, _ = oracle.hash_predict(hw, np.zeros(256, np.float32), cfg.n_blk)
     assert codes[0] == 255
 
 
@@ -577,13 +606,39 @@ def test_hash_stack_matches_integer_products_and_argmax_reading():
         hw = lsgen.hash_weights(cfg, layer)
         for _ in range(20):
             x = rng.standard_normal(1024).astype(np.float32)
-            s, codes = oracle.hash_predict(hw, x, cfg.n_blk)
+            s, codes, prods = oracle.hash_predict(hw, x, cfg.n_blk)
             s_ref, idx_ref, dots = _hash_ref(hw, x, cfg.n_blk)
-            # the fp32 first layer agrees with fp64 away from ties
-            assert np.min(np.abs(dots)) > 1e-3
+            # both sides take the first layer in float64 (library matmul against the oracle's
+            # plain loop); only a product within float64 rounding of zero could differ
+            assert np.min(np.abs(dots)) > 1e-9
+            assert np.allclose(prods, dots, rtol=1e-12, atol=1e-12)
             assert codes.tolist() == idx_ref.tolist()
             assert np.array_equal(s, s_ref)
             assert np.array_equal(s, hw.head[codes[-1]].astype(np.float32))
+
+
+def test_hash_imposed_first_bucket_drives_the_later_layers():
+    cfg = lsgen.CONFIGS["llama2_7b_ffn"].with_(d_model=256, d_ff=1024, block=64)
+    hw = lsgen.hash_weights(cfg, 1)
+    x = np.random.default_rng(3).standard_normal(256).astype(np.float32)
+    s, codes, prods = oracle.hash_predict(hw, x, cfg.n_blk)
+    # imposing the bucket the products give changes nothing
+    s2, codes2, prods2 = oracle.hash_predict(hw, x, cfg.n_blk, code0=int(codes[0]))
+    assert np.array_equal(s, s2) and codes.tolist() == codes2.tolist()
+    assert np.array_equal(prods, prods2)
+    # flipping one first-layer bit re-derives layers 2-5 from the flipped code (integer
+    # products of the table row it selects, Eq. hashfunc_layer)
+    T, W = _unpack_signs(hw.tables), _unpack_signs(hw.w_bin)
+    Z = _Z()
+    for bit in range(8):
+        c0 = int(codes[0]) ^ (1 << (7 - bit))
+        s3, codes3, _ = oracle.hash_predict(hw, x, cfg.n_blk, code0=c0)
+        idx = [c0]
+        for k in range(4):
+            code = np.where(W[k] @ T[k, idx[-1]] >= 0, 1, -1)
+            idx.append(int(np.argmax(Z @ code)))
+        assert codes3.tolist() == idx
+        assert np.array_equal(s3, hw.head[idx[-1]].astype(np.float32))
 
 
 def test_hash_xnor_popcount_equals_signed_product():
