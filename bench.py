@@ -95,33 +95,115 @@ def mean_union_size(f, cfg, xs, B: int, lsffn, torch) -> float:
     return total / n
 
 
-def cpu_baseline(cfg, weights, xs, n_tokens: int, B: int = 1):
-    """The CPU oracle (as it stands) on the first n_tokens decode steps of the same workload:
-    at B = 1 its C layer step, at B > 1 its predictor, union selection and sparse FFN per token."""
+def host_cpu_info() -> dict:
+    """Host CPU model string, nproc, the size of this process's affinity mask and the threads
+    the oracle may use: the affinity mask, capped by OMP_NUM_THREADS when that is set (the
+    machine's CPU share for this job)."""
+    model = platform.processor() or platform.machine()
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    aff = len(os.sched_getaffinity(0))
+    n = aff
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return {"cpu": model, "nproc": os.cpu_count(), "affinity": aff, "threads": n}
+
+
+def cpu_baseline(cfg, weights, xs, max_tokens: int, B: int = 1, budget_s: float = 12.0):
+    """The CPU oracle (as it stands) on the first decode steps of the same workload, both on one
+    thread and with its output loops split over every core this job may use (the same sums in
+    the same order, so the same results).  Each leg decodes tokens until budget_s has passed or
+    max_tokens are done.  At B = 1 the oracle's C layer step; at B > 1 its predictor, union
+    selection and sparse FFN per token (single thread only)."""
     import numpy as np
 
     import oracle
-    t0 = time.perf_counter()
-    for t in range(n_tokens):
-        if B == 1:
-            x = xs[t, 0].copy()
-            for l in range(cfg.n_layers):
-                _, _, _, x = oracle.layer_step(weights[l], cfg, x)
-            continue
-        x = xs[t, :B].astype(np.float64)
-        for l in range(cfg.n_layers):
-            w = weights[l]
-            h = np.stack([oracle.mlp_input(x[b], cfg.prenorm) for b in range(B)])
-            s = np.stack([oracle.predict(w.p1, w.p2, h[b]) for b in range(B)]).astype(np.float32)
-            idx, cnt = oracle.select(s, k=cfg.k, union_batch=True, cap=min(cfg.n_blk, B * cfg.k))
-            blocks = idx[:cnt[0]]
-            x = np.stack([x[b] + oracle.sparse_ffn(w, h[b], blocks, cfg.block, cfg.act, w.threshold)
-                          for b in range(B)]).astype(np.float32).astype(np.float64)
-    dt = time.perf_counter() - t0
-    return {"value": B * n_tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n_tokens} decode steps x {cfg.n_layers} layers of the same workload "
-                      f"(B={B}), fp64 oracle, single thread, {dt:.1f} s",
-            "cpu": platform.processor() or platform.machine()}
+    info = host_cpu_info()
+
+    def leg(n_threads):
+        t0 = time.perf_counter()
+        done = 0
+        while done < max_tokens and (done == 0 or time.perf_counter() - t0 < budget_s):
+            t = done
+            if B == 1:
+                x = xs[t, 0].copy()
+                for l in range(cfg.n_layers):
+                    _, _, _, x = oracle.layer_step(weights[l], cfg, x, n_threads=n_threads)
+            else:
+                x = xs[t, :B].astype(np.float64)
+                for l in range(cfg.n_layers):
+                    w = weights[l]
+                    h = np.stack([oracle.mlp_input(x[b], cfg.prenorm) for b in range(B)])
+                    s = np.stack([oracle.predict(w.p1, w.p2, h[b]) for b in range(B)]).astype(np.float32)
+                    idx, cnt = oracle.select(s, k=cfg.k, union_batch=True, cap=min(cfg.n_blk, B * cfg.k))
+                    blocks = idx[:cnt[0]]
+                    x = np.stack([x[b] + oracle.sparse_ffn(w, h[b], blocks, cfg.block, cfg.act, w.threshold)
+                                  for b in range(B)]).astype(np.float32).astype(np.float64)
+            done += 1
+        return done, time.perf_counter() - t0
+
+    n1, dt1 = leg(0)
+    single = {"value": B * n1 / dt1, "unit": "tokens/s", "cores": 1,
+              "sample": f"first {n1} decode steps x {cfg.n_layers} layers (B={B}), {dt1:.1f} s"}
+    if B == 1 and info["threads"] > 1:
+        nN, dtN = leg(info["threads"])
+        return {"value": nN / dtN, "unit": "tokens/s", "cores": info["threads"], "kind": "oracle",
+                "sample": f"first {nN} decode steps x {cfg.n_layers} layers of the same workload (B=1), "
+                          f"fp64 oracle, output loops split over {info['threads']} threads, {dtN:.1f} s",
+                "single_core": single, **info}
+    return {"value": single["value"], "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": single["sample"] + ", fp64 oracle, single thread", **info}
+
+
+def check_fused_against_kernels(f, cfg, x0, lsffn, torch, dev):
+    """One decode step (B = 1) checked layer by layer: when it ran the fused kernel, its layer
+    input x_l and scores (kept by the library) are fed to the per-kernel entry points (the
+    selection on those scores, then the sparse FFN on x_l), and the fused kernel's layer output
+    x_{l+1} - x_l must match theirs within 2e-3 (relative L2 and largest element, over the
+    largest element).  Returns None when the step did not run the fused kernel."""
+    import numpy as np
+    x = torch.from_numpy(np.ascontiguousarray(x0)).to(dev)
+    f.ls_decode_step(x, 1, cfg.k)
+    f.ls_ffn_sync()
+    xin = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
+    scores = torch.empty(1, cfg.n_blk, dtype=torch.float32, device=dev)
+    try:
+        f.ls_debug_decode_trace(0, scores=scores)
+    except lsffn.LsError:
+        return None
+    idx = torch.empty(cfg.k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    out = torch.empty(1, cfg.d_model, dtype=torch.float32, device=dev)
+    xf = x.cpu().numpy()[0].astype(np.float64)
+    worst = 0.0
+    x_l = torch.from_numpy(np.ascontiguousarray(x0)).to(dev)
+    for l in range(cfg.n_layers):
+        if l > 0:
+            f.ls_debug_decode_trace(l, x_in=xin[0])
+            x_l = xin.clone()
+        f.ls_debug_decode_trace(l, scores=scores[0])
+        if l + 1 < cfg.n_layers:
+            f.ls_debug_decode_trace(l + 1, x_in=xin[0])
+            x_next = xin[0].cpu().numpy().astype(np.float64)
+        else:
+            x_next = xf
+        f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 0, cfg.k, idx, cnt)
+        f.ls_sparse_ffn_step(l, x_l, 1, idx, cnt, 0, cfg.k, out)
+        xl = x_l[0].cpu().numpy().astype(np.float64)
+        y_k = out[0].cpu().numpy().astype(np.float64) - xl
+        y_f = x_next - xl
+        err = max(np.linalg.norm(y_f - y_k) / np.linalg.norm(y_k),
+                  np.max(np.abs(y_f - y_k)) / np.max(np.abs(y_k)))
+        worst = max(worst, float(err))
+    f.ls_ffn_sync()
+    return {"layers": cfg.n_layers, "worst_y_err": worst, "ok": worst <= 2e-3,
+            "what": "fused kernel vs per-kernel entry points on its own layer inputs and scores"}
 
 
 def overlap_from_trace(d: str) -> dict:
@@ -673,7 +755,11 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--config", default="llama2_7b_ffn")
     ap.add_argument("--batch", type=int, default=1)
-    ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle sample size (0: skip)")
+    ap.add_argument("--cpu-tokens", type=int, default=64,
+                    help="most tokens per CPU-oracle leg (each leg stops after about 12 s; 0: skip)")
+    ap.add_argument("--repeats", type=int, default=5, help="timed repetitions of --steps steps (median reported)")
+    ap.add_argument("--no-check", dest="check", action="store_false",
+                    help="skip the per-layer check of one timed step against the per-kernel path")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (testing)")
     ap.add_argument("--path", choices=("auto", "kernels", "fused"), default="auto",
                     help="decode path: fused kernel when supported (auto), per-kernel sequence, fused only")
@@ -778,7 +864,8 @@ def main() -> int:
         weights.append(w if keep_host else None)
         if (l + 1) % 8 == 0:
             print(f"set-up: {l + 1}/{cfg.n_layers} layers", file=sys.stderr, flush=True)
-    xs = lsgen.tokens(cfg, 0, W + K, B)                      # [W+K, B, d] fp32
+    R = args.repeats
+    xs = lsgen.tokens(cfg, 0, W + R * K, B)                  # [W+R*K, B, d] fp32, a fresh token per step
     x_dev = torch.from_numpy(xs).to(dev)                      # inputs resident in HBM
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
@@ -796,6 +883,12 @@ def main() -> int:
                 out[name] = {"total_ms": ms, "launches": n, "avg_us": 1e3 * ms / n}
         return out
 
+    # streaming-read ceiling of this device, measured in the same run (1 GiB, 16-byte loads)
+    probe = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+    ceil_best, ceil_med = f.ls_measure_read_bandwidth(probe, reps=10)
+    del probe
+    torch.cuda.synchronize()
+
     # warm-up; its second half (at most 16 steps; the first steps run cold) brackets every
     # launch with HIP events for the per-kernel breakdown
     n_bd = min(W // 2, 16)
@@ -807,6 +900,7 @@ def main() -> int:
             f.ls_kernel_timing(0, reset=True)
         f.ls_decode_step(x_dev[i], B, cfg.k)
     torch.cuda.synchronize()
+    f.ls_ffn_sync()                     # a device-side failure ends the run here
     if n_bd:
         per_kernel = kernel_times()
         f.ls_set_kernel_timing(False)
@@ -819,18 +913,26 @@ def main() -> int:
     else:
         f.ls_set_kernel_timing(True)
     f.ls_kernel_timing(0, reset=True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for i in range(K):
-        f.ls_decode_step(x_dev[W + i], B, cfg.k)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    # R repetitions of exactly K steps, each between synchronisations; each step decodes a
+    # fresh token
+    walls, gpu_mss = [], []
+    for rep in range(R):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        for i in range(K):
+            f.ls_decode_step(x_dev[W + rep * K + i], B, cfg.k)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        gpu_mss.append(ev0.elapsed_time(ev1))
+    f.ls_ffn_sync()
+    order = sorted(range(R), key=lambda r: walls[r])
+    med = order[R // 2]
+    wall, gpu_ms = walls[med], gpu_mss[med]
     live = kernel_times()
     f.ls_set_kernel_timing(False)
-    gpu_ms = ev0.elapsed_time(ev1)
     if not per_kernel:
         per_kernel = live
         dom_name = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])[0]
@@ -845,6 +947,11 @@ def main() -> int:
         U = mean_union_size(f, cfg, x_dev[W:W + K], B, lsffn, torch)
     bytes_step = int(round(sum(algorithmic_bytes_per_layer(cfg, U) for _ in range(cfg.n_layers))))
     eff_gbs = bytes_step / step_s / 1e9
+    # the same bytes split: FFN blocks and bias only, and with the predictor counted as the two
+    # factors P1, P2 in the weight type (the specification's formula) instead of as stored
+    ffn_only = int(round(cfg.n_layers * (algorithmic_bytes_per_layer(cfg, U) - predictor_bytes(cfg))))
+    factors = cfg.elem_bytes * (cfg.rank * cfg.d_model + cfg.n_blk * cfg.rank)
+    with_factors = ffn_only + cfg.n_layers * factors
 
     # dominant kernel: its algorithmic bytes per launch over its launch time in the timed region
     s = cfg.elem_bytes
@@ -863,13 +970,22 @@ def main() -> int:
         achieved = dom_bytes / (dom_t["avg_us"] * 1e-6) / 1e9
         roofline = {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "measured_ceiling_GBs": round(ceil_best, 1),
+                    "frac_of_measured_ceiling": round(achieved / ceil_best, 4),
                     "traffic": measured_traffic(dom_name, cfg, args.layers in (0, lsgen.CONFIGS[args.config].n_layers)),
                     "bytes_per_launch": dom_bytes,
                     "avg_launch_us": round(dom_t["avg_us"], 3)}
 
+    check = None
+    if B == 1 and args.check:
+        check = check_fused_against_kernels(f, cfg, xs[W + R * K - 1], lsffn, torch, dev)
+        if check is not None and not check["ok"]:
+            print(f"output check failed: {check}", file=sys.stderr)
+            return 1
+
     cpu = None
     if args.cpu_tokens > 0:
-        cpu = cpu_baseline(cfg, weights, xs, min(args.cpu_tokens, W + K), B)
+        cpu = cpu_baseline(cfg, weights, xs, min(args.cpu_tokens, W + R * K), B)
 
     out = {
         "metric": "sparse-FFN decode tokens/sec and effective weight GB/s (% HBM peak), 1 GPU",
@@ -892,8 +1008,19 @@ def main() -> int:
         "effective_weight_GBs": round(eff_gbs, 1),
         "hbm_frac_of_peak": round(eff_gbs / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_step": bytes_step,
+        "bytes_per_step": {"ffn_only": ffn_only, "ffn_plus_predictor_as_stored": bytes_step,
+                           "ffn_plus_predictor_factors": with_factors},
+        "hbm_frac_of_peak_factors_counted": round(with_factors / step_s / 1e9 / HBM_PEAK_GBS, 4),
         "blocks_per_layer": round(U, 2),
         "gpu_event_ms": round(gpu_ms, 3),
+        "repeats": {"n": R, "ms_per_step_median": round(1e3 * walls[med] / K, 4),
+                    "ms_per_step_min": round(1e3 * min(walls) / K, 4),
+                    "tokens_per_s_median": round(B * K / walls[med], 2),
+                    "tokens_per_s_max": round(B * K / min(walls), 2)},
+        "hbm_read_ceiling_GBs": {"best": round(ceil_best, 1), "median": round(ceil_med, 1),
+                                 "how": "ls_measure_read_bandwidth: 1 GiB, 16-byte nontemporal loads, "
+                                        "8 workgroups per CU, 10 launches"},
+        "output_check": check,
         "kernels": {k: {kk: round(vv, 3) if isinstance(vv, float) else vv for kk, vv in v.items()}
                     for k, v in per_kernel.items()},
         "kernels_from": (f"the last {n_bd} warm-up steps, every launch bracketed by HIP events" if n_bd

@@ -94,7 +94,14 @@ typedef struct {
 
 /* Create a context on the current HIP device.  Allocates the weight arena
  * (HBM, or pinned host + HBM cache) and the workspaces.
- * LS_E_INVAL on a bad descriptor; LS_E_NOMEM if an allocation fails. */
+ * The context is the holder of the model's FFN weights in the problem setting
+ * of Sec. 1: weights kept in a large tier (here HBM, or pinned host memory
+ * standing in for the paper's storage) of which each decode step reads only the
+ * predicted sub-matrices.  desc is read during the call only.  On success *out
+ * receives a context the caller owns and releases with ls_ffn_destroy; on
+ * failure *out is set to NULL and ls_last_error(NULL) describes it.
+ * LS_E_INVAL on a bad descriptor; LS_E_NOMEM if an allocation fails (for
+ * instance an hbm_cache_bytes the device cannot hold). */
 ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out);
 
 /* Copy one layer's weights (host, nn.Linear layouts) into the context's own
@@ -105,7 +112,9 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out);
  * of range. */
 ls_status ls_ffn_set_layer(ls_ffn* ctx, int32_t layer, const ls_layer_weights* w);
 
-/* Release everything the context owns.  Synchronises the stream. */
+/* Release everything the context owns (the counterpart of ls_ffn_create,
+ * Sec. 1 problem setting).  Synchronises the stream and the copy stream first.
+ * LS_E_INVAL for a NULL ctx.  ctx is invalid afterwards. */
 ls_status ls_ffn_destroy(ls_ffn* ctx);
 
 /* Predictor (Sec. 3.3.3): h = prenorm(x); scores = P2 (P1 h).
@@ -145,12 +154,18 @@ ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int3
                              const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
                              float* x_acc);
 
-/* LS_WEIGHTS_HOST: make blocks idx_host[0..n) of `layer` resident in the HBM
- * cache, copying misses from pinned host memory in priority order on a copy
- * stream, in n_stages equal contiguous stages; the following
- * ls_sparse_ffn_step calls of this layer wait for the stages they read.  No
- * block of this request is evicted to make room for another of it.
- * LS_WEIGHTS_HBM: no copy, all hits.  LS_E_CAPACITY if n exceeds the cache
+/* The I/O side of Sec. 3.2.1 (Alg. 1: weight blocks loaded in priority order
+ * while the GPU computes the blocks already present) with the block layout of
+ * Sec. 3.2.2 (one contiguous chunk per block, so one copy per block).
+ * LS_WEIGHTS_HOST: make blocks idx_host[0..n) of `layer` (host int32 list, in
+ * priority order, read during the call only) resident in the HBM cache, copying
+ * misses from pinned host memory in priority order on a copy stream, in
+ * n_stages equal contiguous stages; the following ls_sparse_ffn_step calls of
+ * this layer wait for the stages they read.  No block of this request is
+ * evicted to make room for another of it.  Blocks of other layers that it
+ * evicts drop out of those layers' slot tables: their later steps treat them
+ * as not resident.  LS_WEIGHTS_HBM: no copy, all hits.  LS_E_INVAL on a block
+ * id out of range, n < 0 or n_stages < 1; LS_E_CAPACITY if n exceeds the cache
  * slots.  stats may be NULL. */
 ls_status ls_stream_weights(ls_ffn* ctx, int32_t layer, const int32_t* idx_host, int32_t n,
                             int32_t n_stages, ls_stream_stats* stats);
@@ -237,10 +252,15 @@ ls_status ls_decode_step_streamed(ls_ffn* ctx, float* x, int32_t k, int32_t n_st
  * LS_E_STATE if no flagged step has run the layer. */
 ls_status ls_debug_stages_done(ls_ffn* ctx, int32_t layer, int32_t* n_done);
 
-/* One decode step over every layer: for l in 0..L-1:
+/* One decode step over every layer (Sec. 2.1, Eq. 1 for every layer, the
+ * priority list predicted from each layer's complete input): for l in 0..L-1:
  *   scores = predict(l, x); idx = topk(scores, k) (union over the B tokens if B > 1);
  *   x = x + sparse_ffn(l, x, idx[0..count)).
- * x: dev fp32 [B, d], updated in place.  Equal to composing the calls above. */
+ * x: dev fp32 [B, d], updated in place.  1 <= k <= n_blk, 1 <= B <= max_batch
+ * (LS_E_INVAL otherwise); LS_E_STATE if a layer was never set; with host-
+ * resident weights LS_E_UNSUPPORTED (use ls_decode_step_streamed).  Equal to
+ * composing the calls above.  The fused path's device-side failures (a bounded
+ * wait that ran out) are reported by the next ls_ffn_sync. */
 ls_status ls_decode_step(ls_ffn* ctx, float* x, int32_t B, int32_t k);
 
 /* Debug: copy the activations a [B, n_sel * block] (fp32, priority-list order)
@@ -334,8 +354,25 @@ ls_status ls_debug_phase_trace(ls_ffn* ctx, int64_t* host_out, int64_t cap, int6
 ls_status ls_ffn_sync(ls_ffn* ctx);
 
 /* Text of the last failure on ctx (or of the last failed ls_ffn_create when
- * ctx is NULL); valid until the next call on ctx. */
+ * ctx is NULL); valid until the next call on ctx.  The status-code contract
+ * of the boundary (Sec. 1 problem setting: the library is called from a
+ * serving loop that must not abort). */
 const char* ls_last_error(const ls_ffn* ctx);
+
+/* Measurement: the HBM streaming-read ceiling of the device.  Reads buf
+ * (dev, `bytes` bytes, a multiple of 16, at least 1 MiB) reps times with a
+ * kernel of 16-byte nontemporal loads over 8 workgroups per compute unit, each
+ * workgroup a contiguous range, on the context's stream, and returns the
+ * fastest and the median read rate in GB/s (1e9 bytes per second) from HIP
+ * events around each launch.  Synchronises the stream.  Allocates a small
+ * device result buffer per call.  LS_E_INVAL on bad arguments. */
+ls_status ls_measure_read_bandwidth(ls_ffn* ctx, const void* buf, int64_t bytes, int32_t reps,
+                                    double* best_gbs, double* median_gbs);
+
+/* Digest (hex sha256) of the library sources this binary was built from, or
+ * "unknown".  The Python binding refuses a library whose digest differs from
+ * the sources beside it. */
+const char* ls_build_digest(void);
 
 #ifdef __cplusplus
 }

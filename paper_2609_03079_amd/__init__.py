@@ -9,8 +9,10 @@ it has not been built, every call raises ``RuntimeError``.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 
 import numpy as np
 
@@ -31,7 +33,7 @@ EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", 
            "ls_set_hash_predictor", "ls_hash_predict",
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
-           "ls_debug_stages_done", "ls_last_error")
+           "ls_debug_stages_done", "ls_measure_read_bandwidth", "ls_build_digest", "ls_last_error")
 (LS_CFG_DECODE_PATH, LS_CFG_SPEC_BLOCKS, LS_CFG_TRACE_WG, LS_CFG_COOPERATIVE, LS_CFG_BATCH_MFMA, LS_CFG_ZERO_SKIP,
  LS_CFG_STREAM_SYNC, LS_CFG_STAGE_WAIT_US) = range(8)
 LS_SYNC_EVENTS, LS_SYNC_FLAGS, LS_SYNC_HOST = range(3)
@@ -91,6 +93,14 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"HIP library not built: {LIB_PATH} is missing (run __graft_entry__.build())")
     lib = ctypes.CDLL(LIB_PATH)
+    from . import build as _build
+    lib.ls_build_digest.argtypes = []
+    lib.ls_build_digest.restype = ctypes.c_char_p
+    built = lib.ls_build_digest().decode()
+    want = _build.source_digest()
+    if built != want:
+        raise RuntimeError(f"{LIB_PATH} was built from other sources (digest {built[:12]}, sources "
+                           f"{want[:12]}): rebuild it (__graft_entry__.build())")
     P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.ls_ffn_create.argtypes = [ctypes.POINTER(LsFfnDesc), ctypes.POINTER(ctypes.c_void_p)]
     lib.ls_ffn_set_layer.argtypes = [P, I32, ctypes.POINTER(LsLayerWeights)]
@@ -111,10 +121,13 @@ def load():
     lib.ls_ffn_sync.argtypes = [P]
     lib.ls_debug_decode_trace.argtypes = [P, I32, P, P]
     lib.ls_debug_phase_trace.argtypes = [P, P, I64, ctypes.POINTER(I64)]
+    lib.ls_measure_read_bandwidth.argtypes = [P, P, I64, I32, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_double)]
     lib.ls_last_error.argtypes = [P]
     lib.ls_last_error.restype = ctypes.c_char_p
-    for name in EXPORTS[:-1]:
-        getattr(lib, name).restype = ctypes.c_int
+    for name in EXPORTS:
+        if name not in ("ls_last_error", "ls_build_digest"):
+            getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -132,6 +145,21 @@ def _ptr(t) -> int | None:
 
 def _host_ptr(a):
     return None if a is None else np.ascontiguousarray(a).ctypes.data
+
+
+_live = weakref.WeakSet()
+
+
+@atexit.register
+def _close_all():
+    """Destroy every context still open at interpreter exit, while the HIP runtime is alive:
+    objects left to the garbage collector would otherwise be released during interpreter
+    teardown, after the runtime's own exit handlers may have run."""
+    for f in list(_live):
+        try:
+            f.close()
+        except Exception:
+            pass
 
 
 class Ffn:
@@ -155,6 +183,7 @@ class Ffn:
                                                                           block, rank)
         self.n_blk = d_ff // block
         self.max_batch = max_batch
+        _live.add(self)
 
     def close(self):
         if getattr(self, "ctx", None):
@@ -260,6 +289,14 @@ class Ffn:
         _check(self.lib, self.ctx, self.lib.ls_kernel_timing(self.ctx, kernel, int(reset),
                                                              ctypes.byref(ms), ctypes.byref(n)))
         return ms.value, n.value
+
+    def ls_measure_read_bandwidth(self, buf, reps: int = 10):
+        """(best, median) GB/s of a streaming-read kernel over the device tensor buf."""
+        best, med = ctypes.c_double(), ctypes.c_double()
+        nbytes = buf.numel() * buf.element_size()
+        _check(self.lib, self.ctx, self.lib.ls_measure_read_bandwidth(self.ctx, _ptr(buf), nbytes, reps,
+                                                                      ctypes.byref(best), ctypes.byref(med)))
+        return best.value, med.value
 
     def ls_debug_last_activations(self, dst) -> int:
         n = ctypes.c_int64()

@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import concurrent.futures as cf
+import hashlib
 import os
 import subprocess
 
@@ -19,6 +20,24 @@ HIPCC_FLAGS = [
 ]
 
 
+ROOT = os.path.dirname(HERE)
+
+
+def source_digest() -> str:
+    """sha256 over the library's sources (every file in csrc/, the public header and this
+    build script), each as its path relative to the repository and its bytes, in path order."""
+    files = [os.path.join(CSRC, f) for f in os.listdir(CSRC)
+             if f.endswith((".hip", ".h", ".cpp"))]
+    files += [os.path.join(ROOT, "include", "ls_ffn.h"), os.path.abspath(__file__)]
+    h = hashlib.sha256()
+    for path in sorted(files, key=lambda p: os.path.relpath(p, ROOT)):
+        h.update(os.path.relpath(path, ROOT).encode() + b"\0")
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+        h.update(b"\0")
+    return h.hexdigest()
+
+
 def _hipcc() -> str:
     rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
     p = os.path.join(rocm, "bin", "hipcc")
@@ -30,9 +49,12 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = [s for s in SOURCES if os.path.exists(os.path.join(CSRC, s))]
 
+    digest = source_digest()
+
     def compile_one(src: str) -> str:
         obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        cmd = [_hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [_hipcc(), *HIPCC_FLAGS, f'-DLS_BUILD_DIGEST="{digest}"', "-c", os.path.join(CSRC, src),
+               "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

@@ -475,6 +475,8 @@ ls_status ls_ffn_destroy(ls_ffn* c) {
 
 const char* ls_last_error(const ls_ffn* c) { return c ? c->err.c_str() : g_create_error.c_str(); }
 
+static ls_status upload_table(ls_ffn* c, int32_t layer);
+
 ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) {
     ls_status st = check_ctx(c);
     if (st != LS_OK) return st;
@@ -499,6 +501,8 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
         c->staging_bytes = need;
     }
     LS_HIP(c, hipStreamSynchronize(c->stream));  // staging may still feed an earlier copy
+    // host-resident blocks of this layer may still feed queued cache fills
+    if (c->copy_stream) LS_HIP(c, hipStreamSynchronize(c->copy_stream));
     uint8_t* blocks_dst;
     size_t off_small;
     if (c->desc.residency == LS_WEIGHTS_HBM) {
@@ -546,7 +550,16 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
     c->dev[layer].bias =
         w->b_gate ? c->arena[layer] + (c->desc.residency == LS_WEIGHTS_HBM ? lay.bias : 0) : nullptr;
     c->dev[layer].threshold = w->threshold;
-    if (c->desc.residency == LS_WEIGHTS_HOST) c->bcache->invalidate_layer(layer);
+    if (c->desc.residency == LS_WEIGHTS_HOST) {
+        // the cached copies hold the old weights: drop them, give the device an empty table
+        // and require a new ls_stream_weights before the next step of this layer
+        c->bcache->invalidate_layer(layer);
+        ls_status st2 = upload_table(c, layer);
+        if (st2 != LS_OK) return st2;
+        LS_HIP(c, hipStreamSynchronize(c->copy_stream));
+        c->streamed[layer] = 0;
+        c->stage_ranges[layer].clear();
+    }
     {
         ls::LayerPtrs lp{};
         lp.blocks = c->dev[layer].blocks;
@@ -637,6 +650,9 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
             return fail(c, LS_E_STATE, "blocks of this layer were not streamed (ls_stream_weights)");
         L.blocks = c->cache;
         slot_table = c->slot_tables + (size_t)layer * s.n_blk;
+        // the layer's table may have been rewritten since its own stages (another layer's
+        // request evicted some of its blocks)
+        LS_HIP(c, hipStreamWaitEvent(c->stream, c->table_uploaded[layer], 0));
         st = wait_stages(c, layer, begin, end);
         if (st != LS_OK) return st;
     }
@@ -661,6 +677,21 @@ ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t*
     for (int b = 0; b < c->last_act_B; ++b)
         LS_HIP(c, hipMemcpyAsync(dst + (size_t)b * n, c->a + (size_t)b * c->shape.F, (size_t)n * sizeof(float),
                                  hipMemcpyDeviceToDevice, c->stream));
+    return LS_OK;
+}
+
+// Host-resident mode: rewrite the device slot table of `layer` from the block cache, on the
+// copy stream (so copies queued after it see it first) and record table_uploaded[layer], which
+// every later sparse step of the layer waits for.  The pinned mirror may still feed the
+// previous upload, hence the wait on the same event first.
+static ls_status upload_table(ls_ffn* c, int32_t layer) {
+    const Shape& s = c->shape;
+    int32_t* tab = c->slot_tables_host + (size_t)layer * s.n_blk;
+    LS_HIP(c, hipEventSynchronize(c->table_uploaded[layer]));
+    c->bcache->slot_table(layer, tab);
+    LS_HIP(c, hipMemcpyAsync(c->slot_tables + (size_t)layer * s.n_blk, tab, (size_t)s.n_blk * sizeof(int32_t),
+                             hipMemcpyHostToDevice, c->copy_stream));
+    LS_HIP(c, hipEventRecord(c->table_uploaded[layer], c->copy_stream));
     return LS_OK;
 }
 
@@ -691,16 +722,21 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
         for (int l = 0; l < c->desc.n_layers; ++l)
             if (wait[(size_t)l] && c->layer_done_recorded[(size_t)l])
                 LS_HIP(c, hipStreamWaitEvent(c->copy_stream, c->layer_done[(size_t)l], 0));
+        // Tables first, all before any copy: every other layer that lost a slot gets a table
+        // without that block (a block not in the cache contributes nothing), and this layer's
+        // table only changes entries of blocks filled below.  No compute queued so far reads
+        // the slots being reassigned (the copy stream waited for it), and later steps of those
+        // layers wait for their new table.
+        for (int l = 0; l < c->desc.n_layers; ++l)
+            if (wait[(size_t)l] && l != layer) {
+                ls_status st = upload_table(c, l);
+                if (st != LS_OK) return st;
+            }
     }
-    int32_t* tab = c->slot_tables_host + (size_t)layer * s.n_blk;
-    // the pinned table of this layer may still feed its previous upload
-    LS_HIP(c, hipEventSynchronize(c->table_uploaded[layer]));
-    c->bcache->slot_table(layer, tab);
-    // table upload first: it only changes entries of blocks filled below, which no earlier
-    // compute of this layer reads any more (the copy stream waited for it).
-    LS_HIP(c, hipMemcpyAsync(c->slot_tables + (size_t)layer * s.n_blk, tab, (size_t)s.n_blk * sizeof(int32_t),
-                             hipMemcpyHostToDevice, c->copy_stream));
-    LS_HIP(c, hipEventRecord(c->table_uploaded[layer], c->copy_stream));
+    {
+        ls_status st = upload_table(c, layer);
+        if (st != LS_OK) return st;
+    }
     auto& events = c->stage_events[layer];
     auto& ranges = c->stage_ranges[layer];
     while ((int)events.size() < n_stages) {
@@ -1143,6 +1179,56 @@ ls_status ls_debug_stages_done(ls_ffn* c, int32_t layer, int32_t* n_done) {
     *n_done = n;
     return LS_OK;
 }
+
+ls_status ls_measure_read_bandwidth(ls_ffn* c, const void* buf, int64_t bytes, int32_t reps,
+                                    double* best_gbs, double* median_gbs) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    if (!buf || !best_gbs || !median_gbs) return fail(c, LS_E_INVAL, "null pointer");
+    if (bytes < (1 << 20) || bytes % 16) return fail(c, LS_E_INVAL, "bytes must be >= 1 MiB and a multiple of 16");
+    if (reps < 1 || reps > 1000) return fail(c, LS_E_INVAL, "reps must be in 1..1000");
+    int dev = 0, cus = 0;
+    LS_HIP(c, hipGetDevice(&dev));
+    LS_HIP(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    const int grid = 8 * std::max(cus, 1);
+    uint32_t* out = nullptr;
+    if (hipMalloc(reinterpret_cast<void**>(&out), (size_t)grid * 4 * sizeof(uint32_t)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(c, LS_E_NOMEM, "device allocation for the read probe failed");
+    }
+    std::vector<hipEvent_t> ev((size_t)reps + 1, nullptr);
+    hipError_t e = hipSuccess;
+    for (auto& x : ev)
+        if (e == hipSuccess) e = hipEventCreate(&x);
+    // one untimed pass so the first timed one does not pay for first-touch work
+    if (e == hipSuccess) e = ls::launch_read_probe(buf, (size_t)bytes, out, grid, c->stream);
+    if (e == hipSuccess) e = hipEventRecord(ev[0], c->stream);
+    for (int r = 0; r < reps && e == hipSuccess; ++r) {
+        e = ls::launch_read_probe(buf, (size_t)bytes, out, grid, c->stream);
+        if (e == hipSuccess) e = hipEventRecord(ev[(size_t)r + 1], c->stream);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    std::vector<double> gbs;
+    for (int r = 0; r < reps && e == hipSuccess; ++r) {
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, ev[(size_t)r], ev[(size_t)r + 1]);
+        if (e == hipSuccess) gbs.push_back((double)bytes / (ms * 1e-3) / 1e9);
+    }
+    for (auto x : ev)
+        if (x) (void)hipEventDestroy(x);
+    const hipError_t ef = hipFree(out);
+    LS_HIP(c, e);
+    LS_HIP(c, ef);
+    std::sort(gbs.begin(), gbs.end());
+    *best_gbs = gbs.back();
+    *median_gbs = gbs[gbs.size() / 2];
+    return LS_OK;
+}
+
+#ifndef LS_BUILD_DIGEST
+#define LS_BUILD_DIGEST "unknown"
+#endif
+const char* ls_build_digest(void) { return LS_BUILD_DIGEST; }
 
 ls_status ls_ffn_sync(ls_ffn* c) {
     ls_status st = check_ctx(c);

@@ -98,6 +98,10 @@ hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_ta
                        int begin, int end, const float* x_in, float* x_acc, float* part,
                        hipStream_t st);
 
+// Streaming read of `bytes` (a multiple of 16) at buf by `grid` workgroups of 256 threads;
+// out: 4 * grid words of scratch.
+hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* out, int grid, hipStream_t st);
+
 // ---- persistent consumer of a streamed layer's copy stages (ls_stage.hip) ----------------
 constexpr int kMaxStages = 64;
 struct StageArgs {

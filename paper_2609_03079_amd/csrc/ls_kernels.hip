@@ -492,4 +492,36 @@ hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_ta
     return hipErrorInvalidValue;
 }
 
+// ---- streaming-read ceiling (measurement) ------------------------------------------------
+// Workgroup w reads the contiguous vector range [w n / G, (w + 1) n / G) of 16-byte vectors,
+// eight loads in flight per thread, and folds them with XOR; each wave writes one word so the
+// loads cannot be dropped.  out holds 4 words per workgroup.
+__global__ __launch_bounds__(256) void read_probe_kernel(const u32x4* __restrict__ p, size_t n_vec,
+                                                         uint32_t* __restrict__ out) {
+    const size_t lo = (size_t)blockIdx.x * n_vec / gridDim.x;
+    const size_t hi = (size_t)(blockIdx.x + 1) * n_vec / gridDim.x;
+    uint32_t acc = 0;
+    size_t i = lo + threadIdx.x;
+    for (; i + 7 * 256 < hi; i += 8 * 256) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = ld_stream(p + i + (size_t)u * 256);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < hi; i += 256) {
+        const u32x4 v = ld_stream(p + i);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, off, 64);
+    if ((threadIdx.x & 63) == 0) out[(size_t)blockIdx.x * 4 + (threadIdx.x >> 6)] = acc;
+}
+
+hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* out, int grid, hipStream_t st) {
+    hipLaunchKernelGGL(read_probe_kernel, dim3(grid), dim3(256), 0, st, static_cast<const u32x4*>(buf),
+                       bytes / 16, out);
+    return hipGetLastError();
+}
+
 }  // namespace ls

@@ -24,6 +24,18 @@ def rel_l2(a, b) -> float:
     return float(np.linalg.norm(a - b) / nb)
 
 
+def y_err(a, b) -> float:
+    """Error of an FFN output a against the reference b: the larger of the relative L2 error
+    and the largest element error over the largest reference element, so one wrong output
+    column cannot hide in the vector norm.  Both are held to the same tolerance."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    mb = np.max(np.abs(b)) if b.size else 0.0
+    if mb == 0:
+        return 0.0 if np.all(a == 0) else float("inf")
+    return max(rel_l2(a, b), float(np.max(np.abs(a - b)) / mb))
+
+
 def make_ffn(cfg: lsgen.Config, n_layers: int | None = None, max_batch: int = 1,
              residency: int = lsffn.LS_WEIGHTS_HBM, hbm_cache_bytes: int = 0, weights=None):
     """Context for cfg (optionally fewer layers) and the host weights it was given."""

@@ -18,7 +18,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import SCORE_TOL, Y_TOL, dev_f32, empty_f32, host, make_ffn, rel_l2  # noqa: E402
+from gpu_util import SCORE_TOL, Y_TOL, dev_f32, empty_f32, host, make_ffn, rel_l2, y_err  # noqa: E402
 
 C = lsgen.CONFIGS
 
@@ -60,7 +60,7 @@ def _check_layers(f, ws, cfg, x0, x_final):
         y_gpu = x_next.astype(np.float64) - x_l.astype(np.float64)
         h = oracle.mlp_input(x_l, cfg.prenorm)
         y_ref = oracle.sparse_ffn(ws[l], h, blocks, cfg.block, cfg.act, ws[l].threshold)
-        assert rel_l2(y_gpu, y_ref) <= Y_TOL[cfg.dtype], (l, rel_l2(y_gpu, y_ref))
+        assert y_err(y_gpu, y_ref) <= Y_TOL[cfg.dtype], (l, y_err(y_gpu, y_ref))
 
 
 @pytest.mark.parametrize("name", list(FUSED))
@@ -97,7 +97,7 @@ def test_fused_matches_per_kernel_path_and_is_deterministic(name):
         ref = host(x)[0]
         y_f = outs[0][t].astype(np.float64) - xs[t, 0]
         y_k = ref.astype(np.float64) - xs[t, 0]
-        assert rel_l2(y_f, y_k) <= Y_TOL[cfg.dtype]
+        assert y_err(y_f, y_k) <= Y_TOL[cfg.dtype]
 
 
 def test_fused_speculative_width_does_not_change_results():
@@ -112,7 +112,7 @@ def test_fused_speculative_width_does_not_change_results():
         res.append(host(x)[0].astype(np.float64) - x0[0])
     f.ls_ffn_sync()
     for r in res[1:]:
-        assert rel_l2(r, res[0]) <= Y_TOL[cfg.dtype]
+        assert y_err(r, res[0]) <= Y_TOL[cfg.dtype]
 
 
 def test_fused_unsupported_shape_reports_and_auto_falls_back():
@@ -149,3 +149,19 @@ def test_plain_launch_matches_cooperative_bitwise():
     with pytest.raises(lsffn.LsError) as e:
         f.ls_configure(lsffn.LS_CFG_COOPERATIVE, 2)
     assert e.value.status == lsffn.LS_E_INVAL
+
+
+def test_fused_headline_stack_all_layers_plain_launch():
+    """The full Llama-2-7B-shaped stack (32 layers, d 4096, d_ff 11008, fp16, k = 21 of 172) in
+    the benchmark's configuration (plain launch of the persistent grid, default speculative
+    width), two fresh tokens, every layer teacher-forced against the oracle."""
+    cfg = C["llama2_7b_ffn"]
+    f, ws = _fused_ffn(cfg)
+    f.ls_configure(lsffn.LS_CFG_COOPERATIVE, 0)
+    f.ls_configure(lsffn.LS_CFG_SPEC_BLOCKS, 0)
+    for t in range(2):
+        x0 = lsgen.tokens(cfg, 40 + t, 1, 1)[0, 0]
+        x = dev_f32(x0[None, :])
+        f.ls_decode_step(x, 1, cfg.k)
+        f.ls_ffn_sync()
+        _check_layers(f, ws, cfg, x0, host(x)[0].copy())

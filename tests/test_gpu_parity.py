@@ -18,7 +18,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
 from gpu_util import (SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn,  # noqa: E402
-                      rel_l2)
+                      rel_l2, y_err)
 
 C = lsgen.CONFIGS
 
@@ -34,7 +34,17 @@ SMALL = {
     # 16-bit weights, block a multiple of 32: batches of 4+ run on the matrix cores
     "f16_b64": C["llama2_7b_ffn"].with_(n_layers=2, d_model=640, d_ff=1728, block=64, rank=192,
                                         keep_pct=30),
+    # many small blocks and a narrow rank: the fp32 product P2 P1 (512 x 256) would be larger
+    # than the two fp16 factors, so the library keeps P1 then P2
+    "f16_factored": C["llama2_7b_ffn"].with_(n_layers=2, d_model=256, d_ff=4096, block=8, rank=64,
+                                             keep_pct=5),
 }
+
+
+def _folded(cfg) -> bool:
+    """Whether the library stores the predictor as the fp32 product P2 P1 (no larger than the
+    two factors in their storage type)."""
+    return 4 * cfg.n_blk * cfg.d_model <= cfg.elem_bytes * (cfg.rank * cfg.d_model + cfg.n_blk * cfg.rank)
 
 
 GUARD = 1e-4  # |SiLU(g)| this close to the threshold may be decided either way
@@ -69,15 +79,17 @@ def _check_y(f, ws_l, cfg, xin, yg, blocks, tol, tag):
             flips = keep_gpu != keep_ref
             assert np.all(np.abs(sig[flips] - ws_l.threshold) <= GUARD), (tag, b, int(flips.sum()))
             y_ref = oracle.down(ws_l, neurons, np.where(keep_gpu, a_all, 0.0))
-        assert rel_l2(yg[b], y_ref) <= tol, (tag, b, rel_l2(yg[b], y_ref))
+        assert y_err(yg[b], y_ref) <= tol, (tag, b, y_err(yg[b], y_ref))
 
 
 @pytest.mark.parametrize("B", [1, 4, 7, 8])
 @pytest.mark.parametrize("name", list(SMALL))
 def test_predict_parity(name, B):
     """Batches of 4+ compute four predictor rows per workgroup; the shapes include row counts
-    that are not a multiple of four (50 and 27 blocks) and both the folded and factored forms."""
+    that are not a multiple of four (50 and 27 blocks) and both the folded form (P2 P1 in fp32)
+    and the factored one (P1, then P2: f16_factored)."""
     cfg = SMALL[name]
+    assert _folded(cfg) == (name != "f16_factored")
     f, ws = make_ffn(cfg, max_batch=B)
     xs = lsgen.tokens(cfg, 0, 1, B)[0]
     scores = empty_f32(B, cfg.n_blk)
@@ -181,8 +193,8 @@ def test_stages_eq1_eq2(name):
         for j, (lo, hi) in enumerate(oracle.stage_bounds(k, K)):
             f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, lo, hi, acc)
             got = host(acc)[0].astype(np.float64)
-            assert rel_l2(got - x[0], xt[j] - x[0]) <= tol, (K, j)
-        assert rel_l2(host(acc)[0] - x[0], host(single)[0] - x[0]) <= tol
+            assert y_err(got - x[0], xt[j] - x[0]) <= tol, (K, j)
+        assert y_err(host(acc)[0] - x[0], host(single)[0] - x[0]) <= tol
 
 
 @pytest.mark.parametrize("name", ["c1", "f16_ragged"])
@@ -203,8 +215,8 @@ def test_permutation_invariance(name):
         outs.append(host(out)[0].astype(np.float64) - x[0])
     y_ref = _oracle_y(ws[0], cfg, x[0], blocks)
     for y in outs:
-        assert rel_l2(y, y_ref) <= tol
-        assert rel_l2(y, outs[0]) <= tol
+        assert y_err(y, y_ref) <= tol
+        assert y_err(y, outs[0]) <= tol
 
 
 def test_relu_dead_blocks_exact_zero():
@@ -231,7 +243,7 @@ def test_relu_dead_blocks_exact_zero():
             assert np.all(a[pos] == 0.0)
     y = host(out)[0].astype(np.float64) - x[0]
     y_ref = _oracle_y(w, cfg, x[0], live)
-    assert rel_l2(y, y_ref) <= Y_TOL[cfg.dtype]
+    assert y_err(y, y_ref) <= Y_TOL[cfg.dtype]
 
 
 def test_empty_and_clamped_ranges():
@@ -246,7 +258,7 @@ def test_empty_and_clamped_ranges():
     assert np.array_equal(host(out)[0], x[0])
     f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, 0, 5, out)   # clamped to count = 3
     y = host(out)[0].astype(np.float64) - x[0]
-    assert rel_l2(y, _oracle_y(ws[0], cfg, x[0], [3, 1, 4])) <= Y_TOL[cfg.dtype]
+    assert y_err(y, _oracle_y(ws[0], cfg, x[0], [3, 1, 4])) <= Y_TOL[cfg.dtype]
     zero = dev_f32([0]).int()
     f.ls_sparse_ffn_step(0, x_in, 1, idx, zero, 0, 5, out)  # count 0
     assert np.array_equal(host(out)[0], x[0])
@@ -277,7 +289,7 @@ def test_decode_step_equals_composition_and_is_deterministic():
             xi, xo = host(x_in), host(x_out)
             _check_y(f, ws[l], cfg, xi, xo.astype(np.float64) - xi, blocks, Y_TOL[cfg.dtype], l)
             x_in, x_out = x_out, x_in
-        assert rel_l2(host(x_in) - x0, got - x0) <= Y_TOL[cfg.dtype]
+        assert y_err(host(x_in) - x0, got - x0) <= Y_TOL[cfg.dtype]
 
 
 def test_invalid_arguments_return_codes():
@@ -337,6 +349,37 @@ def test_full_size_layers_sampled(cfg_name):
         x_in, x_out = x_out, x_in
 
 
+def test_mistral_full_width_batch4_matrix_cores():
+    """Two full Mistral-7B-shaped layers (d 4096, d_ff 14336, bf16, thresholded SiLU, 128-neuron
+    blocks, k = 56) at B = 4 on the matrix-core kernels (the union list, eight 512-value chunks
+    per row, bf16 hi + lo activations), teacher-forced per layer against the oracle with the
+    threshold guard band."""
+    cfg = C["mistral_7b_ffn"].with_(n_layers=2)
+    B = 4
+    f, ws = make_ffn(cfg, max_batch=B)
+    f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, 1)
+    xs = lsgen.tokens(cfg, 13, 1, B)[0]
+    x_in = dev_f32(xs)
+    x_out = empty_f32(B, cfg.d_model)
+    scores = empty_f32(B, cfg.n_blk)
+    cap = min(cfg.n_blk, B * cfg.k)
+    idx, cnt = empty_i32(cap), empty_i32(1)
+    for l in range(cfg.n_layers):
+        f.ls_predict(l, x_in, B, scores)
+        f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
+        f.ls_sparse_ffn_step(l, x_in, B, idx, cnt, 0, cap, x_out)
+        xi, xo, sc = host(x_in), host(x_out), host(scores)
+        for b in range(B):
+            ref_s = oracle.predict(ws[l].p1, ws[l].p2, oracle.mlp_input(xi[b], cfg.prenorm))
+            assert rel_l2(sc[b], ref_s) <= SCORE_TOL, (l, b)
+        blocks = host(idx)[:host(cnt)[0]]
+        ref_idx, ref_cnt = oracle.select(sc, k=cfg.k, union_batch=True, cap=cap)
+        assert np.array_equal(blocks, ref_idx[:ref_cnt[0]])
+        assert blocks.size > cfg.k       # a real union of four lists
+        _check_y(f, ws[l], cfg, xi, xo.astype(np.float64) - xi, blocks, Y_TOL[cfg.dtype], l)
+        x_in, x_out = x_out, x_in
+
+
 # ReGLU shapes: with thresholded SiLU, two fp32-accurate paths may decide neurons within
 # rounding of the threshold differently (the oracle tests cover that with a guard band).
 MFMA_CMP = {
@@ -382,7 +425,7 @@ def test_batch_matrix_core_path_matches_vector_path(name, B):
     tol = 1e-5 if cfg.dtype == lsgen.DT_F16 else 1e-4
     for b in range(B):
         for y in ys[1:]:
-            assert rel_l2(ys[0][b], y[b]) <= tol, (name, B, b, rel_l2(ys[0][b], y[b]))
+            assert y_err(ys[0][b], y[b]) <= tol, (name, B, b, y_err(ys[0][b], y[b]))
     with pytest.raises(lsffn.LsError):
         f.ls_configure(lsffn.LS_CFG_BATCH_MFMA, 2)
 

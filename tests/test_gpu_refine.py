@@ -20,7 +20,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2  # noqa: E402
+from gpu_util import SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2, y_err  # noqa: E402
 
 CFG = lsgen.CONFIGS["llama2_7b_planted"].with_(n_layers=2, d_model=1024, d_ff=4096, block=64, rank=256)
 
@@ -47,7 +47,7 @@ def test_refined_prediction_per_stage(K, reverse):
             lo, hi = j * k // K, (j + 1) * k // K
             f.ls_sparse_ffn_step(0, x, 1, lst_d, cnt, lo, hi, acc)  # acc = x + stages 0..j
             xt = host(acc)[0]
-            assert rel_l2(xt - x_np, feats_ref[j + 1] - x_np) <= Y_TOL[CFG.dtype], (t, j)
+            assert y_err(xt - x_np, feats_ref[j + 1] - x_np) <= Y_TOL[CFG.dtype], (t, j)
             f.ls_predict(1, acc, 1, scores)
             s_gpu = host(scores)[0]
             s_ref = oracle.predict(ws[1].p1, ws[1].p2, oracle.mlp_input(xt, CFG.prenorm))

@@ -23,7 +23,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2  # noqa: E402
+from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, y_err  # noqa: E402
 
 CFG = lsgen.CONFIGS["llama2_70b_stream"].with_(n_layers=3, d_model=1024, d_ff=4096, block=128,
                                                  rank=256)  # k = 4 of 32 blocks
@@ -150,7 +150,7 @@ def test_flags_full_size_70b_layers_and_oracle():
             f1.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, k, 0.0, 0, k, idx, cnt)
             y_ref = oracle.sparse_ffn(ws[0], oracle.mlp_input(x0[0], cfg.prenorm), host(idx), cfg.block,
                                       cfg.act, ws[0].threshold)
-            assert rel_l2(host(x1)[0].astype(np.float64) - x0[0], y_ref) <= Y_TOL[cfg.dtype]
+            assert y_err(host(x1)[0].astype(np.float64) - x0[0], y_ref) <= Y_TOL[cfg.dtype]
     assert np.array_equal(outs[lsffn.LS_SYNC_EVENTS], outs[lsffn.LS_SYNC_FLAGS])
 
 

@@ -21,7 +21,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2  # noqa: E402
+from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, y_err  # noqa: E402
 
 # A scaled-down 70B-shaped host-resident stack: 32 blocks of 128 neurons (768 KiB each),
 # 12 cache slots, so three layers of 8-block lists force evictions.
@@ -74,7 +74,7 @@ def test_streamed_equals_resident_bitwise(K):
             x_np = host(x)[0].astype(np.float64)
             y_ref = oracle.sparse_ffn(ws[l], oracle.mlp_input(host(x)[0], CFG.prenorm), idx_h,
                                       CFG.block, CFG.act, ws[l].threshold)
-            assert rel_l2(a[0] - x_np, y_ref) <= Y_TOL[CFG.dtype]
+            assert y_err(a[0] - x_np, y_ref) <= Y_TOL[CFG.dtype]
             x = y_h
     fh.ls_ffn_sync()
 
@@ -94,6 +94,85 @@ def test_cache_accounting_hits_capacity_and_invalidation():
     fh.ls_ffn_set_layer(1, ws[1])  # new weights for layer 1: its cached blocks are stale
     st = fh.ls_stream_weights(1, np.array([3, 5], np.int32))
     assert st.misses == 2
+    fh.ls_ffn_sync()
+
+
+def _cpu_cache(tmp_path):
+    """The library's block cache (the same header) built for the host, to replay a request
+    sequence and learn which blocks stay resident."""
+    import ctypes
+    import os
+    import subprocess
+    csrc = os.path.join(os.path.dirname(lsffn.__file__), "csrc")
+    out = tmp_path / "libbc.so"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-o", str(out),
+                    os.path.join(csrc, "block_cache_capi.cpp")], check=True)
+    lib = ctypes.CDLL(str(out))
+    lib.bc_create.restype = ctypes.c_void_p
+    lib.bc_create.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int]
+    lib.bc_request.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+    lib.bc_slot_table.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    lib.bc_destroy.argtypes = [ctypes.c_void_p]
+    return lib
+
+
+def test_eviction_by_another_layer_drops_the_block_from_the_first_layers_table(tmp_path):
+    """Stream layer 0's list, then layer 1's so that it evicts some of layer 0's blocks, then
+    step layer 0 with its full list: the evicted entries must contribute nothing (bitwise the
+    resident step over the list without them), never layer 1's weights in the reused slots."""
+    fr, fh, ws = _pair()
+    lib = _cpu_cache(tmp_path)
+    h = lib.bc_create(SLOTS, CFG.n_layers, CFG.n_blk)
+    x = dev_f32(lsgen.tokens(CFG, 6, 1, 1)[0])
+    n = 8
+    idx, cnt = _priority_list(fr, 0, x, n)
+    idx_h = host(idx)
+    other = np.array([b for b in range(CFG.n_blk) if b not in set(idx_h.tolist())][:n], np.int32)
+    counts = np.zeros(3, np.int64)
+    fills = np.zeros(4 * n, np.int32)
+    nf = np.zeros(1, np.int32)
+    for layer, blocks in ((0, idx_h), (1, other)):
+        st = fh.ls_stream_weights(layer, blocks, n_stages=2)
+        b = np.ascontiguousarray(blocks, np.int32)
+        assert lib.bc_request(h, layer, b.ctypes.data, n, counts.ctypes.data, fills.ctypes.data,
+                              nf.ctypes.data, -1) == 1
+        assert (st.hits, st.misses, st.evictions) == tuple(counts.tolist())
+    assert counts[2] == 2 * n - SLOTS          # layer 1 evicted this many of layer 0's blocks
+    tab = np.zeros(CFG.n_blk, np.int32)
+    lib.bc_slot_table(h, 0, tab.ctypes.data)
+    lib.bc_destroy(h)
+    kept = np.array([b for b in idx_h if tab[b] >= 0], np.int32)
+    assert kept.size == SLOTS - n
+    y_h = _staged(fh, 0, x, idx, cnt, n, 1)
+    kept_d = torch.from_numpy(kept).to("cuda:0")
+    cnt_k = torch.tensor([kept.size], dtype=torch.int32, device="cuda:0")
+    y_r = _staged(fr, 0, x, kept_d, cnt_k, kept.size, 1)
+    assert np.array_equal(host(y_h), host(y_r))
+    # layer 1 still computes from its own blocks
+    y1_h = _staged(fh, 1, x, torch.from_numpy(other).to("cuda:0"),
+                   torch.tensor([n], dtype=torch.int32, device="cuda:0"), n, 1)
+    y1_r = _staged(fr, 1, x, torch.from_numpy(other).to("cuda:0"),
+                   torch.tensor([n], dtype=torch.int32, device="cuda:0"), n, 1)
+    assert np.array_equal(host(y1_h), host(y1_r))
+    fh.ls_ffn_sync()
+
+
+def test_new_weights_for_a_streamed_layer_need_a_new_request():
+    fr, fh, ws = _pair()
+    x = dev_f32(lsgen.tokens(CFG, 8, 1, 1)[0])
+    n = 6
+    idx, cnt = _priority_list(fr, 0, x, n)
+    fh.ls_stream_weights(0, host(idx))
+    _staged(fh, 0, x, idx, cnt, n, 1)
+    fh.ls_ffn_set_layer(0, ws[1])             # other weights for layer 0
+    with pytest.raises(lsffn.LsError) as e:   # its cached blocks are gone
+        _staged(fh, 0, x, idx, cnt, n, 1)
+    assert e.value.status == lsffn.LS_E_STATE
+    st = fh.ls_stream_weights(0, host(idx))
+    assert st.misses == n
+    fr.ls_ffn_set_layer(0, ws[1])
+    assert np.array_equal(host(_staged(fh, 0, x, idx, cnt, n, 1)), host(_staged(fr, 0, x, idx, cnt, n, 1)))
     fh.ls_ffn_sync()
 
 

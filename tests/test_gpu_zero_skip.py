@@ -23,7 +23,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, rel_l2  # noqa: E402
+from gpu_util import Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn, y_err  # noqa: E402
 
 C = lsgen.CONFIGS
 
@@ -86,7 +86,7 @@ def test_zero_skip_equals_block_path(name, B):
             for b in range(B):
                 y_ref = oracle.sparse_ffn(ws[l], oracle.mlp_input(xi[b], cfg.prenorm), blocks, cfg.block,
                                           cfg.act, ws[l].threshold)
-                assert rel_l2(y1[b].astype(np.float64) - xi[b], y_ref) <= Y_TOL[cfg.dtype], (name, B, l, b)
+                assert y_err(y1[b].astype(np.float64) - xi[b], y_ref) <= Y_TOL[cfg.dtype], (name, B, l, b)
         x_in = dev_f32(y1)
     assert skipped > 0  # the case exercises the skip
 
@@ -136,7 +136,7 @@ def test_zero_skip_dead_blocks():
             assert np.all(a[pos] == 0.0)
     y_ref = oracle.sparse_ffn(w, oracle.mlp_input(x[0], cfg.prenorm), [0, 3, 7], cfg.block, cfg.act,
                               w.threshold)
-    assert rel_l2(y1[0].astype(np.float64) - x[0], y_ref) <= Y_TOL[cfg.dtype]
+    assert y_err(y1[0].astype(np.float64) - x[0], y_ref) <= Y_TOL[cfg.dtype]
     # every block dead: the output is the input
     all_dead = np.array(dead, np.int32)
     (z0, z1), _ = _both(f, 0, dev_f32(x), 1, dev_f32(all_dead).int(), dev_f32([3]).int(), 0, 3,
@@ -163,7 +163,7 @@ def test_zero_skip_host_resident_blocks():
         assert np.array_equal(y0, y1), l
         y_ref = oracle.sparse_ffn(ws[l], oracle.mlp_input(host(x)[0], cfg.prenorm), host(idx), cfg.block,
                                   cfg.act, ws[l].threshold)
-        assert rel_l2(y1[0].astype(np.float64) - host(x)[0], y_ref) <= Y_TOL[cfg.dtype]
+        assert y_err(y1[0].astype(np.float64) - host(x)[0], y_ref) <= Y_TOL[cfg.dtype]
         x = dev_f32(y1)
     fh.ls_ffn_sync()
 
@@ -204,4 +204,4 @@ def test_zero_skip_full_size_layer(cfg_name):
         blocks = host(idx)[:cfg.k]
         y_ref = oracle.sparse_ffn(ws[0], oracle.mlp_input(x[0], cfg.prenorm), blocks, cfg.block, cfg.act,
                                   ws[0].threshold)
-        assert rel_l2(y1[0].astype(np.float64) - x[0], y_ref) <= Y_TOL[cfg.dtype]
+        assert y_err(y1[0].astype(np.float64) - x[0], y_ref) <= Y_TOL[cfg.dtype]
