@@ -29,7 +29,7 @@ LS_SEL_TOPK, LS_SEL_THRESHOLD = 0, 1
 LS_PREFETCH_NONE, LS_PREFETCH_ONESHOT, LS_PREFETCH_REFINE = 0, 1, 2
 
 EXPORTS = ("ls_ffn_create", "ls_ffn_set_layer", "ls_ffn_destroy", "ls_predict", "ls_select_blocks",
-           "ls_sparse_ffn_step", "ls_stream_weights", "ls_decode_step_streamed", "ls_decode_step",
+           "ls_sparse_ffn_step", "ls_sparse_ffn_step_static", "ls_stream_weights", "ls_decode_step_streamed", "ls_decode_step",
            "ls_set_hash_predictor", "ls_hash_predict",
            "ls_debug_last_activations", "ls_set_kernel_timing", "ls_kernel_timing",
            "ls_configure", "ls_ffn_sync", "ls_debug_decode_trace", "ls_debug_phase_trace",
@@ -108,6 +108,7 @@ def load():
     lib.ls_predict.argtypes = [P, I32, P, I32, P]
     lib.ls_select_blocks.argtypes = [P, P, I32, ctypes.c_int, I32, ctypes.c_float, I32, I32, P, P]
     lib.ls_sparse_ffn_step.argtypes = [P, I32, P, I32, P, P, I32, I32, P]
+    lib.ls_sparse_ffn_step_static.argtypes = [P, I32, P, I32, P, P, I32, I32, P]
     lib.ls_stream_weights.argtypes = [P, I32, P, I32, I32, ctypes.POINTER(LsStreamStats)]
     lib.ls_decode_step.argtypes = [P, P, I32, I32]
     lib.ls_decode_step_streamed.argtypes = [P, P, I32, I32, I32, I32, ctypes.POINTER(LsStreamReport)]
@@ -217,6 +218,12 @@ class Ffn:
         _check(self.lib, self.ctx, self.lib.ls_sparse_ffn_step(self.ctx, layer, _ptr(x_in), B,
                                                                _ptr(idx), _ptr(count), begin, end,
                                                                _ptr(x_acc)))
+
+    def ls_sparse_ffn_step_static(self, layer: int, x_in, B: int, idx, count, begin: int, end: int,
+                                  x_acc) -> None:
+        _check(self.lib, self.ctx, self.lib.ls_sparse_ffn_step_static(self.ctx, layer, _ptr(x_in), B,
+                                                                      _ptr(idx), _ptr(count), begin, end,
+                                                                      _ptr(x_acc)))
 
     def ls_stream_weights(self, layer: int, idx_host, n_stages: int = 1) -> LsStreamStats:
         a = np.ascontiguousarray(idx_host, dtype=np.int32)

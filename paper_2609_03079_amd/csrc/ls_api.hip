@@ -41,6 +41,7 @@ struct ls_ffn {
     float* dn_part = nullptr; // [kDownSplits, maxB, d]  parts of the split down projection
     int64_t last_act_n = 0;
     int32_t last_act_B = 0;
+    const float* last_act_src = nullptr;  // activations buffer of the last sparse step
 
     // staging for set_layer (pinned host)
     uint8_t* staging = nullptr;
@@ -325,6 +326,8 @@ hipError_t dmalloc(T** p, size_t n) {
 
 extern "C" {
 
+static bool resolve_scratch(int device);
+
 ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
     if (!out) return fail(nullptr, LS_E_INVAL, "out is NULL");
     *out = nullptr;
@@ -352,6 +355,10 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             return fail(nullptr, LS_E_DEVICE, "no HIP device");
         }
         c->n_wg = prop.multiProcessorCount;
+        if (!resolve_scratch(c->device)) {
+            delete c;
+            return fail(nullptr, LS_E_DEVICE, "could not resolve the static scratch array on this device");
+        }
         s.G = c->n_wg;
         s.p1_rpw = (s.r + s.G - 1) / s.G;
         s.p2_rpw = (s.n_blk + s.G - 1) / s.G;
@@ -629,9 +636,13 @@ static ls_status wait_stages(ls_ffn* c, int32_t layer, int32_t begin, int32_t en
     return LS_OK;
 }
 
-ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_t B,
-                             const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
-                             float* x_acc) {
+// The sparse step over [begin, end) of the list with the given scratch: a_buf [B, F]
+// activations, part [kDownSplits, B, d] parts of the split down projection.
+// may_time: bracket the launches with timing events when kernel timing is on (taking an
+// event can create one); false launches them bare.
+static ls_status sparse_step(ls_ffn* c, int32_t layer, const float* x_in, int32_t B, const int32_t* idx,
+                             const int32_t* count, int32_t begin, int32_t end, float* x_acc, float* a_buf,
+                             float* part, bool may_time) {
     ls_status st = check_ctx(c);
     if (st != LS_OK) return st;
     const Shape& s = c->shape;
@@ -656,15 +667,73 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
         st = wait_stages(c, layer, begin, end);
         if (st != LS_OK) return st;
     }
-    LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, slot_table, x_in, B, idx, count, begin, end, c->a, c->stream); }));
-    LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, slot_table, c->a, B, idx, count, begin, end, x_in, x_acc, c->dn_part, c->stream); }));
+    auto gateup = [&] { return ls::launch_gateup(s, L, slot_table, x_in, B, idx, count, begin, end, a_buf, c->stream); };
+    auto down = [&] { return ls::launch_down(s, L, slot_table, a_buf, B, idx, count, begin, end, x_in, x_acc, part, c->stream); };
+    LS_HIP(c, may_time ? timed(c, LS_K_GATEUP, gateup) : gateup());
+    LS_HIP(c, may_time ? timed(c, LS_K_DOWN, down) : down());
     if (c->desc.residency == LS_WEIGHTS_HOST) {
         LS_HIP(c, hipEventRecord(c->layer_done[layer], c->stream));
         c->layer_done_recorded[layer] = 1;
     }
     c->last_act_n = (int64_t)end * s.blk;
     c->last_act_B = B;
+    c->last_act_src = a_buf;
     return LS_OK;
+}
+
+ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_t B,
+                             const int32_t* idx, const int32_t* count, int32_t begin, int32_t end,
+                             float* x_acc) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    return sparse_step(c, layer, x_in, B, idx, count, begin, end, x_acc, c->a, c->dn_part, true);
+}
+
+// ---- the sparse step without allocation -------------------------------------------------
+// A fixed device array holds the scratch of ls_sparse_ffn_step_static (activations [B, F],
+// then the split down projection's parts [kDownSplits, B, d]).  Each GPU the library runs on
+// holds its own copy until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is resolved once per device, with that
+// device current, by ls_ffn_create, and only that address is handed to kernels.
+constexpr size_t kScratchFloats = (size_t)LS_STATIC_SCRATCH_BYTES / sizeof(float);
+static __device__ __align__(256) float scratch[kScratchFloats];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static float* g_scratch_ptr[kMaxDevices];
+
+// Resolve the scratch array's address on `device` (the current device) once.
+static bool resolve_scratch(int device) {
+    if (device < 0 || device >= kMaxDevices) return false;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[device]) return true;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+        (void)hipGetLastError();
+        return false;
+    }
+    g_scratch_ptr[device] = static_cast<float*>(ptr);
+    return true;
+}
+
+static float* scratch_ptr(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
+}
+
+ls_status ls_sparse_ffn_step_static(ls_ffn* c, int32_t layer, const float* x_in, int32_t B,
+                                    const int32_t* idx, const int32_t* count, int32_t begin,
+                                    int32_t end, float* x_acc) {
+    ls_status st = check_ctx(c);
+    if (st != LS_OK) return st;
+    const Shape& s = c->shape;
+    if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
+    const size_t need = (size_t)B * s.F + (size_t)ls::kDownSplits * B * s.d;
+    if (need > kScratchFloats)
+        return fail(c, LS_E_CAPACITY, "B * (d_ff + 4 * d_model) floats exceed the static scratch (LS_STATIC_SCRATCH_BYTES)");
+    float* base = scratch_ptr(c->device);
+    if (!base) return fail(c, LS_E_STATE, "static scratch of this device was not resolved");
+    return sparse_step(c, layer, x_in, B, idx, count, begin, end, x_acc, base, base + (size_t)B * s.F, false);
 }
 
 ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t* n_out) {
@@ -674,8 +743,9 @@ ls_status ls_debug_last_activations(ls_ffn* c, float* dst, int64_t cap, int64_t*
     const int64_t n = c->last_act_n;
     *n_out = n;
     if (cap < (int64_t)c->last_act_B * n) return fail(c, LS_E_INVAL, "cap too small");
+    const float* src = c->last_act_src ? c->last_act_src : c->a;
     for (int b = 0; b < c->last_act_B; ++b)
-        LS_HIP(c, hipMemcpyAsync(dst + (size_t)b * n, c->a + (size_t)b * c->shape.F, (size_t)n * sizeof(float),
+        LS_HIP(c, hipMemcpyAsync(dst + (size_t)b * n, src + (size_t)b * c->shape.F, (size_t)n * sizeof(float),
                                  hipMemcpyDeviceToDevice, c->stream));
     return LS_OK;
 }
@@ -887,6 +957,7 @@ static ls_status launch_stage_consumer(ls_ffn* c, int32_t layer, const float* x_
     c->layer_done_recorded[(size_t)layer] = 1;
     c->last_act_n = (int64_t)n * s.blk;
     c->last_act_B = 1;
+    c->last_act_src = c->a;
     return LS_OK;
 }
 
