@@ -254,7 +254,9 @@ def bench_streaming(args, cfg) -> int:
     import lsgen
     import paper_2609_03079_amd as lsffn
 
-    full_blocks = cfg.n_layers * cfg.n_blk
+    # the cache holds the same fraction of the blocks as the full workload's budget does
+    # (16 GiB over all of its layers), whatever the number of layers run
+    full_blocks = lsgen.CONFIGS[cfg.name].n_layers * cfg.n_blk
     L = args.layers or 6
     cfg = cfg.with_(n_layers=L)
     block_bytes = 3 * cfg.block * cfg.d_model * cfg.elem_bytes
@@ -339,7 +341,7 @@ def bench_streaming(args, cfg) -> int:
         "value": round(K / wall, 3), "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": round(1e3 * wall / K, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": lsgen.DTYPE_NAMES[cfg.dtype], "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {L} of 80 layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, "
+        "config": {"workload": f"{cfg.name}: {L} of {lsgen.CONFIGS[cfg.name].n_layers} layers, d_model {cfg.d_model}, d_ff {cfg.d_ff}, "
                                f"block {cfg.block} (k={cfg.k} of {cfg.n_blk}), rank {cfg.rank}, batch 1, "
                                f"host-resident blocks, HBM cache {slots} slots ({100 * cache_frac:.1f}% of "
                                f"the blocks), {S} copy stages per layer, prefetch {args.prefetch} "

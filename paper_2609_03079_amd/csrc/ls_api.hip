@@ -48,7 +48,7 @@ struct ls_ffn {
     size_t staging_bytes = 0;
 
     // host-resident weights (LS_WEIGHTS_HOST)
-    uint8_t* host_blocks = nullptr;  // pinned, [L][n_blk][block_bytes]
+    std::vector<uint8_t*> host_blocks;  // per layer, pinned [n_blk][block_bytes] (one allocation per layer)
     uint8_t* cache = nullptr;        // device, [slots][block_bytes]
     int32_t* slot_tables = nullptr;  // device, [L][n_blk]
     int32_t* slot_tables_host = nullptr;  // pinned mirror
@@ -298,7 +298,8 @@ void free_all(ls_ffn* c) {
                     (void*)c->trace, (void*)c->stage_cnt})
         if (p) (void)hipFree(p);
     if (c->staging) (void)hipHostFree(c->staging);
-    if (c->host_blocks) (void)hipHostFree(c->host_blocks);
+    for (auto p : c->host_blocks) if (p) (void)hipHostFree(p);
+    c->host_blocks.clear();
     if (c->slot_tables_host) (void)hipHostFree(c->slot_tables_host);
     for (auto& v : c->stage_events)
         for (auto e : v) (void)hipEventDestroy(e);
@@ -404,10 +405,18 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             c->dev[l].p2 = c->arena[l] + (lay.p2 - lay.bias);
             c->dev[l].pf = reinterpret_cast<const float*>(c->arena[l] + (lay.pf - lay.bias));
         }
-        const size_t host_bytes = (size_t)L * s.n_blk * c->block_bytes;
-        if (hipHostMalloc(reinterpret_cast<void**>(&c->host_blocks), host_bytes, hipHostMallocDefault) != hipSuccess) {
-            (void)hipGetLastError();
-            return bail(LS_E_NOMEM, "pinned host allocation of the weight arena failed");
+        // one pinned allocation per layer: a single one of the whole stack (e.g. 107.5 GiB for
+        // the 70B shape) is refused by the runtime where per-layer ones are not
+        const size_t layer_host_bytes = (size_t)s.n_blk * c->block_bytes;
+        c->host_blocks.assign(L, nullptr);
+        for (int l = 0; l < L; ++l) {
+            if (hipHostMalloc(reinterpret_cast<void**>(&c->host_blocks[l]), layer_host_bytes, hipHostMallocDefault) !=
+                hipSuccess) {
+                (void)hipGetLastError();
+                c->host_blocks[l] = nullptr;
+                return bail(LS_E_NOMEM, "pinned host allocation of the weight arena failed at layer " + std::to_string(l) +
+                                            " (" + std::to_string(layer_host_bytes >> 20) + " MiB per layer)");
+            }
         }
         if (hipMalloc(reinterpret_cast<void**>(&c->cache), (size_t)slots * c->block_bytes) != hipSuccess) {
             (void)hipGetLastError();
@@ -516,7 +525,7 @@ ls_status ls_ffn_set_layer(ls_ffn* c, int32_t layer, const ls_layer_weights* w) 
         blocks_dst = c->staging;
         off_small = lay.bias;
     } else {
-        blocks_dst = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+        blocks_dst = c->host_blocks[layer];
         off_small = 0;
     }
     convert_blocks(s, static_cast<const uint8_t*>(w->w_gate), static_cast<const uint8_t*>(w->w_up),
@@ -816,7 +825,7 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
     }
     ranges.clear();
     size_t fi = 0;
-    const uint8_t* layer_host = c->host_blocks + (size_t)layer * s.n_blk * c->block_bytes;
+    const uint8_t* layer_host = c->host_blocks[layer];
     int written = 0;
     for (int sidx = 0; sidx < n_stages; ++sidx) {
         const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);

@@ -262,3 +262,16 @@ def test_streamed_step_errors():
         fh.ls_decode_step_streamed(x, CFG.k, 1, lsffn.LS_PREFETCH_ONESHOT, SLOTS - CFG.k + 1)
     assert e.value.status == lsffn.LS_E_CAPACITY
     fh.ls_ffn_sync()
+
+
+def test_oversized_cache_budget_is_reported_as_out_of_memory():
+    """An HBM cache budget the device cannot hold fails context creation with LS_E_NOMEM and a
+    message, instead of aborting; a sensible budget on the same shape still works."""
+    with pytest.raises(lsffn.LsError) as e:
+        lsffn.Ffn(n_layers=1, d_model=CFG.d_model, d_ff=CFG.d_ff, block=CFG.block, rank=CFG.rank,
+                  dtype=CFG.dtype, residency=lsffn.LS_WEIGHTS_HOST, hbm_cache_bytes=1 << 50)
+    assert e.value.status == lsffn.LS_E_NOMEM
+    assert "cache" in str(e.value)
+    f = lsffn.Ffn(n_layers=1, d_model=CFG.d_model, d_ff=CFG.d_ff, block=CFG.block, rank=CFG.rank,
+                  dtype=CFG.dtype, residency=lsffn.LS_WEIGHTS_HOST, hbm_cache_bytes=4 * BLOCK_BYTES)
+    f.close()

@@ -184,3 +184,35 @@ def test_zero_skip_byte_counts():
     neg_zero[0, 7] = -0.0  # a signed zero is no activation
     assert bench.zero_skip_bytes(cfg, neg_zero, U)[2] == U * blk * row
     assert bench.zero_skip_bytes(cfg, z[:, :0], 0) == (0, 0, 0)
+
+
+# ---- sanitizer builds of the host code (CPU only) ----
+
+NATIVE = os.path.join(ROOT, "tests", "native")
+
+
+def _build_and_run(tmp_path, cmd_build, exe):
+    r = subprocess.run(cmd_build, capture_output=True, text=True)
+    if r.returncode != 0:
+        pytest.skip(f"sanitizer build not available here: {r.stderr[-300:]}")
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+
+
+def test_block_cache_under_address_and_undefined_behaviour_sanitizers(tmp_path):
+    """The host-resident block cache under random request sequences, built with
+    AddressSanitizer and UndefinedBehaviorSanitizer: its invariants hold and no memory or UB
+    error is reported."""
+    exe = str(tmp_path / "cache_fuzz")
+    _build_and_run(tmp_path, ["g++", "-O1", "-g", "-std=c++17", "-fsanitize=address,undefined",
+                              "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-o", exe,
+                              os.path.join(NATIVE, "cache_fuzz.cpp")], exe)
+
+
+def test_threaded_oracle_under_thread_sanitizer(tmp_path):
+    """The oracle's thread-split layer step (used to time it on every host core), built with
+    ThreadSanitizer: no data race is reported and it equals the single-thread step bitwise."""
+    exe = str(tmp_path / "oracle_mt_race")
+    _build_and_run(tmp_path, ["gcc", "-O1", "-g", "-std=c11", "-fsanitize=thread", "-o", exe,
+                              os.path.join(ROOT, "oracle", "ls_oracle.c"),
+                              os.path.join(NATIVE, "oracle_mt_race.c"), "-lm", "-lpthread"], exe)
