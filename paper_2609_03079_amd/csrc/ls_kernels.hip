@@ -24,14 +24,14 @@ namespace {
 // One workgroup of NW waves per R rows; the waves split the rows' 16-byte chunks, then a
 // fixed-order sum of the wave totals.  The R rows share the input reads (with B tokens the
 // input is B times the bytes of a row); every row's dot product is summed in the same order
-// for any R.
-template <ls_dtype T, int B, bool RMS, int R, int NW>
+// for any R.  U: 16-byte loads in flight per lane and row; a lane sums its chunks in ascending
+// order whatever U is.
+template <ls_dtype T, int B, bool RMS, int R, int NW, int U>
 __global__ __launch_bounds__(64 * NW) void gemv_rows_kernel(const uint8_t* __restrict__ W, int rows,
                                                         int cols, int G, int rpw,
                                                         const float* __restrict__ v,
                                                         float* __restrict__ out) {
     constexpr int V = Wt<T>::V;
-    constexpr int U = 4;  // 16-byte loads in flight per lane and row
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int row0 = blockIdx.x * R;
     const int nchunk = cols / V;
@@ -263,7 +263,10 @@ __global__ __launch_bounds__(Q > 8 ? 512 : 1024) void select_kernel(const float*
 }
 
 // ---- gate/up gather + gating: one wave per neuron of list entries [begin, end) ------------
-template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS>
+// HS: the B x d input is first copied to LDS (dynamic shared memory of B d floats), once per
+// workgroup instead of once per wave from L2; the copy starts once the first row loads are in
+// flight.  The sums are the same either way.
+template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS, int U, bool HS>
 __global__ __launch_bounds__(256) void gateup_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
@@ -272,22 +275,68 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int e = begin + (int)(t / blk);
     const int q = (int)(t % blk);
-    if (e >= list_end(count, end, n_blk)) return;
-    gateup_neuron<T, A, B, RMS, ZS>(blocks, block_bytes, slot_table, bias, thresh, h, d, blk, n_blk, F, idx[e], e,
-                                    q, a_buf, threadIdx.x & 63);
+    const int lane = threadIdx.x & 63;
+    if constexpr (HS) {
+        extern __shared__ f32x4 hs[];
+        auto prep = [&] {
+            const f32x4* src = reinterpret_cast<const f32x4*>(h);
+            for (int i = threadIdx.x; i < B * d / 4; i += 256) hs[i] = src[i];
+            // a barrier that orders LDS only: the row loads already issued stay in flight
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        };
+        if (e >= list_end(count, end, n_blk)) {  // a wave past the list still joins the barrier
+            prep();
+            return;
+        }
+        gateup_neuron<T, A, B, RMS, ZS, false, U>(blocks, block_bytes, slot_table, bias, thresh,
+                                                  reinterpret_cast<const float*>(hs), d, blk, n_blk, F, idx[e], e, q,
+                                                  a_buf, lane, prep);
+    } else {
+        if (e >= list_end(count, end, n_blk)) return;
+        gateup_neuron<T, A, B, RMS, ZS, false, U>(blocks, block_bytes, slot_table, bias, thresh, h, d, blk, n_blk, F,
+                                                  idx[e], e, q, a_buf, lane);
+    }
 }
 
 // ---- down projection + residual: one workgroup per 16-column tile ------------------------
-template <ls_dtype T, int B, bool ZS>
+// G: (entry, chunk pair) items whose loads each wave issues together.
+// AS: the range's activations (B (end - begin) blk floats, at most kDownActs) are first copied
+// to LDS, so the products read them there instead of from L2; the copy starts once the first
+// weight loads are in flight.  The sums are the same either way.
+constexpr int kDownActs = 12288;
+
+template <ls_dtype T, int B, bool ZS, int G, bool AS>
 __global__ __launch_bounds__(256) void down_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
     const float* __restrict__ x_in, float* __restrict__ x_acc) {
     __shared__ float part[4][kMaxBatch][kColTile];
-    down_tile<T, B, ZS, false>(blocks, block_bytes, slot_table, a_buf, F, d, blk, n_blk, idx, begin,
-                               list_end(count, end, n_blk), x_in, x_acc, blockIdx.x, threadIdx.x >> 6,
-                               threadIdx.x & 63, true, part, [] { __syncthreads(); });
+    const int n_end = list_end(count, end, n_blk);
+    auto sync = [] { __syncthreads(); };
+    if constexpr (AS) {
+        __shared__ f32x4 acts[kDownActs / 4];
+        const int n4 = (n_end > begin ? n_end - begin : 0) * blk / 4;  // vectors per token
+        auto prep = [&] {
+            const f32x4* src = reinterpret_cast<const f32x4*>(a_buf + (size_t)begin * blk);
+            for (int i = threadIdx.x; i < B * n4; i += 256) {
+                const int tok = i / n4, j = i - tok * n4;
+                acts[i] = src[(size_t)tok * (F / 4) + j];
+            }
+            // a barrier that orders LDS only: the weight loads already issued stay in flight
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        };
+        down_tile<T, B, ZS, false, G>(blocks, block_bytes, slot_table, reinterpret_cast<const float*>(acts), 4 * n4,
+                                      d, blk, n_blk, idx, begin, n_end, x_in, x_acc, blockIdx.x, threadIdx.x >> 6,
+                                      threadIdx.x & 63, true, part, sync, begin, prep);
+    } else {
+        down_tile<T, B, ZS, false, G>(blocks, block_bytes, slot_table, a_buf, F, d, blk, n_blk, idx, begin, n_end,
+                                      x_in, x_acc, blockIdx.x, threadIdx.x >> 6, threadIdx.x & 63, true, part, sync);
+    }
 }
 
 }  // namespace
@@ -300,11 +349,14 @@ static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, cons
     const int R = B >= 4 ? 4 : 1, NW = B >= 4 ? 8 : 4;
     const dim3 grid((unsigned)((rows + R - 1) / R)), blk(64 * NW);
     const uint8_t* w = static_cast<const uint8_t*>(W);
-#define LS_GEMV(NB, NR, NWV) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR, NWV>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
+    // one row per workgroup below B = 4: a row longer than 4 loads per lane is read in one round
+    const bool wide = cols / Wt<T>::V > 64 * NW * 4;
+#define LS_GEMV_U(NB, NR, NWV, U) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR, NWV, U>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
+#define LS_GEMV(NB, NR, NWV) LS_GEMV_U(NB, NR, NWV, 4)
     switch (B) {
-        case 1: LS_GEMV(1, 1, 4); break;
-        case 2: LS_GEMV(2, 1, 4); break;
-        case 3: LS_GEMV(3, 1, 4); break;
+        case 1: if (wide) LS_GEMV_U(1, 1, 4, 8); else LS_GEMV(1, 1, 4); break;
+        case 2: if (wide) LS_GEMV_U(2, 1, 4, 8); else LS_GEMV(2, 1, 4); break;
+        case 3: if (wide) LS_GEMV_U(3, 1, 4, 8); else LS_GEMV(3, 1, 4); break;
         case 4: LS_GEMV(4, 4, 8); break;
         case 5: LS_GEMV(5, 4, 8); break;
         case 6: LS_GEMV(6, 4, 8); break;
@@ -313,6 +365,7 @@ static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, cons
         default: return hipErrorInvalidValue;
     }
 #undef LS_GEMV
+#undef LS_GEMV_U
     return hipGetLastError();
 }
 
@@ -401,9 +454,29 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
     if (tasks <= 0) return hipSuccess;
     const dim3 grid((unsigned)((tasks + 3) / 4)), blk(256);
     const size_t bb = s.block_elems * elem_size(s.dtype);
-#define LS_GU_K(NB, RMS, ZS)                                                                       \
-    hipLaunchKernelGGL((gateup_kernel<T, A, NB, RMS, ZS>), grid, blk, 0, st, L.blocks, bb, slot_table, \
-                       L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, a_buf)
+    // the input goes through LDS while it takes at most 32 KB (five or more workgroups per CU)
+    const size_t hs_bytes = (size_t)B * s.d * sizeof(float);
+    const bool hs = hs_bytes <= 32768;
+#define LS_GU_KU(NB, RMS, ZS, U)                                                                          \
+    do {                                                                                                  \
+        if (hs)                                                                                           \
+            hipLaunchKernelGGL((gateup_kernel<T, A, NB, RMS, ZS, U, true>), grid, blk, hs_bytes, st, L.blocks, bb, \
+                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, \
+                               a_buf);                                                                    \
+        else                                                                                              \
+            hipLaunchKernelGGL((gateup_kernel<T, A, NB, RMS, ZS, U, false>), grid, blk, 0, st, L.blocks, bb, \
+                               slot_table, L.bias, L.threshold, h, s.d, s.blk, s.n_blk, s.F, idx, count, begin, end, \
+                               a_buf);                                                                    \
+    } while (0)
+    // at batch 1 a wave issues every load of its two rows at once (up to 16 chunks per lane)
+    const int per_lane = (s.d / Wt<T>::V + 63) / 64;
+#define LS_GU_K(NB, RMS, ZS)                                                  \
+    do {                                                                      \
+        if (NB > 1 || ZS || per_lane <= 4) LS_GU_KU(NB, RMS, ZS, 4);          \
+        else if (per_lane <= 8) LS_GU_KU(NB, RMS, ZS, (NB > 1 || ZS ? 4 : 8));  \
+        else if (per_lane <= 12) LS_GU_KU(NB, RMS, ZS, (NB > 1 || ZS ? 4 : 12)); \
+        else LS_GU_KU(NB, RMS, ZS, (NB > 1 || ZS ? 4 : 16));                   \
+    } while (0)
 #define LS_GU(NB)                                                                 \
     do {                                                                          \
         if (s.prenorm) {                                                          \
@@ -425,6 +498,7 @@ static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slo
     }
 #undef LS_GU
 #undef LS_GU_K
+#undef LS_GU_KU
     return hipGetLastError();
 }
 
@@ -448,20 +522,28 @@ hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_
     return hipErrorInvalidValue;
 }
 
+// A workgroup owns one tile and the whole list range, so each wave issues the loads of up to
+// 16 items (32 vectors of 16 bytes per lane) at once: at batch 1 the kernel is bound by how
+// many loads a compute unit keeps in flight, not by arithmetic.
+constexpr int kDownItems = 16;
+
 template <ls_dtype T>
 static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
     const dim3 grid(s.d / kColTile), blk(256);
     const size_t bb = s.block_elems * elem_size(s.dtype);
+    const bool as = (long)B * (end - begin) * s.blk <= kDownActs && s.F % 4 == 0;
+#define LS_DN_K(NB, ZS, AS)                                                                          \
+    hipLaunchKernelGGL((down_kernel<T, NB, ZS, kDownItems, AS>), grid, blk, 0, st, L.blocks, bb, slot_table, \
+                       a_buf, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc)
 #define LS_DN(NB)                                                                                   \
     do {                                                                                            \
-        if (s.zero_skip)                                                                            \
-            hipLaunchKernelGGL((down_kernel<T, NB, true>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
-                               s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);      \
-        else                                                                                        \
-            hipLaunchKernelGGL((down_kernel<T, NB, false>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, \
-                               s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);      \
+        if (s.zero_skip) {                                                                          \
+            if (as) LS_DN_K(NB, true, true); else LS_DN_K(NB, true, false);                         \
+        } else {                                                                                    \
+            if (as) LS_DN_K(NB, false, true); else LS_DN_K(NB, false, false);                       \
+        }                                                                                           \
     } while (0)
     switch (B) {
         case 1: LS_DN(1); break;
@@ -475,6 +557,7 @@ static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_
         default: return hipErrorInvalidValue;
     }
 #undef LS_DN
+#undef LS_DN_K
     return hipGetLastError();
 }
 

@@ -29,6 +29,12 @@ __device__ __forceinline__ f32x4 act_load4(const float* p) {
     return r;
 }
 
+// A hook run once per wave by the bodies below before their first read of staged data
+// (the callers that stage it in LDS pass a copy and a barrier); by default nothing.
+struct NoPrep {
+    __device__ void operator()() const {}
+};
+
 // ---- gate/up gather + gating (one wave per neuron) --------------------------------------------------------------
 __device__ inline int list_end(const int32_t* count, int end, int n_blk) {
     int c = *count;
@@ -95,20 +101,25 @@ __device__ __forceinline__ float gate_out(float g, float thresh) {
 // output of some token is nonzero; a neuron whose gate output is zero for every token then
 // costs its gate row alone.  The activations equal those of the one-pass form (same
 // accumulation order; a skipped product is an exact zero).
-template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS, bool COH = false>
+// U: 16-byte chunks per row and lane whose loads are issued together.  Each lane sums its
+// chunks lane, lane + 64, ... in ascending order whatever U is, so U does not change results.
+// prep() runs once before h is first read: after the first U chunks' loads are issued (at the
+// start with ZS, and before returning for an entry that reads nothing).
+template <ls_dtype T, ls_act A, int B, bool RMS, bool ZS, bool COH = false, int U = 4, typename Prep = NoPrep>
 __device__ __forceinline__ void gateup_neuron(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int d, int blk,
-    int n_blk, int F, int b, int e, int q, float* __restrict__ a_buf, int lane) {
+    int n_blk, int F, int b, int e, int q, float* __restrict__ a_buf, int lane, Prep prep = Prep{}) {
     constexpr int V = Wt<T>::V;
-    constexpr int U = 4;
     const size_t apos = (size_t)e * blk + q;
     if (b < 0 || b >= n_blk) {  // invalid id: the entry contributes nothing
+        prep();
         if (lane < B) act_store<COH>(a_buf + (size_t)lane * F + apos, 0.f);
         return;
     }
     const int slot = slot_table ? slot_table[b] : b;
     if (slot < 0) {  // block not in the cache: contributes nothing
+        prep();
         if (lane < B) act_store<COH>(a_buf + (size_t)lane * F + apos, 0.f);
         return;
     }
@@ -122,6 +133,7 @@ __device__ __forceinline__ void gateup_neuron(
     for (int i = 0; i < B; ++i) ag[i] = au[i] = ss[i] = 0.f;
     const float bj = bias ? Wt<T>::scalar(bias, (size_t)b * blk + q) : 0.f;
     if (ZS) {
+        prep();
         row_dot<T, B, RMS>(grow, h, d, lane, ag, ss);
         bool any = false;
 #pragma unroll
@@ -142,7 +154,11 @@ __device__ __forceinline__ void gateup_neuron(
         }
         return;
     }
-    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+    // rounds of U chunks per lane (r0 is the same in every lane, so prep() is reached by the
+    // whole wave); lane L takes chunks L, L + 64, ... in ascending order
+    if (nchunk <= 0) prep();
+    for (int r0 = 0; r0 < nchunk; r0 += 64 * U) {
+        const int c0 = r0 + lane;
         u32x4 rg[U], ru[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -151,6 +167,7 @@ __device__ __forceinline__ void gateup_neuron(
             rg[u] = ok ? ld_stream(grow + c) : u32x4{0u, 0u, 0u, 0u};
             ru[u] = ok ? ld_stream(urow + c) : u32x4{0u, 0u, 0u, 0u};
         }
+        if (r0 == 0) prep();
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 64;
@@ -205,94 +222,111 @@ __device__ __forceinline__ void gateup_neuron(
 // The activation of neuron j of entry e is a_buf[i F + (e - a_off) blk + j].
 // sync() is the barrier of the waves that share `part` (the workgroup's, or the group's);
 // a group with active == false only takes part in it.
+// Wave w takes the entries begin + w + 4j.  Its work is a sequence of items (entry j, chunk
+// pair p: chunks lane + 64 (2p + r), r = 0, 1 of the entry's piece) in entry-major order; the
+// loads of G items are issued together and the products are summed item by item, so the
+// result is the same for every G (G only sets how many loads are in flight).
 // ZS (row-level zero skip): a lane's 16-byte vector holds V neurons of one column; it is read
 // only when one of those neurons has a nonzero activation for some token.  The sums equal
 // those of the full read (a skipped product is an exact zero).
-template <ls_dtype T, int B, bool ZS, bool COH, typename Sync>
+// prep() runs once in every wave before the first activation is read: after the first
+// items' weight loads are issued (before anything, with ZS).  It may hold a barrier of the
+// four waves (a caller that stages the activations in LDS).
+template <ls_dtype T, int B, bool ZS, bool COH, int G, typename Sync, typename Prep = NoPrep>
 __device__ __forceinline__ void down_tile(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, int begin, int n_end,
     const float* __restrict__ x_in, float* __restrict__ x_acc, int tile, int wave, int lane, bool active,
-    float (&part)[4][kMaxBatch][kColTile], Sync sync, int a_off = 0) {
+    float (&part)[4][kMaxBatch][kColTile], Sync sync, int a_off = 0, Prep prep = Prep{}) {
     constexpr int V = Wt<T>::V;
-    constexpr int EU = 4;  // list entries in flight per wave
     if (!active) n_end = begin;
     const int nchunk = blk * Wt<T>::kBytes;  // 16-byte chunks of one (block, tile) piece
-    const int per_lane = (nchunk + 63) / 64;
+    const int npair = (nchunk + 127) / 128;  // chunk pairs per lane and entry
+    const int n_mine = n_end > begin + wave ? (n_end - begin - wave + 3) / 4 : 0;
+    const int n_items = n_mine * npair;
     const size_t down_off = (size_t)2 * blk * d * Wt<T>::kBytes +
                             (size_t)tile * blk * kColTile * Wt<T>::kBytes;
     float acc[B];
 #pragma unroll
     for (int i = 0; i < B; ++i) acc[i] = 0.f;
-    for (int e0 = begin + wave; e0 < n_end; e0 += 4 * EU) {
-        const u32x4* src[EU];
-        int ent[EU];
+    bool prepped = false;
+    if (ZS) {
+        prep();
+        prepped = true;
+    }
+    for (int it0 = 0; it0 < n_items; it0 += G) {
+        const u32x4* src[G];
+        int ent[G], c0[G];
 #pragma unroll
-        for (int u = 0; u < EU; ++u) {
-            const int e = e0 + 4 * u;
-            int b = e < n_end ? idx[e] : -1;
+        for (int u = 0; u < G; ++u) {
+            const int it = it0 + u;
+            const int j = it / npair, pr = it - j * npair;
+            const int e = begin + wave + 4 * j;
+            int b = it < n_items ? idx[e] : -1;
             if (b >= n_blk) b = -1;
-            int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
+            const int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
             ent[u] = slot < 0 ? -1 : e;
+            c0[u] = lane + 128 * pr;
             src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
                                                     down_off);
         }
-        for (int i0 = 0; i0 < per_lane; i0 += 2) {
-            bool use[EU][2];
+        bool use[G][2];
 #pragma unroll
-            for (int u = 0; u < EU; ++u)
+        for (int u = 0; u < G; ++u)
 #pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    use[u][r] = ent[u] >= 0 && c < nchunk;
-                    if (ZS && use[u][r]) {
-                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)(c / kColTile) * V;
-                        bool nz = false;
+            for (int r = 0; r < 2; ++r) {
+                const int c = c0[u] + 64 * r;
+                use[u][r] = ent[u] >= 0 && c < nchunk;
+                if (ZS && use[u][r]) {
+                    const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)(c / kColTile) * V;
+                    bool nz = false;
 #pragma unroll
-                        for (int i = 0; i < B; ++i) {
+                    for (int i = 0; i < B; ++i) {
 #pragma unroll
-                            for (int qq = 0; qq < V / 4; ++qq) {
-                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
-                                nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
-                            }
-                        }
-                        use[u][r] = nz;
-                    }
-                }
-            u32x4 raw[EU][2];
-#pragma unroll
-            for (int u = 0; u < EU; ++u)
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    raw[u][r] = use[u][r] ? ld_stream(src[u] + c) : u32x4{0u, 0u, 0u, 0u};
-                }
-#pragma unroll
-            for (int u = 0; u < EU; ++u)
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const int c = lane + 64 * (i0 + r);
-                    if (use[u][r]) {
-                        float w[V];
-                        Wt<T>::widen(raw[u][r], w);
-                        const int grp = c / kColTile;  // this lane's V neurons
-                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)grp * V;
-#pragma unroll
-                        for (int i = 0; i < B; ++i) {
-#pragma unroll
-                            for (int qq = 0; qq < V / 4; ++qq) {
-                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
-                                acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
-                                acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
-                                acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
-                                acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
-                            }
+                        for (int qq = 0; qq < V / 4; ++qq) {
+                            const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                            nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
                         }
                     }
+                    use[u][r] = nz;
                 }
+            }
+        u32x4 raw[G][2];
+#pragma unroll
+        for (int u = 0; u < G; ++u)
+#pragma unroll
+            for (int r = 0; r < 2; ++r)
+                raw[u][r] = use[u][r] ? ld_stream(src[u] + c0[u] + 64 * r) : u32x4{0u, 0u, 0u, 0u};
+        if (!prepped) {
+            prep();
+            prepped = true;
         }
+#pragma unroll
+        for (int u = 0; u < G; ++u)
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int c = c0[u] + 64 * r;
+                if (use[u][r]) {
+                    float w[V];
+                    Wt<T>::widen(raw[u][r], w);
+                    const int grp = c / kColTile;  // this lane's V neurons
+                    const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)grp * V;
+#pragma unroll
+                    for (int i = 0; i < B; ++i) {
+#pragma unroll
+                        for (int qq = 0; qq < V / 4; ++qq) {
+                            const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                            acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
+                            acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
+                            acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
+                            acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
+                        }
+                    }
+                }
+            }
     }
+    if (!prepped) prep();
     // lanes l, l+16, l+32, l+48 hold the same column
 #pragma unroll
     for (int i = 0; i < B; ++i) {
