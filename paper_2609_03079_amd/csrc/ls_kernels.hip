@@ -12,6 +12,8 @@
 //             selected blocks, so no partial sums leave the workgroup.
 //
 // Every reduction has a fixed order: results are bitwise reproducible.
+#include <atomic>
+
 #include "ls_device.h"
 #include "ls_internal.h"
 #include "ls_sparse.h"
@@ -300,20 +302,23 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     }
 }
 
-// ---- down projection + residual: one workgroup per 16-column tile ------------------------
+// ---- down projection + residual: one workgroup of kDnWaves waves per 16-column tile ------
 // G: (entry, chunk pair) items whose loads each wave issues together.
 // AS: the range's activations (B (end - begin) blk floats, at most kDownActs) are first copied
 // to LDS, so the products read them there instead of from L2; the copy starts once the first
 // weight loads are in flight.  The sums are the same either way.
 constexpr int kDownActs = 12288;
+constexpr int kDnWaves = 16;  // a compute unit needs about 16 waves of scattered reads to stream
 
-template <ls_dtype T, int B, bool ZS, int G, bool AS>
-__global__ __launch_bounds__(256) void down_kernel(
+// OCC: workgroups that must fit in a compute unit together (2: at most 64 registers a lane),
+// for a tile count above the CU count, so that the extra tiles run beside the others.
+template <ls_dtype T, int B, bool ZS, int G, bool AS, int OCC>
+__global__ __launch_bounds__(64 * kDnWaves) __attribute__((amdgpu_waves_per_eu(OCC * kDnWaves / 4))) void down_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin, int end,
     const float* __restrict__ x_in, float* __restrict__ x_acc) {
-    __shared__ float part[4][kMaxBatch][kColTile];
+    __shared__ float part[kDnVirt][kMaxBatch][kColTile];
     const int n_end = list_end(count, end, n_blk);
     auto sync = [] { __syncthreads(); };
     if constexpr (AS) {
@@ -321,7 +326,7 @@ __global__ __launch_bounds__(256) void down_kernel(
         const int n4 = (n_end > begin ? n_end - begin : 0) * blk / 4;  // vectors per token
         auto prep = [&] {
             const f32x4* src = reinterpret_cast<const f32x4*>(a_buf + (size_t)begin * blk);
-            for (int i = threadIdx.x; i < B * n4; i += 256) {
+            for (int i = threadIdx.x; i < B * n4; i += 64 * kDnWaves) {
                 const int tok = i / n4, j = i - tok * n4;
                 acts[i] = src[(size_t)tok * (F / 4) + j];
             }
@@ -330,12 +335,13 @@ __global__ __launch_bounds__(256) void down_kernel(
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
         };
-        down_tile<T, B, ZS, false, G>(blocks, block_bytes, slot_table, reinterpret_cast<const float*>(acts), 4 * n4,
-                                      d, blk, n_blk, idx, begin, n_end, x_in, x_acc, blockIdx.x, threadIdx.x >> 6,
-                                      threadIdx.x & 63, true, part, sync, begin, prep);
+        down_tile<T, B, ZS, false, G, kDnWaves>(blocks, block_bytes, slot_table, reinterpret_cast<const float*>(acts),
+                                                4 * n4, d, blk, n_blk, idx, begin, n_end, x_in, x_acc, blockIdx.x,
+                                                threadIdx.x >> 6, threadIdx.x & 63, true, part, sync, begin, prep);
     } else {
-        down_tile<T, B, ZS, false, G>(blocks, block_bytes, slot_table, a_buf, F, d, blk, n_blk, idx, begin, n_end,
-                                      x_in, x_acc, blockIdx.x, threadIdx.x >> 6, threadIdx.x & 63, true, part, sync);
+        down_tile<T, B, ZS, false, G, kDnWaves>(blocks, block_bytes, slot_table, a_buf, F, d, blk, n_blk, idx, begin,
+                                                n_end, x_in, x_acc, blockIdx.x, threadIdx.x >> 6, threadIdx.x & 63,
+                                                true, part, sync);
     }
 }
 
@@ -446,6 +452,17 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
     return hipGetLastError();
 }
 
+// compute units of the current device (0 when unknown), queried once per device
+static int cu_count() {
+    static std::atomic<int> cached[64];
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (dev >= 0 && dev < 64 && (cus = cached[dev].load(std::memory_order_relaxed)) > 0) return cus;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) return 0;
+    if (dev >= 0 && dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
 template <ls_dtype T, ls_act A>
 static hipError_t gateup_t(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                            const float* h, int B, const int32_t* idx, const int32_t* count,
@@ -522,21 +539,37 @@ hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_
     return hipErrorInvalidValue;
 }
 
-// A workgroup owns one tile and the whole list range, so each wave issues the loads of up to
-// 16 items (32 vectors of 16 bytes per lane) at once: at batch 1 the kernel is bound by how
-// many loads a compute unit keeps in flight, not by arithmetic.
-constexpr int kDownItems = 16;
+// Loads of up to 8 items (16 vectors of 16 bytes per lane) in flight per wave; 4 where the
+// per-token sums (B >= 4) or the zero-skip tests (B >= 2) take the registers.
+constexpr int down_items(int B, bool ZS) { return B == 1 || (!ZS && B <= 3) ? 8 : 4; }
+
+template <ls_dtype T, int NB, bool ZS, bool AS>
+static void down_launch(const Shape& s, const LayerDev& L, const int32_t* slot_table, const float* a_buf,
+                        const int32_t* idx, const int32_t* count, int begin, int end, const float* x_in,
+                        float* x_acc, bool two, hipStream_t st) {
+    const dim3 grid(s.d / kColTile), blk(64 * kDnWaves);
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+    if constexpr (NB == 1 && !ZS) {
+        if (two) {
+            hipLaunchKernelGGL((down_kernel<T, NB, ZS, 2, AS, 2>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
+                               s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((down_kernel<T, NB, ZS, down_items(NB, ZS), AS, 1>), grid, blk, 0, st, L.blocks, bb,
+                       slot_table, a_buf, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc);
+}
 
 template <ls_dtype T>
 static hipError_t down_t(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, const float* x_in, float* x_acc, hipStream_t st) {
-    const dim3 grid(s.d / kColTile), blk(256);
-    const size_t bb = s.block_elems * elem_size(s.dtype);
     const bool as = (long)B * (end - begin) * s.blk <= kDownActs && s.F % 4 == 0;
-#define LS_DN_K(NB, ZS, AS)                                                                          \
-    hipLaunchKernelGGL((down_kernel<T, NB, ZS, kDownItems, AS>), grid, blk, 0, st, L.blocks, bb, slot_table, \
-                       a_buf, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc)
+    // more tiles than CUs (d = 5120: 320 tiles): at batch 1, two workgroups per CU with 2 items
+    // of loads in flight per wave instead of one with 8, so the extra tiles run beside the others
+    const bool two = B == 1 && !s.zero_skip && s.d / kColTile > cu_count();
+#define LS_DN_K(NB, ZS, AS) \
+    down_launch<T, NB, ZS, AS>(s, L, slot_table, a_buf, idx, count, begin, end, x_in, x_acc, two, st)
 #define LS_DN(NB)                                                                                   \
     do {                                                                                            \
         if (s.zero_skip) {                                                                          \

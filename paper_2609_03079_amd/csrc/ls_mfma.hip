@@ -81,7 +81,8 @@ __device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
     return end < c ? end : c;
 }
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;     // gate/up: waves per workgroup
+constexpr int kRowsW = 32 / kWaves;  // gate/up: staged rows loaded by each wave per chunk
 constexpr int kUnroll = 8;    // gate/up: K steps in flight per wave
 constexpr int kUnrollDn = 4;  // down: (entry, K step) items in flight per wave
 constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
@@ -98,8 +99,9 @@ constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
 constexpr int kChunkK = 512;                 // K values per chunk (1 KB of a 16-bit row)
 constexpr int kRowPitch = 2 * kChunkK + 16;  // LDS bytes per staged row
 // three waves per SIMD (at most 168 registers a lane): three workgroups per CU
+constexpr int kGuWavesPerEu = 3;
 template <ls_dtype T, ls_act A, bool RMS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void gateup_mfma_kernel(
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGuWavesPerEu))) void gateup_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const void* __restrict__ bias, float thresh, const float* __restrict__ h, int B, int d, int blk,
     int n_blk, int F, const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int begin,
@@ -125,15 +127,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
     const float* hrow = h + (size_t)(tok_ok ? tok : 0) * d;
-    // staged row j of this wave's 8 loads: gate row r0 + j (j < 16) or up row r0 + j - 16
+    // staged row j of this wave's loads: gate row r0 + j (j < 16) or up row r0 + j - 16
     auto row_ptr = [&](int j) {
         return base + (size_t)(j < 16 ? r0 + j : blk + r0 + j - 16) * row_bytes;
     };
-    auto load_chunk = [&](int c0, u32x4 (&rw)[8]) {
+    auto load_chunk = [&](int c0, u32x4 (&rw)[kRowsW]) {
         const int bytes = 2 * min(kChunkK, d - c0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int j = wave + 4 * i;
+        for (int i = 0; i < kRowsW; ++i) {
+            const int j = wave + kWaves * i;
             rw[i] = lane * 16 < bytes ? ld_stream(reinterpret_cast<const u32x4*>(row_ptr(j) + (size_t)c0 * 2 + lane * 16))
                                       : u32x4{0u, 0u, 0u, 0u};
         }
@@ -156,7 +158,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
     };
     f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
-    u32x4 rw[8];
+    u32x4 rw[kRowsW];
     f32x4 hx[kStepsW][2];
     load_chunk(0, rw);
     load_x(0, hx);
@@ -166,8 +168,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
 #pragma unroll
         for (int j = 0; j < kStepsW; ++j) hc[j][0] = hx[j][0], hc[j][1] = hx[j][1];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-            *reinterpret_cast<u32x4*>(stage + (wave + 4 * i) * kRowPitch + lane * 16) = rw[i];
+        for (int i = 0; i < kRowsW; ++i)
+            *reinterpret_cast<u32x4*>(stage + (wave + kWaves * i) * kRowPitch + lane * 16) = rw[i];
         __syncthreads();
         if (c0 + kChunkK < d) {  // in flight while this chunk runs
             load_chunk(c0 + kChunkK, rw);
@@ -216,10 +218,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
     __syncthreads();
     if (threadIdx.x < 16 * B) {
         const int t = threadIdx.x / 16, r = threadIdx.x % 16;
-        const float sc = RMS ? rms_scale(((pss[0][t] + pss[1][t]) + pss[2][t]) + pss[3][t], d) : 1.f;
-        const float g = sc * (((pg[0][r][t] + pg[1][r][t]) + pg[2][r][t]) + pg[3][r][t]) +
+        float sq = 0.f, gs = 0.f, us = 0.f;  // the waves' partial sums in wave order
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            sq += pss[w][t];
+            gs += pg[w][r][t];
+            us += pu[w][r][t];
+        }
+        const float sc = RMS ? rms_scale(sq, d) : 1.f;
+        const float g = sc * gs +
                         (bias ? Wt<T>::scalar(bias, (size_t)b * blk + r0 + r) : 0.f);
-        const float u = sc * (((pu[0][r][t] + pu[1][r][t]) + pu[2][r][t]) + pu[3][r][t]);
+        const float u = sc * us;
         float a;
         if (A == LS_ACT_REGLU) {
             a = fmaxf(g, 0.f) * u;
@@ -344,7 +353,7 @@ hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* 
     const long groups = (long)(end - begin) * (s.blk / 16);
     if (groups <= 0) return hipSuccess;
     const size_t bb = s.block_elems * elem_size(s.dtype);
-    const dim3 grid((unsigned)groups), blk(256);
+    const dim3 grid((unsigned)groups), blk(64 * kWaves);
     const bool relu = s.act == LS_ACT_REGLU;
 #define LS_GUM(TT, AA)                                                                            \
     do {                                                                                          \

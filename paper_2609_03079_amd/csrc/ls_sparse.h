@@ -43,20 +43,23 @@ __device__ inline int list_end(const int32_t* count, int end, int n_blk) {
 }
 
 // acc[i] += row . h[i] over this lane's 16-byte chunks (c = lane + 64 n), in the same order
-// whether or not the row is read alone; SS also sums h[i]^2 into ss[i].
-template <ls_dtype T, int B, bool SS>
+// whether or not the row is read alone; SS also sums h[i]^2 into ss[i].  U chunks' loads are
+// issued together (the order does not depend on U); prep() runs once, after the first loads.
+template <ls_dtype T, int B, bool SS, int U = 4, typename Prep = NoPrep>
 __device__ __forceinline__ void row_dot(const u32x4* row, const float* __restrict__ h, int d, int lane,
-                                        float (&acc)[B], float (&ss)[B]) {
+                                        float (&acc)[B], float (&ss)[B], Prep prep = Prep{}) {
     constexpr int V = Wt<T>::V;
-    constexpr int U = 4;
     const int nchunk = d / V;
-    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+    if (nchunk <= 0) prep();
+    for (int r0 = 0; r0 < nchunk; r0 += 64 * U) {
+        const int c0 = r0 + lane;
         u32x4 rw[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 64;
             rw[u] = c < nchunk ? ld_stream(row + c) : u32x4{0u, 0u, 0u, 0u};
         }
+        if (r0 == 0) prep();
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 64;
@@ -217,129 +220,137 @@ __device__ __forceinline__ void gateup_neuron(
 }
 
 // ---- down projection + residual -----------------------------------------------------------
-// Column tile `tile` of the down projection over list entries [begin, n_end), by 4 waves
-// (wave 0..3) that own `part`; x_acc = (begin == 0 ? x_in : x_acc) + y for the tile's columns.
+// Column tile `tile` of the down projection over list entries [begin, n_end), by the NP waves
+// (wave 0..NP-1) that own `part`; x_acc = (begin == 0 ? x_in : x_acc) + y for the tile's columns.
 // The activation of neuron j of entry e is a_buf[i F + (e - a_off) blk + j].
 // sync() is the barrier of the waves that share `part` (the workgroup's, or the group's);
 // a group with active == false only takes part in it.
-// Wave w takes the entries begin + w + 4j.  Its work is a sequence of items (entry j, chunk
-// pair p: chunks lane + 64 (2p + r), r = 0, 1 of the entry's piece) in entry-major order; the
-// loads of G items are issued together and the products are summed item by item, so the
-// result is the same for every G (G only sets how many loads are in flight).
+// The sum has one fixed order whatever NP and G are: kDnVirt virtual waves, virtual wave v
+// taking the entries begin + v + kDnVirt j; its work is a sequence of items (entry j, chunk
+// pair p: chunks lane + 64 (2p + r), r = 0, 1 of the entry's piece) in entry-major order,
+// summed item by item per lane; then lanes l, l+16, l+32, l+48 (the same column) are added,
+// and the column's total is the sum of the virtual waves' in order.  Physical wave w runs the
+// virtual waves w, w + NP, ... one after the other; the loads of G items are issued together.
+// So the per-call kernel (16 waves) and the stage-consuming kernel (a 4-wave group) agree
+// bit for bit.
 // ZS (row-level zero skip): a lane's 16-byte vector holds V neurons of one column; it is read
 // only when one of those neurons has a nonzero activation for some token.  The sums equal
 // those of the full read (a skipped product is an exact zero).
-// prep() runs once in every wave before the first activation is read: after the first
-// items' weight loads are issued (before anything, with ZS).  It may hold a barrier of the
-// four waves (a caller that stages the activations in LDS).
-template <ls_dtype T, int B, bool ZS, bool COH, int G, typename Sync, typename Prep = NoPrep>
+constexpr int kDnVirt = 16;
+
+template <ls_dtype T, int B, bool ZS, bool COH, int G, int NP, typename Sync, typename Prep = NoPrep>
 __device__ __forceinline__ void down_tile(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int F, int d, int blk, int n_blk,
     const int32_t* __restrict__ idx, int begin, int n_end,
     const float* __restrict__ x_in, float* __restrict__ x_acc, int tile, int wave, int lane, bool active,
-    float (&part)[4][kMaxBatch][kColTile], Sync sync, int a_off = 0, Prep prep = Prep{}) {
+    float (&part)[kDnVirt][kMaxBatch][kColTile], Sync sync, int a_off = 0, Prep prep = Prep{}) {
+    static_assert(kDnVirt % NP == 0, "whole virtual waves per physical wave");
     constexpr int V = Wt<T>::V;
     if (!active) n_end = begin;
     const int nchunk = blk * Wt<T>::kBytes;  // 16-byte chunks of one (block, tile) piece
     const int npair = (nchunk + 127) / 128;  // chunk pairs per lane and entry
-    const int n_mine = n_end > begin + wave ? (n_end - begin - wave + 3) / 4 : 0;
-    const int n_items = n_mine * npair;
     const size_t down_off = (size_t)2 * blk * d * Wt<T>::kBytes +
                             (size_t)tile * blk * kColTile * Wt<T>::kBytes;
-    float acc[B];
-#pragma unroll
-    for (int i = 0; i < B; ++i) acc[i] = 0.f;
     bool prepped = false;
     if (ZS) {
         prep();
         prepped = true;
     }
-    for (int it0 = 0; it0 < n_items; it0 += G) {
-        const u32x4* src[G];
-        int ent[G], c0[G];
+    for (int vw = wave; vw < kDnVirt; vw += NP) {
+        const int n_mine = n_end > begin + vw ? (n_end - begin - vw + kDnVirt - 1) / kDnVirt : 0;
+        const int n_items = n_mine * npair;
+        float acc[B];
 #pragma unroll
-        for (int u = 0; u < G; ++u) {
-            const int it = it0 + u;
-            const int j = it / npair, pr = it - j * npair;
-            const int e = begin + wave + 4 * j;
-            int b = it < n_items ? idx[e] : -1;
-            if (b >= n_blk) b = -1;
-            const int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
-            ent[u] = slot < 0 ? -1 : e;
-            c0[u] = lane + 128 * pr;
-            src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
-                                                    down_off);
-        }
-        bool use[G][2];
+        for (int i = 0; i < B; ++i) acc[i] = 0.f;
+        for (int it0 = 0; it0 < n_items; it0 += G) {
+            const u32x4* src[G];
+            int ent[G], c0[G];
 #pragma unroll
-        for (int u = 0; u < G; ++u)
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int c = c0[u] + 64 * r;
-                use[u][r] = ent[u] >= 0 && c < nchunk;
-                if (ZS && use[u][r]) {
-                    const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)(c / kColTile) * V;
-                    bool nz = false;
-#pragma unroll
-                    for (int i = 0; i < B; ++i) {
-#pragma unroll
-                        for (int qq = 0; qq < V / 4; ++qq) {
-                            const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
-                            nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
-                        }
-                    }
-                    use[u][r] = nz;
-                }
+            for (int u = 0; u < G; ++u) {
+                const int it = it0 + u;
+                const int j = it / npair, pr = it - j * npair;
+                const int e = begin + vw + kDnVirt * j;
+                int b = it < n_items ? idx[e] : -1;
+                if (b >= n_blk) b = -1;
+                const int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
+                ent[u] = slot < 0 ? -1 : e;
+                c0[u] = lane + 128 * pr;
+                src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
+                                                        down_off);
             }
-        u32x4 raw[G][2];
+            bool use[G][2];
 #pragma unroll
-        for (int u = 0; u < G; ++u)
+            for (int u = 0; u < G; ++u)
 #pragma unroll
-            for (int r = 0; r < 2; ++r)
-                raw[u][r] = use[u][r] ? ld_stream(src[u] + c0[u] + 64 * r) : u32x4{0u, 0u, 0u, 0u};
-        if (!prepped) {
-            prep();
-            prepped = true;
-        }
+                for (int r = 0; r < 2; ++r) {
+                    const int c = c0[u] + 64 * r;
+                    use[u][r] = ent[u] >= 0 && c < nchunk;
+                    if (ZS && use[u][r]) {
+                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)(c / kColTile) * V;
+                        bool nz = false;
 #pragma unroll
-        for (int u = 0; u < G; ++u)
+                        for (int i = 0; i < B; ++i) {
 #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int c = c0[u] + 64 * r;
-                if (use[u][r]) {
-                    float w[V];
-                    Wt<T>::widen(raw[u][r], w);
-                    const int grp = c / kColTile;  // this lane's V neurons
-                    const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)grp * V;
-#pragma unroll
-                    for (int i = 0; i < B; ++i) {
-#pragma unroll
-                        for (int qq = 0; qq < V / 4; ++qq) {
-                            const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
-                            acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
-                            acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
-                            acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
-                            acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                                nz |= (av.x != 0.f) | (av.y != 0.f) | (av.z != 0.f) | (av.w != 0.f);
+                            }
                         }
+                        use[u][r] = nz;
                     }
                 }
+            u32x4 raw[G][2];
+#pragma unroll
+            for (int u = 0; u < G; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r)
+                    raw[u][r] = use[u][r] ? ld_stream(src[u] + c0[u] + 64 * r) : u32x4{0u, 0u, 0u, 0u};
+            if (!prepped) {
+                prep();
+                prepped = true;
             }
+#pragma unroll
+            for (int u = 0; u < G; ++u)
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int c = c0[u] + 64 * r;
+                    if (use[u][r]) {
+                        float w[V];
+                        Wt<T>::widen(raw[u][r], w);
+                        const int grp = c / kColTile;  // this lane's V neurons
+                        const float* ap = a_buf + (size_t)(ent[u] - a_off) * blk + (size_t)grp * V;
+#pragma unroll
+                        for (int i = 0; i < B; ++i) {
+#pragma unroll
+                            for (int qq = 0; qq < V / 4; ++qq) {
+                                const f32x4 av = act_load4<COH>(ap + (size_t)i * F + 4 * qq);
+                                acc[i] = fmaf(av.x, w[4 * qq + 0], acc[i]);
+                                acc[i] = fmaf(av.y, w[4 * qq + 1], acc[i]);
+                                acc[i] = fmaf(av.z, w[4 * qq + 2], acc[i]);
+                                acc[i] = fmaf(av.w, w[4 * qq + 3], acc[i]);
+                            }
+                        }
+                    }
+                }
+        }
+        // lanes l, l+16, l+32, l+48 hold the same column
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            float v = acc[i];
+            v += __shfl_xor(v, 16, 64);
+            v += __shfl_xor(v, 32, 64);
+            if (lane < kColTile) part[vw][i][lane] = v;
+        }
     }
     if (!prepped) prep();
-    // lanes l, l+16, l+32, l+48 hold the same column
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-        float v = acc[i];
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
-        if (lane < kColTile) part[wave][i][lane] = v;
-    }
     sync();
     const int tid = wave * 64 + lane;
     if (active && tid < B * kColTile) {
         const int i = tid / kColTile, col = tid % kColTile;
-        const float y = ((part[0][i][col] + part[1][i][col]) + part[2][i][col]) + part[3][i][col];
+        float y = 0.f;
+#pragma unroll
+        for (int v = 0; v < kDnVirt; ++v) y += part[v][i][col];
         const size_t m = (size_t)i * d + (size_t)tile * kColTile + col;
         x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
     }

@@ -67,7 +67,7 @@ __device__ bool wait_lds(const int* c, int target, uint64_t limit) {
 
 struct Lds {
     float acts[kStageActs];
-    float part[4][kMaxBatch][kColTile];
+    float part[kDnVirt][kMaxBatch][kColTile];
     int arrived;      // gate/up waves: stages whose arrival word was seen (and acquired)
     int gu_done[kMaxStages];  // gate/up waves done with each stage
     int dn_bar;       // down group: barrier arrivals
@@ -163,11 +163,11 @@ __global__ __launch_bounds__(64 * kStageWaves) void stage_consumer_kernel(StageA
         }
         for (int tile = blockIdx.x; tile < ntiles && alive; tile += G) {
             if (staged)
-                down_tile<T, 1, false, false, 4>(p.blocks, p.block_bytes, p.slot_table, sh.acts, p.F, p.d, p.blk,
+                down_tile<T, 1, false, false, 4, 4>(p.blocks, p.block_bytes, p.slot_table, sh.acts, p.F, p.d, p.blk,
                                               p.n_blk, p.idx, lo, hi, p.x_in, p.x_acc, tile, wave, lane, work,
                                               sh.part, group_sync, lo);
             else
-                down_tile<T, 1, false, true, 4>(p.blocks, p.block_bytes, p.slot_table, p.a_buf, p.F, p.d, p.blk,
+                down_tile<T, 1, false, true, 4, 4>(p.blocks, p.block_bytes, p.slot_table, p.a_buf, p.F, p.d, p.blk,
                                              p.n_blk, p.idx, lo, hi, p.x_in, p.x_acc, tile, wave, lane, work,
                                              sh.part, group_sync);
             group_sync();  // the tile's partials (and the staged activations) are read before reuse
