@@ -97,6 +97,7 @@ constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
 // each lane also sums the squares of the x values it loads (every (token, k) exactly once per
 // workgroup) and the dot products are scaled at the end.
 constexpr int kChunkK = 512;                 // K values per chunk (1 KB of a 16-bit row)
+constexpr int kLpr = 2 * kChunkK / 1024;     // 1 KB loads per staged row and chunk
 constexpr int kRowPitch = 2 * kChunkK + 16;  // LDS bytes per staged row
 // three waves per SIMD (at most 168 registers a lane): three workgroups per CU
 constexpr int kGuWavesPerEu = 3;
@@ -131,18 +132,22 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGu
     auto row_ptr = [&](int j) {
         return base + (size_t)(j < 16 ? r0 + j : blk + r0 + j - 16) * row_bytes;
     };
-    auto load_chunk = [&](int c0, u32x4 (&rw)[kRowsW]) {
+    auto load_chunk = [&](int c0, u32x4 (&rw)[kRowsW * kLpr]) {
         const int bytes = 2 * min(kChunkK, d - c0);
 #pragma unroll
         for (int i = 0; i < kRowsW; ++i) {
             const int j = wave + kWaves * i;
-            rw[i] = lane * 16 < bytes ? ld_stream(reinterpret_cast<const u32x4*>(row_ptr(j) + (size_t)c0 * 2 + lane * 16))
-                                      : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int h = 0; h < kLpr; ++h) {
+                const int off = 1024 * h + lane * 16;
+                rw[i * kLpr + h] = off < bytes ? ld_stream(reinterpret_cast<const u32x4*>(row_ptr(j) + (size_t)c0 * 2 + off))
+                                               : u32x4{0u, 0u, 0u, 0u};
+            }
         }
     };
-    // x of this wave's K steps of a chunk (s0 = wave + kWaves j), fetched one chunk ahead with
-    // the weights: waiting for them never waits for the next chunk's weight loads (the counter
-    // of outstanding loads drains in issue order)
+    // x of this wave's K steps of a chunk (s0 = wave + kWaves j), requested once the wave is
+    // done with the previous chunk's (after the next chunk's weights: a wave waits for both
+    // at the top of the chunk anyway)
     constexpr int kStepsW = kChunkK / 32 / kWaves;
     auto load_x = [&](int c0, f32x4 (&hx)[kStepsW][2]) {
         const int steps = min(kChunkK, d - c0) / 32;
@@ -158,29 +163,26 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGu
     };
     f32x4v cg = {0.f, 0.f, 0.f, 0.f}, cu = {0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
-    u32x4 rw[kRowsW];
+    u32x4 rw[kRowsW * kLpr];
     f32x4 hx[kStepsW][2];
     load_chunk(0, rw);
     load_x(0, hx);
     for (int c0 = 0; c0 < d; c0 += kChunkK) {
         const int steps = min(kChunkK, d - c0) / 32;
-        f32x4 hc[kStepsW][2];
-#pragma unroll
-        for (int j = 0; j < kStepsW; ++j) hc[j][0] = hx[j][0], hc[j][1] = hx[j][1];
+        const bool more = c0 + kChunkK < d;
 #pragma unroll
         for (int i = 0; i < kRowsW; ++i)
-            *reinterpret_cast<u32x4*>(stage + (wave + kWaves * i) * kRowPitch + lane * 16) = rw[i];
+#pragma unroll
+            for (int h = 0; h < kLpr; ++h)
+                *reinterpret_cast<u32x4*>(stage + (wave + kWaves * i) * kRowPitch + 1024 * h + lane * 16) = rw[i * kLpr + h];
         __syncthreads();
-        if (c0 + kChunkK < d) {  // in flight while this chunk runs
-            load_chunk(c0 + kChunkK, rw);
-            load_x(c0 + kChunkK, hx);
-        }
+        if (more) load_chunk(c0 + kChunkK, rw);  // in flight while this chunk runs
 #pragma unroll
         for (int j = 0; j < kStepsW; ++j) {
             const int s0 = wave + kWaves * j;
             if (s0 >= steps) break;
             const int kc = 32 * s0 + 8 * (lane >> 4);
-            const f32x4 h0 = hc[j][0], h1 = hc[j][1];
+            const f32x4 h0 = hx[j][0], h1 = hx[j][1];
             const float xv[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
             if (RMS) {
 #pragma unroll
@@ -196,6 +198,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGu
             cu = S::mfma(wu, hi, cu);
             cu = S::mfma(wu, lo, cu);
         }
+        if (more) load_x(c0 + kChunkK, hx);
         __syncthreads();  // every wave is done with the chunk before it is overwritten
     }
     // lane l holds rows 4 (l / 16) + i, token l % 16 of this wave's partial sums
