@@ -1129,10 +1129,20 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
         const ls::LayerDev& L = c->dev[l];
         st = predictor_gemv(c, L, cur, B, c->scores);
         if (st != LS_OK) return st;
-        LS_HIP(c, timed(c, LS_K_SELECT, [&] {
-            return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count, c->stream);
-        }));
-        LS_HIP(c, timed(c, LS_K_GATEUP, [&] { return ls::launch_gateup(s, L, nullptr, cur, B, c->idx, c->count, 0, cap, c->a, c->stream); }));
+        if (ls::gateup_select_ok(s, B, k)) {
+            // batch 1: the selection runs inside the gate/up launch (one launch fewer per layer)
+            LS_HIP(c, timed(c, LS_K_GATEUP, [&] {
+                return ls::launch_gateup_select(s, L, cur, c->scores, k, c->idx, c->count, c->a, c->stream);
+            }));
+        } else {
+            LS_HIP(c, timed(c, LS_K_SELECT, [&] {
+                return ls::launch_select(c->scores, B, s.n_blk, LS_SEL_TOPK, k, 0.f, 1, cap, c->idx, c->count,
+                                         c->stream);
+            }));
+            LS_HIP(c, timed(c, LS_K_GATEUP, [&] {
+                return ls::launch_gateup(s, L, nullptr, cur, B, c->idx, c->count, 0, cap, c->a, c->stream);
+            }));
+        }
         LS_HIP(c, timed(c, LS_K_DOWN, [&] { return ls::launch_down(s, L, nullptr, c->a, B, c->idx, c->count, 0, cap, cur, nxt, c->dn_part, c->stream); }));
         std::swap(cur, nxt);
     }

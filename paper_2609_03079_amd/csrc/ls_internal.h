@@ -91,6 +91,12 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
 hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                          const float* x, int B, const int32_t* idx, const int32_t* count,
                          int begin, int end, float* a_buf, hipStream_t st);
+// Batch 1, resident weights: the top-k selection of `scores` (as launch_select with
+// LS_SEL_TOPK, k, no union) and the gate/up gather of its list in one launch; writes idx[0..n)
+// and count[0] = n for launch_down.  gateup_select_ok: whether the shape allows it.
+bool gateup_select_ok(const Shape& s, int B, int k);
+hipError_t launch_gateup_select(const Shape& s, const LayerDev& L, const float* x, const float* scores, int k,
+                                int32_t* idx, int32_t* count, float* a_buf, hipStream_t st);
 // part: [kDownSplits, B, d] floats of scratch for the matrix-core path's split list (may be
 // null: no split)
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,

@@ -139,6 +139,94 @@ __device__ inline int rank_in(const uint64_t* __restrict__ w, int n_pad, uint64_
     return rank;
 }
 
+// One token's selection by one wave.  With a union: fold the members into bkey (largest key
+// per block) and umask (OR of the member sets); otherwise rank them through mk (an LDS row of
+// at least n + 8 words) and write out_idx[rank] = block index and out_count[0].
+template <int Q>
+__device__ __forceinline__ void select_token(const float* __restrict__ row, int n, int mode, int k, float tau,
+                                             int lane, bool UNION, uint64_t* mk, uint32_t* bkey, uint32_t* umask,
+                                             int32_t* __restrict__ out_idx, int32_t* __restrict__ out_count) {
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int Qn = (n + 63) / 64;
+    // all Q loads in flight before the first use (indices past n re-read entry n - 1, n >= 1)
+    float sv[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) sv[q] = row[min(q * 64 + lane, n - 1)];
+    // entries past n get key 0: below every search candidate (>= 1) and never > T
+    uint32_t ok[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int i = q * 64 + lane;
+        ok[q] = i < n ? order_key(sv[q]) : 0u;
+        if (UNION && i < n) atomicMax(&bkey[i], ok[q]);
+    }
+    // membership rule: key > T, or key == T among the first `rem` such by index
+    uint32_t T = 0u;
+    int rem = 0;
+    const bool thr_mode = mode != LS_SEL_TOPK;
+    if (!thr_mode) {
+        auto step = [&](int bit) {
+            const uint32_t c = T | (1u << bit);
+            int cnt = 0;
+#pragma unroll
+            for (int q = 0; q < Q; ++q) cnt += __popcll(__ballot(ok[q] >= c));
+            if (cnt >= k) T = c;
+        };
+        int bit = 31;
+        for (; bit >= 16; --bit) step(bit);
+        // top 16 bits decided: with exactly k keys at or above them the members are every
+        // such key whatever T's low bits become (ties at T are then all taken), so the low
+        // steps are skipped; T != 0 keeps the padding out of the count
+        int ge = 0;
+        if (T != 0u) {
+#pragma unroll
+            for (int q = 0; q < Q; ++q) ge += __popcll(__ballot(ok[q] >= T));
+        }
+        if (ge != k)
+            for (; bit >= 0; --bit) step(bit);
+        int gt = 0;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) gt += __popcll(__ballot(ok[q] > T));
+        rem = k - gt;
+    }
+    const uint32_t ktau = isnan(tau) ? 0xffffffffu : order_key(tau);
+    int m = 0, eq_before = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        if (q < Qn) {
+            const int i = q * 64 + lane;
+            const bool valid = i < n;
+            bool mem;
+            if (thr_mode) {
+                mem = valid && ok[q] != 0u && ok[q] > ktau;
+            } else {
+                const bool eq = valid && ok[q] == T;
+                const uint64_t eqb = __ballot(eq);
+                mem = valid && (ok[q] > T || (eq && eq_before + __popcll(eqb & below) < rem));
+                eq_before += __popcll(eqb);
+            }
+            const uint64_t mb = __ballot(mem);
+            if (mem) {
+                if (UNION)
+                    atomicOr(&umask[i >> 5], 1u << (i & 31));
+                else
+                    mk[m + __popcll(mb & below)] = rank_word(ok[q], i);
+            }
+            m += __popcll(mb);
+        }
+    }
+    if (!UNION) {
+        const int m_pad = (m + 7) & ~7;
+        if (lane < m_pad - m) mk[m + lane] = 0ull;
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        for (int p = lane; p < m; p += 64) {
+            const uint64_t mine = mk[p];
+            out_idx[rank_in(mk, m_pad, mine)] = 0xffff - (int)(uint32_t)mine;
+        }
+        if (lane == 0) out_count[0] = m;
+    }
+}
+
 template <int Q>
 __global__ __launch_bounds__(Q > 8 ? 512 : 1024) void select_kernel(const float* __restrict__ scores, int B,
                                                       int n, int mode, int k, float tau,
@@ -161,83 +249,8 @@ __global__ __launch_bounds__(Q > 8 ? 512 : 1024) void select_kernel(const float*
         __syncthreads();
     }
     for (int b = wave; b < B; b += nwaves) {
-        // all Q loads in flight before the first use (indices past n re-read entry n - 1, n >= 1)
-        float sv[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) sv[q] = scores[(size_t)b * n + min(q * 64 + lane, n - 1)];
-        // entries past n get key 0: below every search candidate (>= 1) and never > T
-        uint32_t ok[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int i = q * 64 + lane;
-            ok[q] = i < n ? order_key(sv[q]) : 0u;
-            if (do_union && i < n) atomicMax(&bkey[i], ok[q]);
-        }
-        // membership rule: key > T, or key == T among the first `rem` such by index
-        uint32_t T = 0u;
-        int rem = 0;
-        bool thr_mode = mode != LS_SEL_TOPK;
-        if (!thr_mode) {
-            auto step = [&](int bit) {
-                const uint32_t c = T | (1u << bit);
-                int cnt = 0;
-#pragma unroll
-                for (int q = 0; q < Q; ++q) cnt += __popcll(__ballot(ok[q] >= c));
-                if (cnt >= k) T = c;
-            };
-            int bit = 31;
-            for (; bit >= 16; --bit) step(bit);
-            // top 16 bits decided: with exactly k keys at or above them the members are every
-            // such key whatever T's low bits become (ties at T are then all taken), so the low
-            // steps are skipped; T != 0 keeps the padding out of the count
-            int ge = 0;
-            if (T != 0u) {
-#pragma unroll
-                for (int q = 0; q < Q; ++q) ge += __popcll(__ballot(ok[q] >= T));
-            }
-            if (ge != k)
-                for (; bit >= 0; --bit) step(bit);
-            int gt = 0;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) gt += __popcll(__ballot(ok[q] > T));
-            rem = k - gt;
-        }
-        const uint32_t ktau = isnan(tau) ? 0xffffffffu : order_key(tau);
-        int m = 0, eq_before = 0;
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            if (q < Qn) {
-                const int i = q * 64 + lane;
-                const bool valid = i < n;
-                bool mem;
-                if (thr_mode) {
-                    mem = valid && ok[q] != 0u && ok[q] > ktau;
-                } else {
-                    const bool eq = valid && ok[q] == T;
-                    const uint64_t eqb = __ballot(eq);
-                    mem = valid && (ok[q] > T || (eq && eq_before + __popcll(eqb & below) < rem));
-                    eq_before += __popcll(eqb);
-                }
-                const uint64_t mb = __ballot(mem);
-                if (mem) {
-                    if (do_union)
-                        atomicOr(&umask[i >> 5], 1u << (i & 31));
-                    else
-                        mk[b][m + __popcll(mb & below)] = rank_word(ok[q], i);
-                }
-                m += __popcll(mb);
-            }
-        }
-        if (!do_union) {
-            const int m_pad = (m + 7) & ~7;
-            if (lane < m_pad - m) mk[b][m + lane] = 0ull;
-            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
-            for (int p = lane; p < m; p += 64) {
-                const uint64_t mine = mk[b][p];
-                idx[(size_t)b * cap + rank_in(mk[b], m_pad, mine)] = 0xffff - (int)(uint32_t)mine;
-            }
-            if (lane == 0) count[b] = m;
-        }
+        select_token<Q>(scores + (size_t)b * n, n, mode, k, tau, lane, do_union, mk[b], bkey, umask,
+                        idx + (size_t)b * cap, count + b);
     }
     if (!do_union) return;
     __syncthreads();
@@ -302,6 +315,43 @@ __global__ __launch_bounds__(256) void gateup_kernel(
     }
 }
 
+// ---- batch 1: the selection and the gate/up gather in one launch --------------------------
+// Wave 0 of every workgroup ranks the token's scores into LDS with the selection kernel's own
+// code (so the list is the same) while the other waves copy the input to LDS; after one barrier
+// each wave takes its neuron of the list, exactly as gateup_kernel with the input in LDS.
+// Workgroup 0 also writes the list and its length for the down projection.  Every workgroup
+// repeats the ranking of a few hundred keys, which costs about what the separate selection
+// launch did and saves that launch.
+template <ls_dtype T, ls_act A, bool RMS, int U, int Q>
+__global__ __launch_bounds__(256) void gateup_select_kernel(
+    const uint8_t* __restrict__ blocks, size_t block_bytes, const void* __restrict__ bias, float thresh,
+    const float* __restrict__ h, int d, int blk, int n_blk, int F, const float* __restrict__ scores, int k,
+    int32_t* __restrict__ idx, int32_t* __restrict__ count, float* __restrict__ a_buf) {
+    extern __shared__ f32x4 hs[];
+    __shared__ uint64_t mk[Q * 64 + 8];
+    __shared__ int32_t list[Q * 64];
+    __shared__ int32_t lcount;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (wave == 0) {
+        select_token<Q>(scores, n_blk, LS_SEL_TOPK, k, 0.f, lane, false, mk, nullptr, nullptr, list, &lcount);
+    } else {
+        const f32x4* src = reinterpret_cast<const f32x4*>(h);
+        for (int i = (int)threadIdx.x - 64; i < d / 4; i += 192) hs[i] = src[i];
+    }
+    __syncthreads();
+    const int n = lcount;
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i < n; i += 256) idx[i] = list[i];
+        if (threadIdx.x == 0) count[0] = n;
+    }
+    const long t = (long)blockIdx.x * 4 + wave;
+    const int e = (int)(t / blk), q = (int)(t % blk);
+    if (e >= n) return;
+    gateup_neuron<T, A, 1, RMS, false, false, U>(blocks, block_bytes, nullptr, bias, thresh,
+                                                 reinterpret_cast<const float*>(hs), d, blk, n_blk, F, list[e], e,
+                                                 q, a_buf, lane);
+}
+
 // ---- down projection + residual: one workgroup of kDnWaves waves per 16-column tile ------
 // G: (entry, chunk pair) items whose loads each wave issues together.
 // AS: the range's activations (B (end - begin) blk floats, at most kDownActs) are first copied
@@ -346,6 +396,60 @@ __global__ __launch_bounds__(64 * kDnWaves) __attribute__((amdgpu_waves_per_eu(O
 }
 
 }  // namespace
+
+template <ls_dtype T, ls_act A>
+static hipError_t gateup_select_t(const Shape& s, const LayerDev& L, const float* h, const float* scores, int k,
+                                  int32_t* idx, int32_t* count, float* a_buf, hipStream_t st) {
+    const long tasks = (long)k * s.blk;
+    const dim3 grid((unsigned)((tasks + 3) / 4)), blk(256);
+    const size_t bb = s.block_elems * elem_size(s.dtype);
+    const size_t hs_bytes = (size_t)s.d * sizeof(float);
+    const int per_lane = (s.d / Wt<T>::V + 63) / 64;
+#define LS_GS_K(RMS, U, Q)                                                                                    \
+    hipLaunchKernelGGL((gateup_select_kernel<T, A, RMS, U, Q>), grid, blk, hs_bytes, st, L.blocks, bb, L.bias, \
+                       L.threshold, h, s.d, s.blk, s.n_blk, s.F, scores, k, idx, count, a_buf)
+#define LS_GS_Q(RMS, U)                                     \
+    do {                                                    \
+        if (s.n_blk <= 256) LS_GS_K(RMS, U, 4);             \
+        else LS_GS_K(RMS, U, 8);                            \
+    } while (0)
+#define LS_GS_U(RMS)                                        \
+    do {                                                    \
+        if (per_lane <= 4) LS_GS_Q(RMS, 4);                 \
+        else if (per_lane <= 8) LS_GS_Q(RMS, 8);            \
+        else if (per_lane <= 12) LS_GS_Q(RMS, 12);          \
+        else LS_GS_Q(RMS, 16);                              \
+    } while (0)
+    if (s.prenorm) LS_GS_U(true); else LS_GS_U(false);
+#undef LS_GS_U
+#undef LS_GS_Q
+#undef LS_GS_K
+    return hipGetLastError();
+}
+
+bool gateup_select_ok(const Shape& s, int B, int k) {
+    return B == 1 && !s.zero_skip && k >= 1 && k <= s.n_blk && s.n_blk <= 512 &&
+           (size_t)s.d * sizeof(float) <= 32768;
+}
+
+hipError_t launch_gateup_select(const Shape& s, const LayerDev& L, const float* h, const float* scores, int k,
+                                int32_t* idx, int32_t* count, float* a_buf, hipStream_t st) {
+    if (k < 1) return hipSuccess;
+    const bool relu = s.act == LS_ACT_REGLU;
+    switch (s.dtype) {
+        case LS_F32:
+            return relu ? gateup_select_t<LS_F32, LS_ACT_REGLU>(s, L, h, scores, k, idx, count, a_buf, st)
+                        : gateup_select_t<LS_F32, LS_ACT_SWIGLU_THRESH>(s, L, h, scores, k, idx, count, a_buf, st);
+        case LS_F16:
+            return relu ? gateup_select_t<LS_F16, LS_ACT_REGLU>(s, L, h, scores, k, idx, count, a_buf, st)
+                        : gateup_select_t<LS_F16, LS_ACT_SWIGLU_THRESH>(s, L, h, scores, k, idx, count, a_buf, st);
+        case LS_BF16:
+            return relu ? gateup_select_t<LS_BF16, LS_ACT_REGLU>(s, L, h, scores, k, idx, count, a_buf, st)
+                        : gateup_select_t<LS_BF16, LS_ACT_SWIGLU_THRESH>(s, L, h, scores, k, idx, count, a_buf, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 
 
 template <ls_dtype T, bool RMS>

@@ -324,6 +324,32 @@ def test_invalid_arguments_return_codes():
     assert e.value.status == lsffn.LS_E_INVAL
 
 
+@pytest.mark.parametrize("name", ["f16_b64", "bf16_swiglu", "f32_stack", "llama2_7b_2l", "llama2_13b_2l"])
+def test_decode_step_per_kernel_equals_entry_points(name):
+    """ls_decode_step on the per-kernel path at B = 1, where the selection runs inside the
+    gate/up launch, gives the same bits as ls_predict, ls_select_blocks and
+    ls_sparse_ffn_step called layer by layer."""
+    cfg = SMALL[name] if name in SMALL else {"llama2_7b_2l": C["llama2_7b_ffn"],
+                                             "llama2_13b_2l": C["llama2_13b_ffn"]}[name].with_(n_layers=2)
+    f, ws = make_ffn(cfg)
+    f.ls_configure(lsffn.LS_CFG_DECODE_PATH, 1)
+    for t in range(2):
+        x0 = lsgen.tokens(cfg, 21 + t, 1, 1)[0]
+        x = dev_f32(x0)
+        f.ls_decode_step(x, 1, cfg.k)
+        got = host(x)
+        xin, xout = dev_f32(x0), empty_f32(1, cfg.d_model)
+        scores = empty_f32(1, cfg.n_blk)
+        idx, cnt = empty_i32(cfg.k), empty_i32(1)
+        for l in range(cfg.n_layers):
+            f.ls_predict(l, xin, 1, scores)
+            f.ls_select_blocks(scores, 1, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 0, cfg.k, idx, cnt)
+            f.ls_sparse_ffn_step(l, xin, 1, idx, cnt, 0, cfg.k, xout)
+            xin, xout = xout, xin
+        assert np.array_equal(got, host(xin)), (name, t)
+    f.ls_ffn_sync()
+
+
 @pytest.mark.parametrize("cfg_name", ["llama2_7b_ffn", "llama2_13b_ffn", "mistral_7b_ffn"])
 def test_full_size_layers_sampled(cfg_name):
     """Full-size layer shapes (2 layers of each stack), B=1, teacher-forced per layer."""
