@@ -22,6 +22,11 @@ struct ls_ffn {
     int device = 0;
     hipStream_t stream = nullptr;
     hipStream_t copy_stream = nullptr;
+    // host-resident mode: a second copy stream takes every other block copy of a stage (one
+    // stream keeps the host link about 92% busy with block-sized copies, two about 100%); it
+    // forks from copy_stream at each request and joins back before each stage is signalled
+    hipStream_t copy_stream2 = nullptr;
+    hipEvent_t copy_fork = nullptr, copy_join = nullptr;
     size_t block_bytes = 0;
     size_t layer_bytes = 0;  // blocks + bias + predictor (resident arena of one layer)
 
@@ -308,7 +313,11 @@ void free_all(ls_ffn* c) {
     if (c->idx_pinned) (void)hipHostFree(c->idx_pinned);
     if (c->stage_done) (void)hipHostFree(c->stage_done);
     if (c->arrive) arrive_give(c->arrive, c->arrive_bytes);
+    if (c->copy_stream2) (void)hipStreamSynchronize(c->copy_stream2);
     if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
+    if (c->copy_stream2) (void)hipStreamDestroy(c->copy_stream2);
+    if (c->copy_fork) (void)hipEventDestroy(c->copy_fork);
+    if (c->copy_join) (void)hipEventDestroy(c->copy_join);
     for (auto e : c->table_uploaded) if (e) (void)hipEventDestroy(e);
     for (auto& p : c->pending) {
         (void)hipEventDestroy(p.start);
@@ -434,7 +443,10 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             return bail(LS_E_DEVICE, "slot table upload failed");
         c->bcache = new (std::nothrow) ls::BlockCache(slots, L, s.n_blk);
         if (!c->bcache) return bail(LS_E_NOMEM, "host allocation failed");
-        if (hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking) != hipSuccess)
+        if (hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking) != hipSuccess ||
+            hipStreamCreateWithFlags(&c->copy_stream2, hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&c->copy_fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&c->copy_join, hipEventDisableTiming) != hipSuccess)
             return bail(LS_E_DEVICE, "stream creation failed");
         c->table_uploaded.assign(L, nullptr);
         c->layer_done.assign(L, nullptr);
@@ -827,6 +839,12 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
     size_t fi = 0;
     const uint8_t* layer_host = c->host_blocks[layer];
     int written = 0;
+    // the second copy stream starts after everything queued on the first (the waits and table
+    // uploads above included)
+    if (!fills.empty()) {
+        LS_HIP(c, hipEventRecord(c->copy_fork, c->copy_stream));
+        LS_HIP(c, hipStreamWaitEvent(c->copy_stream2, c->copy_fork, 0));
+    }
     for (int sidx = 0; sidx < n_stages; ++sidx) {
         const int lo = (int)((int64_t)sidx * n / n_stages), hi = (int)((int64_t)(sidx + 1) * n / n_stages);
         const size_t fi0 = fi;
@@ -834,8 +852,12 @@ static ls_status stream_request(ls_ffn* c, int32_t layer, const int32_t* idx_hos
             const auto& f = fills[fi];
             LS_HIP(c, hipMemcpyAsync(c->cache + (size_t)f.slot * c->block_bytes,
                                      layer_host + (size_t)f.block * c->block_bytes, c->block_bytes,
-                                     hipMemcpyHostToDevice, c->copy_stream));
+                                     hipMemcpyHostToDevice, (fi - fi0) % 2 ? c->copy_stream2 : c->copy_stream));
             if (copied) copied->push_back(f.block);
+        }
+        if (fi - fi0 > 1) {  // the stage's copies on the second stream are done before it is signalled
+            LS_HIP(c, hipEventRecord(c->copy_join, c->copy_stream2));
+            LS_HIP(c, hipStreamWaitEvent(c->copy_stream, c->copy_join, 0));
         }
         if (!arrive_tag) {
             LS_HIP(c, hipEventRecord(events[sidx], c->copy_stream));
