@@ -17,7 +17,7 @@ if not torch.cuda.is_available():  # pragma: no cover
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2609_03079_amd as lsffn  # noqa: E402
-from gpu_util import (SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn,  # noqa: E402
+from gpu_util import (DEV, SCORE_TOL, Y_TOL, dev_f32, empty_f32, empty_i32, host, make_ffn,  # noqa: E402
                       rel_l2, y_err)
 
 C = lsgen.CONFIGS
@@ -324,13 +324,20 @@ def test_invalid_arguments_return_codes():
     assert e.value.status == lsffn.LS_E_INVAL
 
 
-@pytest.mark.parametrize("name", ["f16_b64", "bf16_swiglu", "f32_stack", "llama2_7b_2l", "llama2_13b_2l"])
+WIDE = {
+    "llama2_7b_2l": C["llama2_7b_ffn"].with_(n_layers=2),
+    "llama2_13b_2l": C["llama2_13b_ffn"].with_(n_layers=2),
+    # 300 blocks: the selection inside the gate/up launch takes its 8-keys-per-lane form
+    "f16_nb300": C["llama2_7b_ffn"].with_(n_layers=2, d_model=512, d_ff=4800, block=16, rank=64, keep_pct=10),
+}
+
+
+@pytest.mark.parametrize("name", ["f16_b64", "bf16_swiglu", "f32_stack", "llama2_7b_2l", "llama2_13b_2l", "f16_nb300"])
 def test_decode_step_per_kernel_equals_entry_points(name):
     """ls_decode_step on the per-kernel path at B = 1, where the selection runs inside the
     gate/up launch, gives the same bits as ls_predict, ls_select_blocks and
     ls_sparse_ffn_step called layer by layer."""
-    cfg = SMALL[name] if name in SMALL else {"llama2_7b_2l": C["llama2_7b_ffn"],
-                                             "llama2_13b_2l": C["llama2_13b_ffn"]}[name].with_(n_layers=2)
+    cfg = SMALL[name] if name in SMALL else WIDE[name]
     f, ws = make_ffn(cfg)
     f.ls_configure(lsffn.LS_CFG_DECODE_PATH, 1)
     for t in range(2):
@@ -347,6 +354,24 @@ def test_decode_step_per_kernel_equals_entry_points(name):
             f.ls_sparse_ffn_step(l, xin, 1, idx, cnt, 0, cfg.k, xout)
             xin, xout = xout, xin
         assert np.array_equal(got, host(xin)), (name, t)
+    f.ls_ffn_sync()
+
+
+@pytest.mark.parametrize("cfg_name", ["llama2_13b_ffn", "mistral_7b_ffn"])
+def test_every_block_selected_equals_dense(cfg_name):
+    """One full-size layer with every block in the list at B = 1: the activations no longer fit
+    the down kernel's LDS copy (13B shape: 216 x 64 floats), so it reads them from memory; with
+    d = 5120 it also runs two workgroups per CU.  The result is the dense FFN (oracle)."""
+    cfg = C[cfg_name].with_(n_layers=1)
+    f, ws = make_ffn(cfg)
+    x = lsgen.tokens(cfg, 3, 1, 1)[0]
+    x_in = dev_f32(x)
+    x_out = empty_f32(1, cfg.d_model)
+    idx = torch.arange(cfg.n_blk, dtype=torch.int32, device=DEV)
+    cnt = torch.full((1,), cfg.n_blk, dtype=torch.int32, device=DEV)
+    f.ls_sparse_ffn_step(0, x_in, 1, idx, cnt, 0, cfg.n_blk, x_out)
+    y = host(x_out).astype(np.float64) - x.astype(np.float64)
+    _check_y(f, ws[0], cfg, x, y, np.arange(cfg.n_blk), Y_TOL[cfg.dtype], cfg_name)
     f.ls_ffn_sync()
 
 
