@@ -222,8 +222,6 @@ struct Smem {
     int hole_miss[kMaxKp];   // speculative position -> miss it recomputes, or -1
     int missE[kMaxKp];       // miss m -> E entry
     int row_of_e[kMaxKp];    // E entry -> list position whose partial row holds its partial
-    int hole_pos[kMaxKp];    // miss m -> the list position (hole) that computes it
-    int n_miss;
     int posE[kMaxNb];   // block -> position in E, or -1
     int posP[kMaxNb];   // block -> position in the current speculative list, or -1
     alignas(16) float aall[kMaxA];  // activations of the speculative list, in list order
