@@ -232,7 +232,7 @@ struct Smem {
     u32x4 dnl[kMaxDnTot][64 * kDnPer];
     alignas(16) float amiss[kMaxKp][64];  // activations of the misses
     // LDS flags (value = layer + 1 once set for that layer)
-    int f_keys, f_acts, f_E, f_pn, f_out;
+    int f_keys, f_acts, f_E, f_pn, f_out, f_mrows;
     int f_done[kWaves];
 };
 
@@ -382,27 +382,32 @@ __device__ __forceinline__ void ctl_gate_up(const Smem& sm, const Geo& g, int la
     }
 }
 
-// Control wave, misses: this tile's down partial of misses 0..M-1 (rows kMaxDnTot + m of
-// dparts), eight at a time: their down pieces are requested first, then their activations
-// are gathered from every workgroup.
+// Control wave, misses: this tile's down pieces of misses m0..m0+cnt-1 (cnt <= 8).
 template <ls_dtype T>
-__device__ __forceinline__ void ctl_miss_down(const FusedArgs& P, Smem& sm, const Geo& g, int l,
-                                              int M, int lane) {
-    constexpr int V = Wt<T>::V;
+__device__ __forceinline__ void miss_pieces(const FusedArgs& P, const Smem& sm, const Geo& g, int l, int m0,
+                                            int cnt, int lane, u32x4 (&pc)[8][kDnPer]) {
     constexpr int KB = Wt<T>::kBytes;
     const size_t down_off = 2 * (size_t)g.blk * P.d * KB + (size_t)g.w * g.blk * kColTile * KB;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        if (u < cnt) {
+            const uint8_t* base = sm.lt[l].blocks + (size_t)sm.E[sm.missE[m0 + u]] * P.block_bytes + down_off;
+#pragma unroll
+            for (int i = 0; i < kDnPer; ++i) pc[u][i] = gload_u(base, (uint32_t)min(lane + 64 * i, g.NPC - 1) * 16u);
+        }
+    }
+}
+
+// Control wave, misses: this tile's down partial of misses 0..M-1 (rows kMaxDnTot + m of
+// dparts), eight at a time: their down pieces are requested first (the first eight's by the
+// caller, in pc), then their activations are gathered from every workgroup.
+template <ls_dtype T>
+__device__ __forceinline__ void ctl_miss_down(const FusedArgs& P, Smem& sm, const Geo& g, int l,
+                                              int M, int lane, u32x4 (&pc)[8][kDnPer]) {
+    constexpr int V = Wt<T>::V;
     for (int m0 = 0; m0 < M; m0 += 8) {
         const int cnt = min(M - m0, 8);
-        u32x4 pc[8][kDnPer];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            if (u < cnt) {
-                const uint8_t* base = sm.lt[l].blocks + (size_t)sm.E[sm.missE[m0 + u]] * P.block_bytes + down_off;
-#pragma unroll
-                for (int i = 0; i < kDnPer; ++i)
-                    pc[u][i] = gload_u(base, (uint32_t)min(lane + 64 * i, g.NPC - 1) * 16u);
-            }
-        }
+        if (m0 > 0) miss_pieces<T>(P, sm, g, l, m0, cnt, lane, pc);
         const int n = cnt * g.blk;
         uint64_t v[8];
         wait_words<8>(P.amb + (size_t)l * g.AW + g.miss_base + m0 * g.blk, n, g.tag, lane, P.err, v);
@@ -566,8 +571,11 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
         }
         LS_STAMP(P, g, l, 6, lane == 0);
+        u32x4 pc[8][kDnPer];
         if (M > 0) {
-            // activations of the misses' neurons held by this workgroup's hole slots
+            // this tile's down pieces of the first eight misses, then the activations of the
+            // misses' neurons held by this workgroup's hole slots
+            if (g.has_tile) miss_pieces<T>(P, sm, g, l, 0, min(M, 8), lane, pc);
             for (int i0 = 0; i0 < kWorkers * kSlots; i0 += 2) {
                 int bb2[2], qq2[2], mm2[2];
 #pragma unroll
@@ -585,9 +593,11 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                     if (mm2[u] >= 0 && lane == 0)
                         mb_store(P.amb + (size_t)l * g.AW + g.miss_base + mm2[u] * g.blk + qq2[u], g.tag, a2[u]);
             }
-            // this tile's down partial of every miss
-            if (g.has_tile) ctl_miss_down<T>(P, sm, g, l, M, lane);
         }
+        // the misses' rows are in: the workers may queue the next layer's loads behind them
+        flag_set(&sm.f_mrows, l + 1, lane);
+        // this tile's down partial of every miss
+        if (M > 0 && g.has_tile) ctl_miss_down<T>(P, sm, g, l, M, lane, pc);
         LS_STAMP(P, g, l, 7, lane == 0);
         // every worker's down partials of the list positions
 #pragma unroll
@@ -779,13 +789,15 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
             const int p = ok ? p0 : 0;  // a lane group without a position reads position 0
             u32x4 wr[NG];
             f32x4 av[NG][V / 4];
+            const f32x4* a4 = reinterpret_cast<const f32x4*>(sm.aall) + p * (g.blk / 4);
 #pragma unroll
             for (int n = 0; n < NG; ++n) {
                 wr[n] = sm.dnl[p][n * kColTile + c];
 #pragma unroll
-                for (int i = 0; i < V / 4; ++i)
-                    av[n][i] = reinterpret_cast<const f32x4*>(sm.aall + p * g.blk + n * V)[i];
+                for (int i = 0; i < V / 4; ++i) av[n][i] = a4[n * (V / 4) + i];
             }
+            // all of the round's LDS reads are in flight before the first product
+            __builtin_amdgcn_sched_barrier(0);
             float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int n = 0; n < NG; ++n) {
@@ -893,9 +905,11 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         }
         flag_wait(&sm.f_acts, l + 1, lane, P.err);
         LS_STAMP(P, g, l, 15, wave == 3 && lane == 0);
+        // list positions of this wave: (wave - 1) + kWorkers * jp below kp; round r takes 4r..4r+3
+        const int npos = min(kDnPos, (g.kp - (wave - 1) + kWorkers - 1) / kWorkers);
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
-            if (l > 0 && g.has_tile) {
+            if (l > 0 && g.has_tile && 4 * sl < npos) {
                 if (ng == 8) down_round(std::integral_constant<int, 8>{}, sl);
                 else if (ng == 4) down_round(std::integral_constant<int, 4>{}, sl);
                 else down_round(std::integral_constant<int, 2>{}, sl);
@@ -903,6 +917,10 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
         }
         flag_set(&sm.f_done[wave], l + 1, lane);
         LS_STAMP(P, g, l, 11, wave == 3 && lane == 0);
+        // the rest of the next layer's loads queue behind the control wave's loads of this
+        // layer's missed rows (with a miss, a compute unit's memory pipeline full of the
+        // stream held those rows back by several microseconds)
+        flag_wait(&sm.f_mrows, l + 1, lane, P.err);
 #pragma unroll
         for (int sl = kEarlySlots; sl < kSlots; ++sl) {
             const int t = slot_t[sl];
@@ -954,7 +972,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
         const int words = P.L * (int)(sizeof(LayerPtrs) / 4);
         for (int i = threadIdx.x; i < words; i += kThreads) dst[i] = src[i];
         if (threadIdx.x == 0) {
-            sm.f_keys = sm.f_acts = sm.f_E = sm.f_pn = sm.f_out = 0;
+            sm.f_keys = sm.f_acts = sm.f_E = sm.f_pn = sm.f_out = sm.f_mrows = 0;
             for (int v = 0; v < kWaves; ++v) sm.f_done[v] = 0;
         }
         __syncthreads();
