@@ -312,8 +312,8 @@ ls_status ls_kernel_timing(ls_ffn* ctx, int32_t kernel, int32_t reset, double* t
  *    (ls_decode_step then returns LS_E_UNSUPPORTED for shapes it cannot run).
  *  LS_CFG_SPEC_BLOCKS: blocks of the next layer the fused kernel prefetches
  *    speculatively (its top-kp by scores predicted from the current layer's
- *    input, Eq. 2); 0 = automatic (k + ceil(k/5), or fewer when the kernel's
- *    neuron slots hold fewer).  Never changes results.
+ *    input, Eq. 2); 0 = automatic (k + ceil(k/4), or fewer when the kernel's
+ *    neuron slots or down positions hold fewer).  Never changes results.
  *  LS_CFG_COOPERATIVE: 1 (default) launch the fused kernel with
  *    hipLaunchCooperativeKernel, which guarantees that its one-workgroup-per-
  *    compute-unit grid is resident at once; 0 a plain launch of the same grid

@@ -1105,7 +1105,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
     if (c->desc.residency != LS_WEIGHTS_HBM)
         return fail(c, LS_E_UNSUPPORTED, "ls_decode_step needs HBM-resident weights; use the per-layer calls");
     if (c->decode_path != 1) {
-        int kp = c->spec_blocks > 0 ? c->spec_blocks : k + (k + 4) / 5;
+        int kp = c->spec_blocks > 0 ? c->spec_blocks : k + (k + 3) / 4;
         kp = std::min(kp, ls::fused_max_spec(s, c->n_wg));
         kp = std::max(kp, k);
         const ls::FusedSupport sup = ls::fused_supported(s, B, k, kp, c->n_wg, c->desc.n_layers);

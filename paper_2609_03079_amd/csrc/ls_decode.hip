@@ -524,11 +524,13 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         if (l > 0 && g.has_tile) {
             const int n = g.kp * g.blk;
             const uint64_t* row = P.amb + (size_t)l * g.AW;
-            for (int base = 0; base < n; base += 16 * 64) {
-                uint64_t v[16];
-                wait_words<16>(row + base, min(n - base, 16 * 64), g.tag, lane, P.err, v);
+            // one poll round of up to 32 words per lane (26 at the 7B shape; two rounds of 16
+            // gathered 0.3 us later)
+            for (int base = 0; base < n; base += 32 * 64) {
+                uint64_t v[32];
+                wait_words<32>(row + base, min(n - base, 32 * 64), g.tag, lane, P.err, v);
 #pragma unroll
-                for (int u = 0; u < 16; ++u) {
+                for (int u = 0; u < 32; ++u) {
                     const int i = base + u * 64 + lane;
                     if (i < n) sm.aall[i] = word_value(v[u]);
                 }
