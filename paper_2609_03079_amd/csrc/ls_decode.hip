@@ -255,10 +255,9 @@ struct Geo {
 // set is every key > T plus the elements equal to T with the smallest indices.  Members
 // are written to out[] in index order (the set is what matters to the fused step; its
 // summation order is fixed by the slot map).  Only the top BITS bits of each key take part
-// (BITS = 32: the exact order).  Needs 1 <= m <= n.
-template <int BITS>
-__device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int* out, int lane) {
-    constexpr int Q = kMaxNb / 64;
+// (BITS = 32: the exact order).  Q key slots per lane, Q * 64 >= n.  Needs 1 <= m <= n.
+template <int BITS, int Q>
+__device__ __forceinline__ void top_set_q(const uint32_t* keys, int n, int m, int* out, int lane) {
     uint32_t ok[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -291,6 +290,16 @@ __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int*
         eq_before += __popcll(eqb);
         mem_before += __popcll(memb);
     }
+}
+
+// The search's cost is its instruction count (one wave per SIMD runs it at a few cycles per
+// instruction), so it takes only as many key slots per lane as n needs: Q = 3 at n <= 192
+// ranks 20% faster than Q = 4 (1.7 against 2.1 us for the exact 32-bit search at n = 172).
+template <int BITS>
+__device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int* out, int lane) {
+    if (n <= 128) top_set_q<BITS, 2>(keys, n, m, out, lane);
+    else if (n <= 192) top_set_q<BITS, 3>(keys, n, m, out, lane);
+    else top_set_q<BITS, kMaxNb / 64>(keys, n, m, out, lane);
 }
 
 // X, one quarter per wave: words [wave*D/4, (wave+1)*D/4) of the layer input into xin (and
