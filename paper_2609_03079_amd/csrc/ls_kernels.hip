@@ -410,7 +410,9 @@ static hipError_t gateup_select_t(const Shape& s, const LayerDev& L, const float
                        L.threshold, h, s.d, s.blk, s.n_blk, s.F, scores, k, idx, count, a_buf)
 #define LS_GS_Q(RMS, U)                                     \
     do {                                                    \
-        if (s.n_blk <= 256) LS_GS_K(RMS, U, 4);             \
+        if (s.n_blk <= 128) LS_GS_K(RMS, U, 2);             \
+        else if (s.n_blk <= 192) LS_GS_K(RMS, U, 3);        \
+        else if (s.n_blk <= 256) LS_GS_K(RMS, U, 4);        \
         else LS_GS_K(RMS, U, 8);                            \
     } while (0)
 #define LS_GS_U(RMS)                                        \
@@ -550,7 +552,13 @@ hipError_t launch_select(const float* scores, int B, int n_blk, int mode, int k,
     const int max_waves = n_blk <= 512 ? 16 : 8;  // the widest body needs 256 registers a lane
     waves = waves > max_waves ? max_waves : waves;
     const int threads = 64 * waves;
-    auto fn = n_blk <= 256 ? select_kernel<4> : n_blk <= 512 ? select_kernel<8> : select_kernel<kMaxBlocks / 64>;
+    // key slots per lane: only as many as n_blk needs (the search's time follows its
+    // instruction count)
+    auto fn = n_blk <= 128   ? select_kernel<2>
+              : n_blk <= 192 ? select_kernel<3>
+              : n_blk <= 256 ? select_kernel<4>
+              : n_blk <= 512 ? select_kernel<8>
+                             : select_kernel<kMaxBlocks / 64>;
     hipLaunchKernelGGL(fn, dim3(1), dim3(threads), 0, st, scores, B, n_blk, mode, k, tau,
                        union_batch, cap, idx, count);
     return hipGetLastError();
