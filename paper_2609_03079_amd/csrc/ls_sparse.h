@@ -265,15 +265,30 @@ __device__ __forceinline__ void down_tile(
         for (int i = 0; i < B; ++i) acc[i] = 0.f;
         for (int it0 = 0; it0 < n_items; it0 += G) {
             const u32x4* src[G];
-            int ent[G], c0[G];
+            int ent[G], c0[G], bv[G];
+            // the items' list entries, then (host-resident weights) their cache slots: every load
+            // of a kind issued before the first use, entries past the list clamped to a valid one
+            // (a per-item branch had made each load wait for the one before)
+#pragma unroll
+            for (int u = 0; u < G; ++u) {
+                const int it = it0 + u;
+                bv[u] = it < n_items ? idx[begin + vw + kDnVirt * (it / npair)] : -1;
+            }
+#pragma unroll
+            for (int u = 0; u < G; ++u) bv[u] = bv[u] < n_blk ? bv[u] : -1;
+            if (slot_table) {
+#pragma unroll
+                for (int u = 0; u < G; ++u) {
+                    const int sl = slot_table[bv[u] < 0 ? 0 : bv[u]];
+                    bv[u] = bv[u] < 0 ? -1 : sl;
+                }
+            }
 #pragma unroll
             for (int u = 0; u < G; ++u) {
                 const int it = it0 + u;
                 const int j = it / npair, pr = it - j * npair;
                 const int e = begin + vw + kDnVirt * j;
-                int b = it < n_items ? idx[e] : -1;
-                if (b >= n_blk) b = -1;
-                const int slot = b < 0 ? -1 : (slot_table ? slot_table[b] : b);
+                const int slot = bv[u];
                 ent[u] = slot < 0 ? -1 : e;
                 c0[u] = lane + 128 * pr;
                 src[u] = reinterpret_cast<const u32x4*>(blocks + (size_t)(slot < 0 ? 0 : slot) * block_bytes +
