@@ -47,6 +47,10 @@ def algorithmic_bytes_per_layer(cfg, U: int, Z: int = 0) -> int:
     return s * (ffn + bias) + predictor_bytes(cfg)
 
 
+# the dominant kernel's launches are bracketed with HIP events in every this-many-th timed step
+TIMING_SAMPLE_EVERY = 8
+
+
 def measured_traffic(kernel: str, cfg, n_layers_default: bool):
     """HBM bytes per launch of `kernel` on this workload from the committed rocprofv3 counter
     summary (profiles/<kernel>_<workload>.md), or None when there is none, the workload differs,
@@ -548,9 +552,8 @@ def bench_zero_skip(args, cfg) -> int:
         f.ls_configure(lsffn.LS_CFG_ZERO_SKIP, zs)
         for i in range(W):
             f.ls_decode_step(xs[i].clone(), B, cfg.k)
-        torch.cuda.synchronize()
-        f.ls_set_kernel_timing(True)
-        f.ls_kernel_timing(0, reset=True)
+        # the rate with no events between the launches, then the kernels' times with an event
+        # pair around each launch (the pairs widen every launch gap)
         xw = [xs[W + i].clone() for i in range(K)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -558,6 +561,11 @@ def bench_zero_skip(args, cfg) -> int:
             f.ls_decode_step(xw[i], B, cfg.k)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        f.ls_set_kernel_timing(True)
+        f.ls_kernel_timing(0, reset=True)
+        for i in range(K):
+            f.ls_decode_step(xs[W + i].clone(), B, cfg.k)
+        torch.cuda.synchronize()
         f.ls_set_kernel_timing(False)
         r = {"tokens_per_s": round(B * K / wall, 2), "ms_per_step": round(1e3 * wall / K, 4)}
         for kid, name in ((lsffn.LS_K_GATEUP, "gateup"), (lsffn.LS_K_DOWN, "down")):
@@ -908,12 +916,12 @@ def main() -> int:
         f.ls_set_kernel_timing(False)
 
     # timed region: K decode steps; HIP event pairs bracket the launches of the dominant kernel
-    # (the largest share of the warm-up's time), or of every kernel without a warm-up
+    # (the largest share of the warm-up's time), or of every kernel without a warm-up, in every
+    # TIMING_SAMPLE_EVERY-th step: an event pair around a launch widens the gap before the next
+    # one (the per-kernel path at batch 1 ran about 25% slower with a pair around every gate/up
+    # launch), so the other steps run without them
     dom_name = max(per_kernel.items(), key=lambda kv: kv[1]["total_ms"])[0] if per_kernel else None
-    if dom_name:
-        f.ls_set_kernel_timing(True, kernels=[kernel_ids[dom_name]])
-    else:
-        f.ls_set_kernel_timing(True)
+    timed_ids = [kernel_ids[dom_name]] if dom_name else None
     f.ls_kernel_timing(0, reset=True)
     # R repetitions of exactly K steps, each between synchronisations; each step decodes a
     # fresh token
@@ -924,7 +932,12 @@ def main() -> int:
         t0 = time.perf_counter()
         ev0.record(stream)
         for i in range(K):
+            sample = i % TIMING_SAMPLE_EVERY == 0
+            if sample:
+                f.ls_set_kernel_timing(True, kernels=timed_ids)
             f.ls_decode_step(x_dev[W + rep * K + i], B, cfg.k)
+            if sample:
+                f.ls_set_kernel_timing(False)
         ev1.record(stream)
         torch.cuda.synchronize()
         walls.append(time.perf_counter() - t0)
