@@ -51,13 +51,30 @@ __global__ __launch_bounds__(64 * NW) void gemv_rows_kernel(const uint8_t* __res
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][b] = 0.f;
     }
+    // PRE (a few tokens): the input chunks are requested with the weights, so the products wait
+    // for one round trip; otherwise each chunk's input read is issued at its first use (the
+    // inputs of many tokens would take too many registers)
+    constexpr bool PRE = B <= 3;
+    constexpr int UX = PRE ? U : 1;
     for (int c0 = threadIdx.x; c0 < nchunk; c0 += 64 * NW * U) {
         u32x4 raw[U][R];
+        f32x4 xin[UX][PRE ? B : 1][V / 4];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * 64 * NW;
 #pragma unroll
             for (int r = 0; r < R; ++r) raw[u][r] = c < nchunk ? ld_stream(wr[r] + c) : u32x4{0u, 0u, 0u, 0u};
+        }
+        if constexpr (PRE) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int c = min(c0 + u * 64 * NW, nchunk - 1);
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+#pragma unroll
+                    for (int q = 0; q < V / 4; ++q)
+                        xin[u][b][q] = reinterpret_cast<const f32x4*>(v + (size_t)b * cols + (size_t)c * V)[q];
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -71,7 +88,7 @@ __global__ __launch_bounds__(64 * NW) void gemv_rows_kernel(const uint8_t* __res
                     const f32x4* vp = reinterpret_cast<const f32x4*>(v + (size_t)b * cols + (size_t)c * V);
 #pragma unroll
                     for (int q = 0; q < V / 4; ++q) {
-                        const f32x4 x4 = vp[q];
+                        const f32x4 x4 = PRE ? xin[PRE ? u : 0][PRE ? b : 0][q] : vp[q];
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             acc[r][b] = fmaf(w[r][4 * q + 0], x4.x, acc[r][b]);
