@@ -51,10 +51,11 @@ __global__ __launch_bounds__(64 * NW) void gemv_rows_kernel(const uint8_t* __res
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][b] = 0.f;
     }
-    // PRE (a few tokens): the input chunks are requested with the weights, so the products wait
-    // for one round trip; otherwise each chunk's input read is issued at its first use (the
-    // inputs of many tokens would take too many registers)
-    constexpr bool PRE = B <= 3;
+    // PRE (up to 3 tokens): the input chunks are requested with the weights, so the products
+    // wait for one round trip; otherwise each chunk's input read is issued at its first use
+    // (measured at 8 tokens, requesting them early was slower: 2260 against 2272 tokens/s on
+    // the 13B shape), and so it is where they would take more than 32 registers of 16 bytes
+    constexpr bool PRE = B <= 3 && U * B * (V / 4) <= 32;
     constexpr int UX = PRE ? U : 1;
     for (int c0 = threadIdx.x; c0 < nchunk; c0 += 64 * NW * U) {
         u32x4 raw[U][R];
