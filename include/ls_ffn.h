@@ -157,7 +157,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int3
 /* For callers that cannot allocate memory (code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc): ls_sparse_ffn_step with the
  * same arguments, kernels and results, whose scratch (the activations
- * [B, d_ff] and the split down projection's parts [4, B, d_model], fp32) lives
+ * [B, d_ff] and the split down projection's parts [8, B, d_model], fp32) lives
  * in a fixed device array of LS_STATIC_SCRATCH_BYTES that the library defines
  * instead of in the context's workspace.  Each GPU holds its own copy of that
  * array from the first ls_ffn_create on it until the process ends.  The call
@@ -166,7 +166,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* ctx, int32_t layer, const float* x_in, int3
  * earlier in the same call), but every call on one GPU shares the array and it
  * keeps the last call's contents: calls that overlap on one GPU (other streams,
  * other contexts, other host threads) race, so the caller must order them.
- * LS_E_CAPACITY if B * (d_ff + 4 d_model) floats exceed the array; otherwise
+ * LS_E_CAPACITY if B * (d_ff + 8 d_model) floats exceed the array; otherwise
  * the errors of ls_sparse_ffn_step.  ls_debug_last_activations then reads the
  * activations from the array. */
 #define LS_STATIC_SCRATCH_BYTES (4u << 20)

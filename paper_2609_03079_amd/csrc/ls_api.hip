@@ -43,7 +43,7 @@ struct ls_ffn {
     int32_t* count = nullptr; // [maxB]
     float* a = nullptr;       // [maxB, F]
     float* xbuf = nullptr;    // [maxB, d]  ping-pong partner of the decode step
-    float* dn_part = nullptr; // [kDownSplits, maxB, d]  parts of the split down projection
+    float* dn_part = nullptr; // [kDownPartsMax, maxB, d]  parts of the split down projection
     int64_t last_act_n = 0;
     int32_t last_act_B = 0;
     const float* last_act_src = nullptr;  // activations buffer of the last sparse step
@@ -471,7 +471,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
         dmalloc(&c->scores, (size_t)B * s.n_blk) != hipSuccess ||
         dmalloc(&c->idx, (size_t)B * s.n_blk) != hipSuccess || dmalloc(&c->count, (size_t)B) != hipSuccess ||
         dmalloc(&c->a, (size_t)B * s.F) != hipSuccess || dmalloc(&c->xbuf, (size_t)B * s.d) != hipSuccess ||
-        dmalloc(&c->dn_part, (size_t)ls::kDownSplits * B * s.d) != hipSuccess) {
+        dmalloc(&c->dn_part, (size_t)ls::kDownPartsMax * B * s.d) != hipSuccess) {
         (void)hipGetLastError();
         return bail(LS_E_NOMEM, "workspace allocation failed");
     }
@@ -658,7 +658,7 @@ static ls_status wait_stages(ls_ffn* c, int32_t layer, int32_t begin, int32_t en
 }
 
 // The sparse step over [begin, end) of the list with the given scratch: a_buf [B, F]
-// activations, part [kDownSplits, B, d] parts of the split down projection.
+// activations, part [kDownPartsMax, B, d] parts of the split down projection.
 // may_time: bracket the launches with timing events when kernel timing is on (taking an
 // event can create one); false launches them bare.
 static ls_status sparse_step(ls_ffn* c, int32_t layer, const float* x_in, int32_t B, const int32_t* idx,
@@ -712,7 +712,7 @@ ls_status ls_sparse_ffn_step(ls_ffn* c, int32_t layer, const float* x_in, int32_
 
 // ---- the sparse step without allocation -------------------------------------------------
 // A fixed device array holds the scratch of ls_sparse_ffn_step_static (activations [B, F],
-// then the split down projection's parts [kDownSplits, B, d]).  Each GPU the library runs on
+// then the split down projection's parts [kDownPartsMax, B, d]).  Each GPU the library runs on
 // holds its own copy until the process ends.  In host code `scratch` names a host-side
 // stand-in, not device memory: its device address is resolved once per device, with that
 // device current, by ls_ffn_create, and only that address is handed to kernels.
@@ -749,9 +749,9 @@ ls_status ls_sparse_ffn_step_static(ls_ffn* c, int32_t layer, const float* x_in,
     if (st != LS_OK) return st;
     const Shape& s = c->shape;
     if (B < 1 || B > c->desc.max_batch) return fail(c, LS_E_INVAL, "B out of range");
-    const size_t need = (size_t)B * s.F + (size_t)ls::kDownSplits * B * s.d;
+    const size_t need = (size_t)B * s.F + (size_t)ls::kDownPartsMax * B * s.d;
     if (need > kScratchFloats)
-        return fail(c, LS_E_CAPACITY, "B * (d_ff + 4 * d_model) floats exceed the static scratch (LS_STATIC_SCRATCH_BYTES)");
+        return fail(c, LS_E_CAPACITY, "B * (d_ff + 8 * d_model) floats exceed the static scratch (LS_STATIC_SCRATCH_BYTES)");
     float* base = scratch_ptr(c->device);
     if (!base) return fail(c, LS_E_STATE, "static scratch of this device was not resolved");
     return sparse_step(c, layer, x_in, B, idx, count, begin, end, x_acc, base, base + (size_t)B * s.F, false);

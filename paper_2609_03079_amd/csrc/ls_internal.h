@@ -97,7 +97,7 @@ hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_
 bool gateup_select_ok(const Shape& s, int B, int k);
 hipError_t launch_gateup_select(const Shape& s, const LayerDev& L, const float* x, const float* scores, int k,
                                 int32_t* idx, int32_t* count, float* a_buf, hipStream_t st);
-// part: [kDownSplits, B, d] floats of scratch for the matrix-core path's split list (may be
+// part: [kDownPartsMax, B, d] floats of scratch for the matrix-core path's split list (may be
 // null: no split)
 hipError_t launch_down(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                        const float* a_buf, int B, const int32_t* idx, const int32_t* count,
@@ -139,7 +139,14 @@ bool mfma_path(const Shape& s, int B);
 hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                               const float* x, int B, const int32_t* idx, const int32_t* count,
                               int begin, int end, float* a_buf, hipStream_t st);
-constexpr int kDownSplits = 4;  // list parts of the matrix-core down projection (divides 16)
+constexpr int kDownPartsMax = 8;  // list parts of the matrix-core down projection, at most
+// Layout of the matrix-core down projection: nt adjacent 16-column tiles per workgroup, the
+// list cut into `splits` parts (partial sums in the part buffer, added by a finish kernel),
+// `waves` waves per workgroup.
+struct DownLayout {
+    int nt, splits, waves;
+};
+DownLayout down_layout(const Shape& s, int B);
 hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
                             const float* a_buf, int B, const int32_t* idx, const int32_t* count,
                             int begin, int end, const float* x_in, float* x_acc, float* part,

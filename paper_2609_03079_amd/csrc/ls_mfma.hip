@@ -243,14 +243,19 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGu
     }
 }
 
-// One workgroup per 16-column tile of y and part of the list; its waves split that part's
-// entries.  The down piece of a block for one tile is [blk/8][16][8]: K step s of an entry
-// is the contiguous kilobyte of chunks 64 s .. 64 s + 63, exactly one A fragment.
+// One workgroup per NT adjacent 16-column tiles of y and part of the list; its waves split
+// that part's entries.  The down piece of a block for one 16-column tile is [blk/8][16][8]:
+// K step s of an entry is the contiguous kilobyte of chunks 64 s .. 64 s + 63, exactly one A
+// fragment, and the pieces of adjacent tiles are adjacent.  A wave loads the activations of
+// a work item once for its NT fragments: every workgroup reads the whole part's activations
+// (L2 hits, but through the same per-CU memory path as the weights, which bounds these
+// kernels), so NT tiles per workgroup divide those reads by NT.
 // With splits > 1 the list range is cut into `splits` equal parts (workgroup
 // tile + n_tiles * part) so that the workgroup count is a multiple of the CU count even when
 // the tile count is not; each part's sum goes to part_out[part][token][column] and
-// down_finish_kernel adds the parts in order.  The wave count is blockDim.x / 64.
-template <ls_dtype T>
+// down_finish_kernel adds the parts in order.  The wave count is blockDim.x / 64 (at most
+// kWavesDn, and at most kWavesDn / NT with NT > 1).
+template <ls_dtype T, int NT>
 __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int B, int F, int d, int blk, int n_blk,
@@ -258,14 +263,16 @@ __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const float* __restrict__ x_in, float* __restrict__ x_acc, int splits,
     float* __restrict__ part_out) {
     using S = Split<T>;
-    const int n_tiles = d / kColTile;
+    constexpr int kU = kUnrollDn;  // items in flight per wave
+    const int n_tiles = d / (kColTile * NT);
     const int tile = (int)blockIdx.x % n_tiles, sp = (int)blockIdx.x / n_tiles;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int n_waves = (int)(blockDim.x >> 6);
     const int len = max(0, list_end_m(count, end, n_blk) - begin);
     const int e0 = begin + (int)((long)len * sp / splits);
     const int e1 = begin + (int)((long)len * (sp + 1) / splits);
-    const size_t down_off = (size_t)2 * blk * d * 2 + (size_t)tile * blk * kColTile * 2;
+    const size_t down_off = (size_t)2 * blk * d * 2 + (size_t)tile * NT * blk * kColTile * 2;
+    const int piece_v = blk * kColTile * 2 / 16;  // 16-byte vectors of one tile's piece
     const int ksteps = blk / 32;
     const int tok = lane & 15;
     const bool tok_ok = tok < B;
@@ -277,16 +284,18 @@ __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
         slots[e - e0] = (b < 0 || b >= n_blk) ? -1 : (slot_table ? slot_table[b] : b);
     }
     __syncthreads();
-    f32x4v c = {0.f, 0.f, 0.f, 0.f};
-    // work items (entry, K step) of the part, dealt to the waves round-robin; kUnrollDn items
-    // per wave are in flight together
-    const long items = (long)(e1 - e0) * ksteps;
-    for (long i0 = wave; i0 < items; i0 += (long)n_waves * kUnrollDn) {
-        const u32x4* src[kUnrollDn];
-        const float* arow[kUnrollDn];
-        bool live[kUnrollDn];
+    f32x4v c[NT];
 #pragma unroll
-        for (int u = 0; u < kUnrollDn; ++u) {
+    for (int j = 0; j < NT; ++j) c[j] = f32x4v{0.f, 0.f, 0.f, 0.f};
+    // work items (entry, K step) of the part, dealt to the waves round-robin; kU items per
+    // wave are in flight together
+    const long items = (long)(e1 - e0) * ksteps;
+    for (long i0 = wave; i0 < items; i0 += (long)n_waves * kU) {
+        const u32x4* src[kU];
+        const float* arow[kU];
+        bool live[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
             const long it = i0 + (long)n_waves * u;
             const int e = e0 + (int)(it / ksteps), s = (int)(it % ksteps);
             live[u] = it < items;
@@ -296,36 +305,42 @@ __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
                                                     down_off) + 64 * s + lane;
             arow[u] = a_buf + (size_t)(tok_ok ? tok : 0) * F + (size_t)e * blk + 32 * s + 8 * (lane >> 4);
         }
-        u32x4 w[kUnrollDn];
-        f32x4 av[kUnrollDn][2];
+        u32x4 w[kU][NT];
+        f32x4 av[kU][2];
 #pragma unroll
-        for (int u = 0; u < kUnrollDn; ++u) {
+        for (int u = 0; u < kU; ++u) {
             const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-            w[u] = live[u] ? ld_stream(src[u]) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < NT; ++j) w[u][j] = live[u] ? ld_stream(src[u] + j * piece_v) : u32x4{0u, 0u, 0u, 0u};
             av[u][0] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[0] : z;
             av[u][1] = live[u] && tok_ok ? reinterpret_cast<const f32x4*>(arow[u])[1] : z;
         }
 #pragma unroll
-        for (int u = 0; u < kUnrollDn; ++u) {
+        for (int u = 0; u < kU; ++u) {
             const float xv[8] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w,
                                  av[u][1].x, av[u][1].y, av[u][1].z, av[u][1].w};
             typename S::vec hi, lo;
             S::run(xv, hi, lo);
-            const typename S::vec wv = S::from_raw(w[u]);
-            c = S::mfma(wv, hi, c);
-            c = S::mfma(wv, lo, c);
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const typename S::vec wv = S::from_raw(w[u][j]);
+                c[j] = S::mfma(wv, hi, c[j]);
+                c[j] = S::mfma(wv, lo, c[j]);
+            }
         }
     }
-    // lane l holds columns 4 (l / 16) + i of the tile for token l % 16
-    __shared__ float part[kWavesDn][16][16];
+    // lane l holds columns 4 (l / 16) + i of tile j for token l % 16
+    __shared__ float part[NT == 1 ? kWavesDn : kWavesDn / NT][NT][16][16];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) part[wave][4 * (lane >> 4) + i][lane & 15] = c[i];
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) part[wave][j][4 * (lane >> 4) + i][lane & 15] = c[j][i];
     __syncthreads();
-    if (threadIdx.x < 16 * B) {
-        const int t = threadIdx.x / 16, col = threadIdx.x % 16;
+    for (int q = (int)threadIdx.x; q < NT * 16 * B; q += (int)blockDim.x) {
+        const int j = q / (16 * B), t = (q / 16) % B, col = q % 16;
         float y = 0.f;
-        for (int w = 0; w < n_waves; ++w) y += part[w][col][t];
-        const size_t m = (size_t)t * d + (size_t)tile * kColTile + col;
+        for (int w = 0; w < n_waves; ++w) y += part[w][j][col][t];
+        const size_t m = (size_t)t * d + (size_t)(tile * NT + j) * kColTile + col;
         if (splits == 1)
             x_acc[m] = (begin == 0 ? x_in[m] : x_acc[m]) + y;
         else
@@ -382,13 +397,20 @@ hipError_t launch_gateup_mfma(const Shape& s, const LayerDev& L, const int32_t* 
     return hipGetLastError();
 }
 
-int down_splits(const Shape& s) {
-    // tiles that do not fill whole rounds of the CUs: cut the list in kDownSplits parts
+DownLayout down_layout(const Shape& s, int B) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-        return 1;
-    return (s.d / kColTile) % cus == 0 ? 1 : kDownSplits;
+        cus = 256;
+    // Chosen from launch times over list lengths on the three model shapes (B = 4 and 8):
+    // 32 columns per workgroup wherever the activation reads are a large share of a
+    // workgroup's bytes; tiles that do not fill whole rounds of the CUs (d = 5120) and 128-row
+    // blocks (one block's piece of a tile is 4 KB) take 8 list parts of 4 waves; 64-row blocks
+    // at d = 4096 take 2 parts of 8 waves at B = 8 and one 16-column tile per workgroup, no
+    // parts, below.
+    if ((s.d / kColTile) % cus != 0 || s.blk >= 128) return DownLayout{2, 8, 4};
+    if (B >= 8 && (s.d / (2 * kColTile)) * 2 % cus == 0) return DownLayout{2, 2, 8};
+    return DownLayout{1, 1, kWavesDn};
 }
 
 hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* slot_table,
@@ -396,21 +418,29 @@ hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* sl
                             int begin, int end, const float* x_in, float* x_acc, float* part,
                             hipStream_t st) {
     const size_t bb = s.block_elems * elem_size(s.dtype);
-    const int splits = part ? down_splits(s) : 1;
-    // the same number of waves per tile either way: 16 in one workgroup or 16 / splits in each
-    const dim3 grid((unsigned)(s.d / kColTile * splits)), blk(64 * kWavesDn / splits);
+    DownLayout lay = down_layout(s, B);
+    if (!part) lay = DownLayout{1, 1, kWavesDn};
+    const dim3 grid((unsigned)(s.d / (kColTile * lay.nt) * lay.splits)), blk(64 * lay.waves);
+#define LS_DNM(TT, NT)                                                                                  \
+    hipLaunchKernelGGL((down_mfma_kernel<TT, NT>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, B, \
+                       s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, lay.splits, part)
+#define LS_DNT(TT)                          \
+    do {                                    \
+        if (lay.nt == 1) LS_DNM(TT, 1);     \
+        else LS_DNM(TT, 2);                 \
+    } while (0)
     if (s.dtype == LS_F16)
-        hipLaunchKernelGGL(down_mfma_kernel<LS_F16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
-                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, splits, part);
+        LS_DNT(LS_F16);
     else if (s.dtype == LS_BF16)
-        hipLaunchKernelGGL(down_mfma_kernel<LS_BF16>, grid, blk, 0, st, L.blocks, bb, slot_table, a_buf,
-                           B, s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, splits, part);
+        LS_DNT(LS_BF16);
     else
         return hipErrorInvalidValue;
+#undef LS_DNT
+#undef LS_DNM
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || splits == 1) return e;
+    if (e != hipSuccess || lay.splits == 1) return e;
     const int n = B * s.d;
-    hipLaunchKernelGGL(down_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, splits, n,
+    hipLaunchKernelGGL(down_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, lay.splits, n,
                        x_in, x_acc, begin == 0 ? 1 : 0);
     return hipGetLastError();
 }

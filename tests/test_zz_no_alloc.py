@@ -63,7 +63,7 @@ def test_static_scratch_step_equals_the_allocating_step(name):
 
 
 def test_static_scratch_refuses_an_oversized_request():
-    # B * (d_ff + 4 d_model) = 4 * (262144 + 256) floats > the 4 MiB array
+    # B * (d_ff + 8 d_model) = 4 * (262144 + 512) floats > the 4 MiB array
     f = lsffn.Ffn(n_layers=1, d_model=64, d_ff=262144, block=128, rank=64, max_batch=4,
                   dtype=lsffn.LS_F16)
     x = empty_f32(4, 64)
