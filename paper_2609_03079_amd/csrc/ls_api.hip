@@ -484,6 +484,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             return bail(LS_E_NOMEM, "fused-kernel workspace allocation failed");
         }
         if (hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)) != hipSuccess ||
+            hipMemset(c->mailbox, 0xff, ls::fused_input_words(s, L) * sizeof(uint64_t)) != hipSuccess ||
             hipMemset(c->dev_err, 0, sizeof(int)) != hipSuccess ||
             hipMemset(c->layer_tab, 0, (size_t)L * sizeof(ls::LayerPtrs)) != hipSuccess)
             return bail(LS_E_DEVICE, "workspace initialisation failed");
@@ -1113,6 +1114,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             if (c->epoch == 0xffffffffu) {  // epoch tags wrap: clear the mailboxes first
                 LS_HIP(c, hipStreamSynchronize(c->stream));
                 LS_HIP(c, hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)));
+                LS_HIP(c, hipMemset(c->mailbox, 0xff, ls::fused_input_words(s, c->desc.n_layers) * sizeof(uint64_t)));
                 c->epoch = 0;
             }
             ls::FusedArgs a{};
@@ -1258,7 +1260,10 @@ ls_status ls_debug_decode_trace(ls_ffn* c, int32_t layer, float* x_in, float* sc
     const uint64_t* smb = xmb + L * s.d;
     if (x_in) {
         if (layer == 0) return fail(c, LS_E_INVAL, "layer 0 input is the caller's own x");
-        LS_HIP(c, ls::launch_untag(xmb + (size_t)layer * s.d, s.d, 1, x_in, c->stream));
+        // the last launch's half of the input rows: bare fp32 words
+        const float* rows = reinterpret_cast<const float*>(c->mailbox) + (size_t)(c->epoch & 1u) * L * s.d;
+        LS_HIP(c, hipMemcpyAsync(x_in, rows + (size_t)layer * s.d, (size_t)s.d * sizeof(float),
+                                 hipMemcpyDeviceToDevice, c->stream));
     }
     if (scores)
         LS_HIP(c, ls::launch_untag(smb + (size_t)layer * ls::fused_score_words(s), s.n_blk, ls::kScoreStride, scores, c->stream));

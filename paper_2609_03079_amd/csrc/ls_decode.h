@@ -19,7 +19,8 @@ struct FusedArgs {
     int L, d, nb, blk, F, k, kp, prenorm;
     size_t block_bytes;
     float* x;                 // [d]: input at entry, output at exit
-    uint64_t* xmb;            // [L][d]      tagged x of every layer input (row 0: the input,
+    uint64_t* xmb;            // [L][d]      as 2 x [L][d] 32-bit words: the layer inputs of
+                              //             launches with even / odd tag (row 0: the input,
                               //             unused when L >= 2: layer 0 then reads x itself)
     uint64_t* smb;            // [L][2 n_blk] tagged scores (exact | speculative)
     uint64_t* amb;            // [L][2F]     tagged activations: list positions, then misses
@@ -41,14 +42,17 @@ FusedSupport fused_supported(const Shape& s, int B, int k, int kp, int n_wg, int
 // Largest speculative width (blocks prefetched for the next layer) the fused kernel holds.
 int fused_max_spec(const Shape& s, int n_wg);
 
-// Mailbox layout of the fused kernel: per layer, the input x (d words; workgroup w writes its
-// 16-column tile, one 128-byte line), then the scores (kScoreStride words per workgroup, a
+// Mailbox layout of the fused kernel: the layer inputs (L * d 64-bit words, used as two halves
+// of [L][d] bare 32-bit words selected by the parity of the launch's tag, each word 0xffffffff
+// until published; workgroup w writes its 16-column tile of a row, one 64-byte line), then per
+// layer the scores (kScoreStride words per workgroup, a
 // 64-byte line of its own: exact at +0, speculative at +1; when many workgroups write into
 // one line the exchange takes about twice as long), then the activations in list order
 // (kp*blk words, then k*blk for the misses; at most F + F).
 constexpr int kScoreStride = 8;
 __host__ __device__ inline size_t fused_score_words_n(int n_blk) { return (size_t)n_blk * kScoreStride; }
 inline size_t fused_score_words(const Shape& s) { return fused_score_words_n(s.n_blk); }
+inline size_t fused_input_words(const Shape& s, int L) { return (size_t)L * s.d; }
 inline size_t fused_mailbox_words(const Shape& s, int L, int /*n_wg*/) {
     return (size_t)L * ((size_t)s.d + fused_score_words(s) + 2 * (size_t)s.F);
 }

@@ -19,9 +19,15 @@
 // Cross-workgroup exchange: every published value is one 64-bit word
 // (launch epoch << 32 | fp32 bits) written and read with agent-scope relaxed
 // atomics, which are coherent across the XCDs without cache maintenance; a
-// reader spins on the word until its epoch matches.  Each layer has its own
-// mailbox rows, so no value is overwritten within a launch.  Every wait is
-// bounded: on timeout an error flag is set and the kernel runs to completion.
+// reader spins on the word until its epoch matches.  The layer inputs, the largest
+// exchange (every workgroup reads all d values of every layer), travel as bare 32-bit
+// words instead, so a poll moves half the bytes: each launch uses one of two halves of
+// the input rows (by the parity of its epoch), where an empty word holds a pattern no
+// published value has (NaNs are published in their canonical form), and every
+// workgroup empties its tile of the other half as it publishes, for the next launch.
+// Each layer has its own mailbox rows, so no value is overwritten within a launch.
+// Every wait is bounded: on timeout an error flag is set and the kernel runs to
+// completion.
 //
 // The predictor runs in its folded form Pf = P2 P1 (fp32 [n_blk, d], Sec. 3.3.3 with the
 // projection and the head applied as one matrix), so a layer needs three exchanges.
@@ -66,6 +72,7 @@ constexpr int kMaxSRows = 1;            // folded predictor rows (block scores) 
 constexpr int kPfPer = (kMaxD / 4 + kWL - 1) / kWL;  // 16-byte chunks of one row per worker lane
 constexpr int kMaxLayers = 128;
 constexpr unsigned kSpinLimit = 1u << 18;  // ~0.3 s of polling per wait
+constexpr uint32_t kXEmpty = 0xffffffffu;  // an input word not yet published
 
 // Phase stamp of the traced workgroup (tracing aid; off when P.trace is null).
 #define LS_STAMP(P, g, l, pt, cond)                                                     \
@@ -164,6 +171,32 @@ __device__ __forceinline__ void wait_gather_off(const uint64_t* base, Off off, i
 }
 
 __device__ __forceinline__ float word_value(uint64_t w) { return __uint_as_float((uint32_t)w); }
+
+// Layer-input rows of the launch with epoch `tag` (half tag & 1 of the input region, [L][d]
+// 32-bit words), and the bits published for v (canonical NaN, never kXEmpty).
+__device__ __forceinline__ uint32_t* x_rows(const FusedArgs& P, uint32_t tag) {
+    return reinterpret_cast<uint32_t*>(P.xmb) + (size_t)(tag & 1u) * P.L * P.d;
+}
+__device__ __forceinline__ uint32_t x_bits(float v) { return v != v ? 0x7fc00000u : __float_as_uint(v); }
+
+// Wait until the W * 64 input words src[u * 64 + lane] are all published (v[u] their bits).
+template <int W>
+__device__ __forceinline__ void wait_x(const uint32_t* src, int lane, int* err, uint32_t (&v)[W]) {
+    for (unsigned spins = 0;; ++spins) {
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            v[u] = __hip_atomic_load(src + u * 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bool done = true;
+#pragma unroll
+        for (int u = 0; u < W; ++u) done &= v[u] != kXEmpty;
+        if (__all(done)) break;
+        if (spins > kSpinLimit) {
+            if (lane == 0) atomicOr(err, 1);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
 
 // Flags between the waves of one workgroup, in LDS: the writer's earlier LDS stores are
 // visible to a reader that saw the flag reach v.  Waits are bounded like the mailbox waits.
@@ -308,7 +341,7 @@ __device__ __forceinline__ void top_set(const uint32_t* keys, int n, int m, int*
 // safe because the output goes into x only at the last layer.  No workgroup gets past layer
 // 1's input before every workgroup has finished its layer-0 gather: that gather precedes
 // the workgroup's own layer-0 output tile, which every layer-1 gather waits for.  With one
-// layer, a small kernel first tags x into the mailbox row 0.
+// layer, a small kernel first writes x into the input row 0.
 template <int D>
 __device__ __forceinline__ void gather_input(const FusedArgs& P, Smem& sm, const Geo& g, int l, int wave,
                                              int lane) {
@@ -319,10 +352,10 @@ __device__ __forceinline__ void gather_input(const FusedArgs& P, Smem& sm, const
 #pragma unroll
         for (int u = 0; u < W; ++u) xv[u] = P.x[wave * Q + u * 64 + lane];
     } else {
-        uint64_t v[W];
-        wait_words<W>(P.xmb + (size_t)l * D + wave * Q, Q, g.tag, lane, P.err, v);
+        uint32_t v[W];
+        wait_x<W>(x_rows(P, g.tag) + (size_t)l * D + wave * Q, lane, P.err, v);
 #pragma unroll
-        for (int u = 0; u < W; ++u) xv[u] = word_value(v[u]);
+        for (int u = 0; u < W; ++u) xv[u] = __uint_as_float(v[u]);
     }
     float ss = 0.f;
 #pragma unroll
@@ -625,8 +658,14 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
             y += __shfl_xor(y, 32, 64);
             const float xn = sm.xt[col] + y;
             if (lane < kColTile) {
-                if (last) P.x[g.w * kColTile + lane] = xn;
-                else mb_store(P.xmb + (size_t)(l + 1) * D + g.w * kColTile + lane, g.tag, xn);
+                if (last) {
+                    P.x[g.w * kColTile + lane] = xn;
+                } else {
+                    const size_t o = (size_t)(l + 1) * D + g.w * kColTile + lane;
+                    __hip_atomic_store(x_rows(P, g.tag) + o, x_bits(xn), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    // the next launch's half: emptied here, read only after this launch ends
+                    __hip_atomic_store(x_rows(P, g.tag + 1u) + o, kXEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
             }
         }
         flag_set(&sm.f_out, l + 1, lane);  // the output store is issued: the workers may queue loads
@@ -993,9 +1032,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
 }
 
 // The layer-0 input as tagged mailbox words (launched before the fused kernel).
-__global__ void tag_input_kernel(const float* __restrict__ x, int n, uint32_t tag, uint64_t* __restrict__ dst) {
+__global__ void tag_input_kernel(const float* __restrict__ x, int n, uint32_t* __restrict__ dst) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) dst[i] = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(x[i]);
+    if (i < n) dst[i] = x_bits(x[i]);
 }
 
 template <ls_dtype T, ls_act A>
@@ -1007,7 +1046,9 @@ hipError_t launch_t(const Shape& s, const FusedArgs& a, int n_wg, bool coop, hip
     else if (nc == 8) fn = reinterpret_cast<void*>(decode_fused_kernel<T, A, 8>);
     else return hipErrorNotSupported;
     if (a.L < 2) {  // with two or more layers, layer 0 reads x itself
-        hipLaunchKernelGGL(tag_input_kernel, dim3((s.d + 255) / 256), dim3(256), 0, st, a.x, s.d, a.tag, a.xmb);
+        // row 0 of this launch's input half (one layer: L * d = d words per half)
+        uint32_t* row0 = reinterpret_cast<uint32_t*>(a.xmb) + (size_t)(a.tag & 1u) * a.L * s.d;
+        hipLaunchKernelGGL(tag_input_kernel, dim3((s.d + 255) / 256), dim3(256), 0, st, a.x, s.d, row0);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
