@@ -284,8 +284,11 @@ ls_status ls_debug_stages_done(ls_ffn* ctx, int32_t layer, int32_t* n_done);
 ls_status ls_decode_step(ls_ffn* ctx, float* x, int32_t B, int32_t k);
 
 /* Debug: copy the activations a [B, n_sel * block] (fp32, priority-list order)
- * of the most recent ls_sparse_ffn_step into dst (dev).  LS_E_INVAL if cap is
- * smaller than what the last step produced; *n_out receives n_sel * block. */
+ * of the most recent ls_sparse_ffn_step into dst (dev), n_sel = that step's
+ * end.  Positions at or past the list's device count (*count) are not written
+ * by the step: they hold whatever the activation buffer held before.
+ * LS_E_INVAL if cap is smaller than what the last step produced; *n_out
+ * receives n_sel * block. */
 ls_status ls_debug_last_activations(ls_ffn* ctx, float* dst, int64_t cap, int64_t* n_out);
 
 /* Per-kernel timing (tracing aid).  While enabled, every kernel launch the

@@ -76,9 +76,10 @@ def test_zero_skip_equals_block_path(name, B):
         f.ls_select_blocks(scores, B, lsffn.LS_SEL_TOPK, cfg.k, 0.0, 1, cap, idx, cnt)
         (y0, y1), (a0, a1) = _both(f, l, x_in, B, idx, cnt, 0, cap, cfg.d_model, cfg.d_ff)
         assert np.array_equal(y0, y1), (name, B, l)
-        assert np.array_equal(a0, a1), (name, B, l)
+        # the union list has U <= cap entries: positions past it are not written by either step
         U = int(host(cnt)[0])
         a = a1.reshape(B, -1)[:, :U * cfg.block]
+        assert np.array_equal(a0.reshape(B, -1)[:, :U * cfg.block], a), (name, B, l)
         skipped += int((~(a != 0).any(axis=0)).sum())
         if cfg.act == lsgen.ACT_REGLU:
             blocks = host(idx)[:U]
