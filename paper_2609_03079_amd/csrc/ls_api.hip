@@ -332,6 +332,17 @@ hipError_t dmalloc(T** p, size_t n) {
     return hipMalloc(reinterpret_cast<void**>(p), std::max<size_t>(n, 1) * sizeof(T));
 }
 
+// The fused kernel's bare 32-bit exchange words start empty (0xffffffff): the layer inputs
+// and, in every layer's activation row, the list's two halves (its first F 64-bit words).
+hipError_t empty_bare_words(ls_ffn* c) {
+    const ls::Shape& s = c->shape;
+    const int L = c->desc.n_layers;
+    hipError_t e = hipMemset(c->mailbox, 0xff, ls::fused_input_words(s, L) * sizeof(uint64_t));
+    if (e != hipSuccess) return e;
+    return hipMemset2D(c->mailbox + ls::fused_acts_offset(s, L), 2 * (size_t)s.F * sizeof(uint64_t), 0xff,
+                       (size_t)s.F * sizeof(uint64_t), (size_t)L);
+}
+
 }  // namespace
 
 extern "C" {
@@ -484,7 +495,7 @@ ls_status ls_ffn_create(const ls_ffn_desc* desc, ls_ffn** out) {
             return bail(LS_E_NOMEM, "fused-kernel workspace allocation failed");
         }
         if (hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)) != hipSuccess ||
-            hipMemset(c->mailbox, 0xff, ls::fused_input_words(s, L) * sizeof(uint64_t)) != hipSuccess ||
+            empty_bare_words(c) != hipSuccess ||
             hipMemset(c->dev_err, 0, sizeof(int)) != hipSuccess ||
             hipMemset(c->layer_tab, 0, (size_t)L * sizeof(ls::LayerPtrs)) != hipSuccess)
             return bail(LS_E_DEVICE, "workspace initialisation failed");
@@ -1114,7 +1125,7 @@ ls_status ls_decode_step(ls_ffn* c, float* x, int32_t B, int32_t k) {
             if (c->epoch == 0xffffffffu) {  // epoch tags wrap: clear the mailboxes first
                 LS_HIP(c, hipStreamSynchronize(c->stream));
                 LS_HIP(c, hipMemset(c->mailbox, 0, c->mailbox_words * sizeof(uint64_t)));
-                LS_HIP(c, hipMemset(c->mailbox, 0xff, ls::fused_input_words(s, c->desc.n_layers) * sizeof(uint64_t)));
+                LS_HIP(c, empty_bare_words(c));
                 c->epoch = 0;
             }
             ls::FusedArgs a{};

@@ -47,12 +47,15 @@ int fused_max_spec(const Shape& s, int n_wg);
 // until published; workgroup w writes its 16-column tile of a row, one 64-byte line), then per
 // layer the scores (kScoreStride words per workgroup, a
 // 64-byte line of its own: exact at +0, speculative at +1; when many workgroups write into
-// one line the exchange takes about twice as long), then the activations in list order
-// (kp*blk words, then k*blk for the misses; at most F + F).
+// one line the exchange takes about twice as long), then per layer 2F words of activations:
+// the list's activations in list order as two halves of F bare 32-bit words (by the tag's
+// parity, each word 0xffffffff until published, as for the inputs), then the misses' tagged
+// words (k*blk <= F).
 constexpr int kScoreStride = 8;
 __host__ __device__ inline size_t fused_score_words_n(int n_blk) { return (size_t)n_blk * kScoreStride; }
 inline size_t fused_score_words(const Shape& s) { return fused_score_words_n(s.n_blk); }
 inline size_t fused_input_words(const Shape& s, int L) { return (size_t)L * s.d; }
+inline size_t fused_acts_offset(const Shape& s, int L) { return (size_t)L * (s.d + fused_score_words(s)); }
 inline size_t fused_mailbox_words(const Shape& s, int L, int /*n_wg*/) {
     return (size_t)L * ((size_t)s.d + fused_score_words(s) + 2 * (size_t)s.F);
 }

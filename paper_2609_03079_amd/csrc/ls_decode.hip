@@ -179,13 +179,22 @@ __device__ __forceinline__ uint32_t* x_rows(const FusedArgs& P, uint32_t tag) {
 }
 __device__ __forceinline__ uint32_t x_bits(float v) { return v != v ? 0x7fc00000u : __float_as_uint(v); }
 
-// Wait until the W * 64 input words src[u * 64 + lane] are all published (v[u] their bits).
+// List activations of layer l of the launch with epoch `tag`: half tag & 1 of the first F
+// 64-bit words of the layer's activation row, as F bare 32-bit words (the misses follow,
+// tagged, at word F of the row).
+__device__ __forceinline__ uint32_t* acts_rows(const FusedArgs& P, int AW, int F, int l, uint32_t tag) {
+    return reinterpret_cast<uint32_t*>(P.amb + (size_t)l * AW) + (size_t)(tag & 1u) * F;
+}
+
+// Wait until the bare words src[0..n) are all published: lane holds word u * 64 + lane in v[u]
+// (u < W, W * 64 >= n; indices past n read the last word and are ignored).
 template <int W>
-__device__ __forceinline__ void wait_x(const uint32_t* src, int lane, int* err, uint32_t (&v)[W]) {
+__device__ __forceinline__ void wait_x(const uint32_t* src, int n, int lane, int* err, uint32_t (&v)[W]) {
+    const int last = n - 1;
     for (unsigned spins = 0;; ++spins) {
 #pragma unroll
         for (int u = 0; u < W; ++u)
-            v[u] = __hip_atomic_load(src + u * 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            v[u] = __hip_atomic_load(src + min(u * 64 + lane, last), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         bool done = true;
 #pragma unroll
         for (int u = 0; u < W; ++u) done &= v[u] != kXEmpty;
@@ -276,7 +285,7 @@ struct Geo {
     int CH;   // 16-byte chunks of one folded row (d / 4)
     int NPC;  // 16-byte chunks of one block's down piece for one column tile
     int SW;   // score words per layer
-    int AW;   // activation words per layer: list positions, then misses
+    int AW;   // 64-bit activation words per layer (2F): the list's halves, then the misses
     int miss_base;
     bool has_tile;
     uint32_t tag;
@@ -353,7 +362,7 @@ __device__ __forceinline__ void gather_input(const FusedArgs& P, Smem& sm, const
         for (int u = 0; u < W; ++u) xv[u] = P.x[wave * Q + u * 64 + lane];
     } else {
         uint32_t v[W];
-        wait_x<W>(x_rows(P, g.tag) + (size_t)l * D + wave * Q, lane, P.err, v);
+        wait_x<W>(x_rows(P, g.tag) + (size_t)l * D + wave * Q, Q, lane, P.err, v);
 #pragma unroll
         for (int u = 0; u < W; ++u) xv[u] = __uint_as_float(v[u]);
     }
@@ -565,16 +574,16 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
         // before the workers start streaming the next layer's weights
         if (l > 0 && g.has_tile) {
             const int n = g.kp * g.blk;
-            const uint64_t* row = P.amb + (size_t)l * g.AW;
+            const uint32_t* row = acts_rows(P, g.AW, g.F, l, g.tag);
             // one poll round of up to 32 words per lane (26 at the 7B shape; two rounds of 16
             // gathered 0.3 us later)
             for (int base = 0; base < n; base += 32 * 64) {
-                uint64_t v[32];
-                wait_words<32>(row + base, min(n - base, 32 * 64), g.tag, lane, P.err, v);
+                uint32_t v[32];
+                wait_x<32>(row + base, min(n - base, 32 * 64), lane, P.err, v);
 #pragma unroll
                 for (int u = 0; u < 32; ++u) {
                     const int i = base + u * 64 + lane;
-                    if (i < n) sm.aall[i] = word_value(v[u]);
+                    if (i < n) sm.aall[i] = __uint_as_float(v[u]);
                 }
             }
         }
@@ -667,6 +676,13 @@ __device__ __forceinline__ void control_loop(const FusedArgs P, Smem& sm, const 
                     __hip_atomic_store(x_rows(P, g.tag + 1u) + o, kXEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
+        }
+        {   // empty this layer's list activations of the next launch's half (a slice per
+            // workgroup; every list position of any width lies in the first F words)
+            const int per = (g.F + g.G - 1) / g.G;
+            uint32_t* nxt = acts_rows(P, g.AW, g.F, l, g.tag + 1u);
+            for (int i = g.w * per + lane; i < min((g.w + 1) * per, g.F); i += 64)
+                __hip_atomic_store(nxt + i, kXEmpty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         flag_set(&sm.f_out, l + 1, lane);  // the output store is issued: the workers may queue loads
         LS_STAMP(P, g, l, 9, lane == 0);
@@ -921,7 +937,9 @@ __device__ __forceinline__ void worker_loop(const FusedArgs P, Smem& sm, const G
             gate_up(l, sc, use, bs, qs, as);
 #pragma unroll
             for (int sl = 0; sl < kSlots; ++sl)
-                if ((use & (1u << sl)) && lane == 0) mb_store(P.amb + (size_t)l * g.AW + slot_t[sl], g.tag, as[sl]);
+                if ((use & (1u << sl)) && lane == 0)
+                    __hip_atomic_store(acts_rows(P, g.AW, g.F, l, g.tag) + slot_t[sl], x_bits(as[sl]), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
         }
         LS_STAMP(P, g, l, 13, wave == 3 && lane == 0);
         // the selection: wave 2 the exact top-k of this layer, wave 3 the next layer's list
@@ -1011,8 +1029,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_fused_kernel(FusedArgs P) 
     g.SPW = g.w < g.nb ? (g.nb - 1 - g.w) / g.G + 1 : 0;
     g.CH = D / 4;
     g.SW = (int)fused_score_words_n(g.nb);
-    g.miss_base = g.kp * g.blk;
-    g.AW = (g.kp + g.k) * g.blk;
+    g.miss_base = g.F;  // 64-bit words: the list's two 32-bit halves come first
+    g.AW = 2 * g.F;
     g.NPC = g.blk * KB;
     g.has_tile = g.w < D / kColTile;
     g.tag = P.tag;
