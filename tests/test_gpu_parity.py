@@ -437,15 +437,15 @@ MFMA_CMP = {
     "f16_b64": SMALL["f16_b64"],
     "bf16_reglu": C["mistral_7b_ffn"].with_(n_layers=1, d_model=512, d_ff=2048, block=128, rank=128,
                                             keep_pct=50, act=lsgen.ACT_REGLU),
-    # 256 column tiles: at B = 4 the down projection runs unsplit with 16-column tiles, at B = 8
-    # with 32-column tiles and the list in 2 parts (the two above: 32-column tiles, 8 parts)
+    # 256 column tiles: below B = 8 the down projection runs unsplit with 16-column tiles, at
+    # B = 8 with 32-column tiles and the list in 2 parts (the two above: 32-column tiles, 8 parts)
     "f16_d4096": C["llama2_7b_ffn"].with_(n_layers=1, d_model=4096, d_ff=2048, block=64, rank=128,
                                           keep_pct=30),
 }
 
 
 @pytest.mark.parametrize("name", list(MFMA_CMP))
-@pytest.mark.parametrize("B", [4, 8])
+@pytest.mark.parametrize("B", [4, 6, 8])
 def test_batch_matrix_core_path_matches_vector_path(name, B):
     """The matrix-core kernels (B >= 4) against the vector-ALU kernels on the same union list:
     both accumulate in fp32, the activations enter the matrix cores as hi + lo 16-bit parts
