@@ -115,6 +115,30 @@ def test_fused_speculative_width_does_not_change_results():
         assert y_err(r, res[0]) <= Y_TOL[cfg.dtype]
 
 
+def test_fused_width_changes_between_launches():
+    """Launches alternate between two halves of the bare-word exchange rows, each launch emptying
+    the other half for the next one; widening or narrowing the speculative list between launches
+    must not expose words of an older launch.  Every launch is checked against the per-kernel
+    path on the same token."""
+    cfg = FUSED["llama2_7b_4l"]
+    f, ws = _fused_ffn(cfg)
+    widths = (cfg.k + 6, cfg.k, cfg.k + 3, 0, cfg.k + 1, cfg.k + 6, cfg.k)
+    xs = lsgen.tokens(cfg, 21, len(widths), 1)
+    fused = []
+    for t, kp in enumerate(widths):
+        f.ls_configure(lsffn.LS_CFG_SPEC_BLOCKS, kp)
+        x = dev_f32(xs[t])
+        f.ls_decode_step(x, 1, cfg.k)
+        fused.append(host(x)[0].astype(np.float64) - xs[t, 0])
+    f.ls_ffn_sync()
+    f.ls_configure(lsffn.LS_CFG_DECODE_PATH, 1)
+    for t in range(len(widths)):
+        x = dev_f32(xs[t])
+        f.ls_decode_step(x, 1, cfg.k)
+        ref = host(x)[0].astype(np.float64) - xs[t, 0]
+        assert y_err(fused[t], ref) <= Y_TOL[cfg.dtype], (t, widths[t], y_err(fused[t], ref))
+
+
 def test_fused_unsupported_shape_reports_and_auto_falls_back():
     cfg = C["llama2_7b_ffn"].with_(n_layers=2, d_model=576, d_ff=1200, block=24, rank=192)
     f, _ = make_ffn(cfg)
