@@ -475,16 +475,18 @@ hipError_t launch_gateup_select(const Shape& s, const LayerDev& L, const float* 
 template <ls_dtype T, bool RMS>
 static hipError_t gemv_t(const void* W, int rows, int cols, int G, int rpw, const float* v, int B,
                          float* out, hipStream_t st) {
-    // four rows and eight waves per workgroup once the batch makes the input reads dominate
-    const int R = B >= 4 ? 4 : 1, NW = B >= 4 ? 8 : 4;
+    // four rows and eight waves per workgroup once the batch makes the input reads dominate;
+    // one row per workgroup below, on eight waves at batch 1 (against four: 7B shape 1664 ->
+    // 1681 tokens/s, 13B 1106 -> 1114 on the per-kernel path) and four at B = 2, 3
+    const int R = B >= 4 ? 4 : 1, NW = B >= 4 || B == 1 ? 8 : 4;
     const dim3 grid((unsigned)((rows + R - 1) / R)), blk(64 * NW);
     const uint8_t* w = static_cast<const uint8_t*>(W);
-    // one row per workgroup below B = 4: a row longer than 4 loads per lane is read in one round
+    // a row longer than 4 loads per lane is read in one round of 8
     const bool wide = cols / Wt<T>::V > 64 * NW * 4;
 #define LS_GEMV_U(NB, NR, NWV, U) hipLaunchKernelGGL((gemv_rows_kernel<T, NB, RMS, NR, NWV, U>), grid, blk, 0, st, w, rows, cols, G, rpw, v, out)
 #define LS_GEMV(NB, NR, NWV) LS_GEMV_U(NB, NR, NWV, 4)
     switch (B) {
-        case 1: if (wide) LS_GEMV_U(1, 1, 4, 8); else LS_GEMV(1, 1, 4); break;
+        case 1: if (wide) LS_GEMV_U(1, 1, 8, 8); else LS_GEMV(1, 1, 8); break;
         case 2: if (wide) LS_GEMV_U(2, 1, 4, 8); else LS_GEMV(2, 1, 4); break;
         case 3: if (wide) LS_GEMV_U(3, 1, 4, 8); else LS_GEMV(3, 1, 4); break;
         case 4: LS_GEMV(4, 4, 8); break;
