@@ -84,7 +84,7 @@ __device__ inline int list_end_m(const int32_t* count, int end, int n_blk) {
 constexpr int kWaves = 4;     // gate/up: waves per workgroup
 constexpr int kRowsW = 32 / kWaves;  // gate/up: staged rows loaded by each wave per chunk
 constexpr int kUnroll = 8;    // gate/up: K steps in flight per wave
-constexpr int kUnrollDn = 4;  // down: (entry, K step) items in flight per wave
+constexpr int kUnrollDn = 4;  // down: (entry, K step) items in flight per wave, at most
 constexpr int kWavesDn = 16;  // down: waves per workgroup (one 16-column tile)
 
 // One workgroup per group of 16 neurons (rows r0..r0+15 of one list entry).  The gate and up
@@ -255,7 +255,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kGu
 // the tile count is not; each part's sum goes to part_out[part][token][column] and
 // down_finish_kernel adds the parts in order.  The wave count is blockDim.x / 64 (at most
 // kWavesDn, and at most kWavesDn / NT with NT > 1).
-template <ls_dtype T, int NT>
+template <ls_dtype T, int NT, int KU>
 __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const uint8_t* __restrict__ blocks, size_t block_bytes, const int32_t* __restrict__ slot_table,
     const float* __restrict__ a_buf, int B, int F, int d, int blk, int n_blk,
@@ -263,7 +263,8 @@ __global__ __launch_bounds__(64 * kWavesDn) void down_mfma_kernel(
     const float* __restrict__ x_in, float* __restrict__ x_acc, int splits,
     float* __restrict__ part_out) {
     using S = Split<T>;
-    constexpr int kU = kUnrollDn;  // items in flight per wave
+    static_assert(KU >= 1 && KU <= kUnrollDn, "items in flight per wave");
+    constexpr int kU = KU;
     const int n_tiles = d / (kColTile * NT);
     const int tile = (int)blockIdx.x % n_tiles, sp = (int)blockIdx.x / n_tiles;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -421,13 +422,19 @@ hipError_t launch_down_mfma(const Shape& s, const LayerDev& L, const int32_t* sl
     DownLayout lay = down_layout(s, B);
     if (!part) lay = DownLayout{1, 1, kWavesDn};
     const dim3 grid((unsigned)(s.d / (kColTile * lay.nt) * lay.splits)), blk(64 * lay.waves);
-#define LS_DNM(TT, NT)                                                                                  \
-    hipLaunchKernelGGL((down_mfma_kernel<TT, NT>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, B, \
+    // items in flight per wave: 4 with eight waves per workgroup, else 2 (measured at B = 4 and
+    // 8 on the three shapes: 2 against 4 gave the 13B shape at B = 8 2357 -> 2367 tokens/s, the
+    // Mistral-7B shape at B = 4 1208 -> 1230, the 7B shape at B = 4 2719 -> 2757, and lost 1.5%
+    // on the 7B shape at B = 8, the eight-wave layout; 6 lost everywhere)
+    const int ku = lay.waves == 8 ? 4 : 2;
+#define LS_DNM(TT, NT, KU)                                                                                   \
+    hipLaunchKernelGGL((down_mfma_kernel<TT, NT, KU>), grid, blk, 0, st, L.blocks, bb, slot_table, a_buf, B, \
                        s.F, s.d, s.blk, s.n_blk, idx, count, begin, end, x_in, x_acc, lay.splits, part)
-#define LS_DNT(TT)                          \
-    do {                                    \
-        if (lay.nt == 1) LS_DNM(TT, 1);     \
-        else LS_DNM(TT, 2);                 \
+#define LS_DNT(TT)                                     \
+    do {                                               \
+        if (lay.nt == 1) LS_DNM(TT, 1, 2);             \
+        else if (ku == 4) LS_DNM(TT, 2, 4);            \
+        else LS_DNM(TT, 2, 2);                         \
     } while (0)
     if (s.dtype == LS_F16)
         LS_DNT(LS_F16);
