@@ -671,12 +671,13 @@ hipError_t launch_gateup(const Shape& s, const LayerDev& L, const int32_t* slot_
     return hipErrorInvalidValue;
 }
 
-// Items of loads in flight per wave (an item: 2 vectors of 16 bytes per lane): 2 up to B = 3,
-// where each wave then reaches its first products sooner (with 8: Mistral-7B shape at batch 1
-// 751 against 768 tokens/s, 7B shape 1587 against 1662 on the per-kernel path, 13B shape at
-// B = 2 1192 against 1288; 3 and 4 in between); 8 for batch 1 with zero skip; 4 where the
-// per-token sums (B >= 4) or the zero-skip tests (B >= 2) take the registers.
-constexpr int down_items(int B, bool ZS) { return ZS ? (B == 1 ? 8 : 4) : (B <= 3 ? 2 : 4); }
+// Items of loads in flight per wave (an item: 2 vectors of 16 bytes per lane): 2 up to B = 3
+// (zero skip: at batch 1), where each wave then reaches its first products sooner (with 8:
+// Mistral-7B shape at batch 1 751 against 768 tokens/s, 7B shape 1587 against 1662 on the
+// per-kernel path, 13B shape at B = 2 1192 against 1288, 7B shape with zero skip 1473 against
+// 1578; 3 and 4 in between); 4 where the per-token sums (B >= 4) or the zero-skip tests
+// (B >= 2) take the registers.
+constexpr int down_items(int B, bool ZS) { return (ZS ? B == 1 : B <= 3) ? 2 : 4; }
 
 template <ls_dtype T, int NB, bool ZS, bool AS>
 static void down_launch(const Shape& s, const LayerDev& L, const int32_t* slot_table, const float* a_buf,
